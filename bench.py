@@ -1,0 +1,234 @@
+"""Benchmark of one UBTree draft step on one MI355X.
+
+A step is the whole hot path on one batch of synthetic proposer outputs:
+ubt_topk (softmax statistics + top-K over the vocabulary), ubt_bigram_scores
+(selector scores + normalisation) and ubt_build_tree (beam search, pruning, tree and
+ancestor mask).  Steps rotate over a pool of distinct logit buffers whose total size
+exceeds the 256 MB last-level cache, so every step reads its logits from HBM.  Inputs
+are resident in HBM before the timed region; the steps are captured once into a HIP
+graph and replayed.
+
+Prints one JSON line: trees/s (value), ms per step, the sweep kernel's achieved HBM
+bandwidth against the 8 TB/s peak (roofline), and the fp64 oracle timed on the host
+cores (cpu_baseline).
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "draft trees/sec and µs/step at B=32, V=151936; achieved HBM GB/s vs peak"
+HBM_PEAK_GBPS = 8000.0
+POOL_BYTES = 512 << 20  # pool size that defeats the 256 MB Infinity Cache
+SWEEP_KERNEL = "topk_sweep_kernel"
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "topk_sweep_zipf-v151936-b32_counters.md")
+
+
+def log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def sweep_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in ("topk.hip", "ubt_device.h"):
+        with open(os.path.join(ROOT, "paper_2609_39972_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic() -> dict | None:
+    """HBM bytes per sweep launch from the committed counter summary, if it was taken on
+    the current sweep source."""
+    if not os.path.exists(TRAFFIC_PROFILE):
+        return None
+    txt = open(TRAFFIC_PROFILE).read()
+    m_hash = re.search(r"source hash:\s*`?([0-9a-f]{16})", txt)
+    m_bytes = re.search(r"hbm bytes per launch:\s*([0-9.eE+]+)", txt)
+    if not (m_hash and m_bytes) or m_hash.group(1) != sweep_source_hash():
+        return None
+    return {"bytes": float(m_bytes.group(1))}
+
+
+def cpu_baseline(w, d, min_seconds: float) -> dict:
+    import oracle
+
+    threads = oracle.default_threads()
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        oracle.pipeline(d["logits"], d["phi"], d["psi"], d["gate"], d["anchor"], d["alpha"], d["lam"], w.K, w.W,
+                        w.budget, w.zeta, threads=threads)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= min_seconds:
+            break
+    return {"value": round(reps * w.B / el, 3), "unit": "trees/s", "cores": threads, "kind": "oracle",
+            "sample": f"{reps} full step(s) of the workload ({reps * w.B} trees, {reps * w.rows} logit rows) on "
+                      f"pool buffer 0, fp64 C++ oracle, {threads} threads, {el:.1f} s"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=1000)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", type=int, default=3, help="synthetic workload id (3 = B=32, V=151936 headline)")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0, help="minimum oracle time for cpu_baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--sweep-launches", type=int, default=200, help="individually timed sweep launches")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run a plain device copy of known size (counter calibration) and exit")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); sequences shard across GPUs with no "
+              f"exchange, so the multi-GPU figure is N times this one.", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    import paper_2609_39972_amd as ubt
+    import synth
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    if args.copy_calibration:
+        n = 256 << 20
+        src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "launches": 5}))
+        return 0
+
+    w = synth.WORKLOADS[args.workload]
+    pool = max(1, -(-POOL_BYTES // w.logit_bytes))
+    log(f"workload {w.cfg}: {w.describe()}; pool of {pool} logit buffers ({pool * w.logit_bytes / 1e6:.0f} MB)")
+
+    t0 = time.perf_counter()
+    phi_np, psi_np = synth.tables(w)
+    to_dev = (lambda a: ubt.bf16_tensor_from_bits(a, dev)) if w.feat_dtype == "bf16" else \
+        (lambda a: torch.from_numpy(a).to(dev))
+    to_dev_logits = (lambda a: ubt.bf16_tensor_from_bits(a, dev)) if w.dtype == "bf16" else \
+        (lambda a: torch.from_numpy(a).to(dev))
+    phi, psi = to_dev(phi_np), to_dev(psi_np)
+    bufs = []
+    host0 = None
+    for p in range(pool):
+        d = synth.inputs(w, p, with_tables=False)
+        if p == 0:
+            host0 = dict(d, phi=phi_np, psi=psi_np)
+        step = ubt.DraftStep(w.B, w.gamma, w.V, w.K, w.W, w.budget, phi, psi, to_dev(d["gate"]),
+                             torch.from_numpy(d["anchor"]).to(dev), d["alpha"], d["lam"], w.zeta,
+                             logits_dtype=torch.bfloat16 if w.dtype == "bf16" else torch.float32)
+        bufs.append((to_dev_logits(d["logits"]), step))
+    torch.cuda.synchronize()
+    log(f"inputs resident in HBM ({time.perf_counter() - t0:.1f} s)")
+
+    stream = torch.cuda.Stream(device=dev)
+    torch.cuda.synchronize()
+    with torch.cuda.stream(stream):
+        for s in range(args.warmup):
+            x, st = bufs[s % pool]
+            st.run(x)
+    torch.cuda.synchronize()
+
+    # One graph holds one step per pool buffer.
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=stream):
+        for x, st in bufs:
+            st.run(x)
+    torch.cuda.synchronize()
+    replays = max(1, -(-args.steps // pool))
+    steps = replays * pool
+    for _ in range(2):
+        graph.replay()
+    torch.cuda.synchronize()
+
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    start.record(stream)
+    for _ in range(replays):
+        graph.replay()
+    end.record(stream)
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - t_wall) * 1e3
+    elapsed_ms = start.elapsed_time(end)
+    ms_per_step = elapsed_ms / steps
+    log(f"{steps} steps in {elapsed_ms:.2f} ms (wall {wall_ms:.2f} ms): {ms_per_step * 1e3:.2f} us/step")
+
+    # Per-kernel durations: each launch bracketed by its own events on the launch stream.
+    def timed(fn, n):
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+        with torch.cuda.stream(stream):
+            for j in range(n):
+                evs[j][0].record(stream)
+                fn(j)
+                evs[j][1].record(stream)
+        torch.cuda.synchronize()
+        return float(np.mean([a.elapsed_time(b) for a, b in evs])) * 1e3  # us
+
+    n = args.sweep_launches
+    sweep_us = timed(lambda j: ubt.topk(bufs[j % pool][0], w.K, bufs[j % pool][1].ws, bufs[j % pool][1].cand), n)
+    bigram_us = timed(lambda j: ubt.bigram_scores(bufs[j % pool][1].phi, bufs[j % pool][1].psi,
+                                                  bufs[j % pool][1].gate, bufs[j % pool][1].anchor,
+                                                  bufs[j % pool][1].cand["cand_ids"],
+                                                  bufs[j % pool][1].cand["cand_logit"], bufs[j % pool][1].alpha,
+                                                  bufs[j % pool][1].lam, bufs[j % pool][1].sel), n)
+    tree_us = timed(lambda j: ubt.build_tree(bufs[j % pool][1].anchor, bufs[j % pool][1].cand["cand_ids"],
+                                             bufs[j % pool][1].sel["logq"], w.W, w.budget, w.zeta,
+                                             bufs[j % pool][1].tree), n)
+    sweep_bytes = w.logit_bytes
+    achieved = sweep_bytes / (sweep_us * 1e-6) / 1e9
+    log(f"sweep {sweep_us:.2f} us ({achieved:.0f} GB/s), selector {bigram_us:.2f} us, tree {tree_us:.2f} us")
+
+    traffic = measured_traffic()
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("timing the oracle on the host cores ...")
+        cpu = cpu_baseline(w, host0, args.cpu_seconds)
+        log(f"oracle: {cpu['value']} trees/s on {cpu['cores']} threads")
+
+    value = w.B / (ms_per_step * 1e-3)
+    res = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "trees/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 6),
+        "us_per_step": round(ms_per_step * 1e3, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": w.name, "B": w.B, "L": w.L, "gamma": w.gamma, "V": w.V, "K": w.K, "r": w.r,
+                   "budget": w.budget, "W": w.W, "logits": f"{w.dtype} {w.logits}", "features": w.feat_dtype,
+                   "pool_buffers": pool, "graph": f"{pool} steps per HIP graph, replayed {replays} times"},
+        "kernels_us": {"topk_sweep": round(sweep_us, 3), "bigram": round(bigram_us, 3), "build_tree": round(tree_us, 3)},
+        "roofline": {"bound": "hbm", "kernel": SWEEP_KERNEL, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                     "traffic": None if traffic is None else traffic["bytes"],
+                     "algorithmic_bytes_per_launch": sweep_bytes, "source_hash": sweep_source_hash()},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(res), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

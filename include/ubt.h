@@ -1,0 +1,191 @@
+/* ubt.h -- C ABI of libubt.so: UBTree draft-tree construction on AMD Instinct MI355X
+ * (gfx950).  UBTree is arXiv 2609.39972; section, equation and algorithm names below
+ * refer to that paper.
+ *
+ * One draft step turns the proposer logits of B independent sequences into B draft
+ * trees.  Sequence b carries gamma = L - 1 logit rows (draft depths 1..gamma; the block
+ * of L positions includes the anchor x_0).  The calls run in this order:
+ *
+ *   ubt_topk           per row: softmax statistics and the top-K candidate set C_i
+ *   ubt_bigram_scores  per (b, depth): selector scores Delta_i and normalised log q^bi
+ *   ubt_build_tree     per sequence: beam search + global pruning -> tree and mask
+ *   ubt_tree_mask      (optional) the ancestor mask of any parent-pointer tree
+ *
+ * Conventions shared by every call:
+ *   - Every pointer is device memory unless marked [host].  The caller owns every
+ *     buffer; the library never allocates or frees device memory.
+ *   - Calls are asynchronous on `stream` (a hipStream_t; 0 = the null stream).  The
+ *     library never synchronises and keeps no mutable global state, so calls may be
+ *     issued from several host threads and captured into HIP graphs.
+ *   - Every argument check runs on the host before any launch.  On an error status
+ *     nothing is launched and no output is written.  Values inside device buffers
+ *     (logits, ids, scores) are not checked; the documented value ranges are the
+ *     caller's responsibility, and values outside them give unspecified results but
+ *     never out-of-bounds accesses.
+ *   - Arrays are row-major and contiguous unless a stride is given.  Outputs sized
+ *     [B, gamma, K] etc. are indexed [b][i][k] with i = 0..gamma-1 the position (draft
+ *     depth i+1).
+ */
+#ifndef UBT_H
+#define UBT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define UBT_ABI_VERSION 1
+
+/* Limits checked by the host-side validation. */
+#define UBT_MAX_K 64          /* candidates per position */
+#define UBT_MAX_GAMMA 64      /* logit rows (draft depths) per sequence */
+#define UBT_MAX_BUDGET 255    /* non-root nodes per tree; N = budget + 1 <= 256 slots */
+#define UBT_MAX_WIDTH 255     /* search width W */
+#define UBT_MAX_EXPANSION 4096 /* W * K extensions per depth, and gamma * W supertree nodes */
+#define UBT_MAX_RANK 512      /* selector rank r (a multiple of 16) */
+
+typedef enum ubt_dtype { UBT_F32 = 0, UBT_BF16 = 1 } ubt_dtype_t;
+
+typedef enum ubt_status {
+  UBT_OK = 0,
+  UBT_ERR_NULL = 1,        /* a required pointer is NULL */
+  UBT_ERR_SHAPE = 2,       /* a size, stride or limit is violated */
+  UBT_ERR_VALUE = 3,       /* a scalar argument is out of range (zeta > 0, alpha <= 0, ...) */
+  UBT_ERR_UNSUPPORTED = 4, /* a valid combination this build does not handle */
+  UBT_ERR_WORKSPACE = 5,   /* workspace missing, too small or misaligned */
+  UBT_ERR_HIP = 6          /* a HIP launch failed; see ubt_last_hip_error() */
+} ubt_status_t;
+
+/* Human-readable name of a status code (static storage). */
+const char* ubt_status_str(ubt_status_t status);
+
+/* UBT_ABI_VERSION of the loaded library. */
+int ubt_abi_version(void);
+
+/* hipError_t of the last launch that returned UBT_ERR_HIP on the calling host thread. */
+int ubt_last_hip_error(void);
+
+/* ------------------------------------------------------------------------------------
+ * ubt_topk -- softmax statistics and candidate sets.
+ * Method / Unigram Proposer, Eq. (ubtree-unigram): q_i = softmax(u_i) over the whole
+ * vocabulary; "Candidate Sets": C_i = the K tokens of largest q_i.  Softmax is
+ * increasing, so C_i is ranked on the logits themselves.
+ *
+ * logits   : u[b][i][v] at element offset b*stride_b + i*stride_i + v, dtype `dt`
+ *            (UBT_BF16 or UBT_F32); values finite or -inf, at least one finite value
+ *            per row; NaN gives unspecified results.  stride_i >= V, stride_b >=
+ *            gamma*stride_i.  Rows whose start is 16-byte aligned take the fast path.
+ * B, gamma : sequences and rows per sequence, 1 <= gamma <= UBT_MAX_GAMMA, B >= 1.
+ * V        : vocabulary size, K <= V < 2^31.
+ * K        : candidates per row, 1 <= K <= UBT_MAX_K.
+ * cand_ids : int32 [B, gamma, K]   token ids ordered by (logit desc, id asc); -0 == +0.
+ * cand_logit : float [B, gamma, K] the candidates' logits (exact for both dtypes).
+ * cand_logprob : float [B, gamma, K] log q_i(candidate) = logit - lse; may be NULL.
+ * lse      : float [B, gamma]      log sum_v exp(u_v) (natural log); may be NULL.
+ * workspace: device scratch of at least ubt_topk_workspace_bytes(...) bytes, 256-byte
+ *            aligned.  Its first 4*B*gamma bytes are counters that must be zero before
+ *            the first call that uses the buffer (hipMemset once after allocation);
+ *            every call leaves them zero again.  Calls that may overlap in time need
+ *            separate workspaces.
+ * ------------------------------------------------------------------------------------ */
+size_t ubt_topk_workspace_bytes(int B, int gamma, int64_t V, int K, ubt_dtype_t dt);
+
+ubt_status_t ubt_topk(const void* logits, ubt_dtype_t dt, int B, int gamma, int64_t V,
+                      int64_t stride_b, int64_t stride_i, int K, int32_t* cand_ids,
+                      float* cand_logit, float* cand_logprob, float* lse, void* workspace,
+                      size_t workspace_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------------------
+ * ubt_bigram_scores -- selector scores and normalised transition log-probabilities.
+ * Background, Eq. (dflash2-selector): delta_i(a, b) = (P(h_i) (.) phi(a))^T psi(b).
+ * Method / Parallel Computation, Eq. (ubtree-edge-matrix): Delta_i = Phi_{i-1}
+ * diag(P(h_i)) Psi_i^T over all pairs of C_{i-1} x C_i, with C_0 = {x_0}.
+ * Method / Depth Calibration, Eq. (ubtree-depth): s_i = alpha_i u_i(b) + lambda_i delta_i.
+ * Appendix A / Path Scores, Eq. (ubtree-path): log q_i^bi(b|a) = s_i(a,b) -
+ * log sum_{v in C_i} exp s_i(a, v).
+ *
+ * phi_tab, psi_tab : [V, r] vocabulary-wide codebook tables (Eq. ubtree-codebook,
+ *            precomputed), dtype feat_dt.  gate : [B, gamma, r] = P(h_i), dtype feat_dt.
+ *            r % 16 == 0, 16 <= r <= UBT_MAX_RANK.
+ * anchor   : int32 [B] anchor tokens x_0, each in [0, V).
+ * cand_ids, cand_logit : outputs of ubt_topk ([B, gamma, K]).
+ * alpha, lambda : [host] float [gamma], finite and > 0.
+ * delta    : float [B, gamma, K, K] indexed [b][i][a][c] (a = predecessor rank, c =
+ *            successor rank); may be NULL.  logq : float [B, gamma, K, K], same
+ *            indexing, every entry <= 0.  At i = 0 the predecessor is the anchor: row
+ *            a = 0 holds the scores; rows 1..K-1 are written as 0.
+ * bf16 features: each product P(h)_k phi_k(a) psi_k(b) is formed exactly in fp32 and
+ * summed in fp32 (matrix cores); fp32 features: fp32 fused multiply-adds.
+ * ------------------------------------------------------------------------------------ */
+ubt_status_t ubt_bigram_scores(const void* phi_tab, const void* psi_tab, const void* gate,
+                               ubt_dtype_t feat_dt, int64_t V, int r, const int32_t* anchor,
+                               const int32_t* cand_ids, const float* cand_logit,
+                               const float* alpha, const float* lambda, int B, int gamma, int K,
+                               float* delta, float* logq, hipStream_t stream);
+
+/* ------------------------------------------------------------------------------------
+ * ubt_build_tree -- Algorithm 1 (Appendix A): depth-wise expansion, Eq.
+ * (ubtree-frontier), F_d = Top_W(E_d) over all extensions of F_{d-1}; depth bonus, Eq.
+ * (ubtree-depth-bonus), l_zeta(y_{1:d}) = l_zeta(y_{1:d-1}) + log q_d^bi + zeta; global
+ * pruning, Eq. (ubtree-pruning), T = {root} + Top_budget(union of F_d).
+ *
+ * Ties: within a depth, score desc, then the parent's position in F_{d-1}, then the
+ * candidate rank; across depths, score desc, then depth asc, then that order.  Scores
+ * are accumulated in fp32 as (l(parent) + logq) + zeta.
+ *
+ * anchor, cand_ids : as for ubt_bigram_scores.  logq : [B, gamma, K, K] from
+ *            ubt_bigram_scores; entries must be <= 0 (any finite values <= 0 work).
+ * W        : search width, 1 <= W <= UBT_MAX_WIDTH, W*K <= UBT_MAX_EXPANSION and
+ *            gamma*W <= UBT_MAX_EXPANSION.
+ * budget   : non-root node budget (the paper's B), 1 <= budget <= UBT_MAX_BUDGET;
+ *            N = budget + 1 tree slots.
+ * zeta     : depth bonus, finite and <= 0 (the paper uses 0).
+ * n_nodes  : int32 [B] = 1 + min(budget, |union of F_d|).
+ * token, parent, depth, cand_rank : int32 [B, N]; score : float [B, N].  Slot 0 is the
+ *            root (token = anchor, parent -1, depth 0, cand_rank -1, score 0); slots
+ *            1..n_nodes-1 hold the selected nodes in pruning order, which is
+ *            topological (parent[n] < n).  Unused slots: -1 and score -inf.
+ * mask     : uint32 [B, N, ceil(N/32)] or NULL.  Bit m%32 of word m/32 of row n is set
+ *            iff slot m is slot n or an ancestor of it; rows >= n_nodes are zero.
+ * dbg      : [host] pointer to a struct of device arrays, or NULL.  When given, receives
+ *            the supertree: f_count int32 [B, gamma] = |F_d|; f_parent_slot (the parent's
+ *            position in F_{d-1}), f_cand (candidate rank) int32 [B, gamma, W] and
+ *            f_score float [B, gamma, W], in F_d order; unused entries -1 / -inf.
+ * ------------------------------------------------------------------------------------ */
+typedef struct ubt_supertree {
+  int32_t* f_count;
+  int32_t* f_parent_slot;
+  int32_t* f_cand;
+  float* f_score;
+} ubt_supertree_t;
+
+ubt_status_t ubt_build_tree(const int32_t* anchor, const int32_t* cand_ids, const float* logq,
+                            int B, int gamma, int K, int W, int budget, float zeta,
+                            int32_t* n_nodes, int32_t* token, int32_t* parent, int32_t* depth,
+                            int32_t* cand_rank, float* score, uint32_t* mask,
+                            const ubt_supertree_t* dbg, hipStream_t stream);
+
+/* ------------------------------------------------------------------------------------
+ * ubt_tree_mask -- the ancestor ("tree attention") mask of a tree given by parent
+ * pointers.  Appendix A / Verification via Tree-attention: each node is verified under
+ * its own prefix, i.e. it attends to itself and its ancestors.
+ *
+ * parent   : int32 [B, N] with parent[0] = -1 and 0 <= parent[n] < n for
+ *            1 <= n < n_nodes[b]; entries at n >= n_nodes[b] are ignored.
+ * n_nodes  : int32 [B], values in [0, N].
+ * N        : slots per tree, 1 <= N <= UBT_MAX_BUDGET + 1.
+ * mask     : uint32 [B, N, ceil(N/32)], same layout as ubt_build_tree's.  A parent
+ *            pointer outside [0, n) ends that row's walk (the row is then unspecified).
+ * ------------------------------------------------------------------------------------ */
+ubt_status_t ubt_tree_mask(const int32_t* parent, const int32_t* n_nodes, int B, int N,
+                           uint32_t* mask, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* UBT_H */

@@ -1,0 +1,273 @@
+"""UBTree draft-tree construction on AMD Instinct MI355X (gfx950).
+
+A thin binding over the C ABI of ``libubt.so`` (``include/ubt.h``).  Every step of the
+path runs in the library's HIP kernels; this module only allocates outputs with torch,
+passes raw device pointers and the current HIP stream, and turns status codes into
+exceptions.  It fails loudly when the library is missing: there is no fallback.
+
+Calls, in pipeline order (the paper's section and equation names in brackets):
+
+* :func:`topk` -- softmax statistics and top-K candidates per row [Method / Unigram
+  Proposer, Eq. ubtree-unigram; Candidate Sets];
+* :func:`bigram_scores` -- selector scores and normalised transition log-probs
+  [Eq. dflash2-selector, ubtree-depth, ubtree-edge-matrix, ubtree-path];
+* :func:`build_tree` -- beam search with global pruning and the ancestor mask
+  [Appendix A, Algorithm 1];
+* :func:`tree_mask` -- the ancestor mask of any parent-pointer tree.
+
+:class:`DraftStep` preallocates everything for one workload shape and runs the three
+calls back to back on one stream (graph-capturable).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libubt.so")
+
+UBT_F32, UBT_BF16 = 0, 1
+STATUS = {0: "UBT_OK", 1: "UBT_ERR_NULL", 2: "UBT_ERR_SHAPE", 3: "UBT_ERR_VALUE", 4: "UBT_ERR_UNSUPPORTED",
+          5: "UBT_ERR_WORKSPACE", 6: "UBT_ERR_HIP"}
+
+# Every symbol include/ubt.h declares.
+EXPORTS = ("ubt_status_str", "ubt_abi_version", "ubt_last_hip_error", "ubt_topk_workspace_bytes", "ubt_topk",
+           "ubt_bigram_scores", "ubt_build_tree", "ubt_tree_mask")
+
+_p = ctypes.c_void_p
+_i32 = ctypes.c_int
+_i64 = ctypes.c_int64
+_f32 = ctypes.c_float
+_lib = None
+
+
+class UbtError(RuntimeError):
+    def __init__(self, call: str, status: int):
+        self.status = status
+        super().__init__(f"{call} failed: {STATUS.get(status, status)}")
+
+
+class _Supertree(ctypes.Structure):
+    _fields_ = [("f_count", _p), ("f_parent_slot", _p), ("f_cand", _p), ("f_score", _p)]
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded ``libubt.so``.  Raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() (hipcc, gfx950)")
+        L = ctypes.CDLL(LIB_PATH)
+        L.ubt_status_str.argtypes = [_i32]
+        L.ubt_status_str.restype = ctypes.c_char_p
+        L.ubt_abi_version.restype = _i32
+        L.ubt_last_hip_error.restype = _i32
+        L.ubt_topk_workspace_bytes.argtypes = [_i32, _i32, _i64, _i32, _i32]
+        L.ubt_topk_workspace_bytes.restype = ctypes.c_size_t
+        L.ubt_topk.argtypes = [_p, _i32, _i32, _i32, _i64, _i64, _i64, _i32, _p, _p, _p, _p, _p, ctypes.c_size_t, _p]
+        L.ubt_bigram_scores.argtypes = [_p, _p, _p, _i32, _i64, _i32, _p, _p, _p, _p, _p, _i32, _i32, _i32, _p, _p,
+                                        _p]
+        L.ubt_build_tree.argtypes = [_p, _p, _p, _i32, _i32, _i32, _i32, _i32, _f32, _p, _p, _p, _p, _p, _p, _p,
+                                     ctypes.POINTER(_Supertree), _p]
+        L.ubt_tree_mask.argtypes = [_p, _p, _i32, _i32, _p, _p]
+        for f in (L.ubt_topk, L.ubt_bigram_scores, L.ubt_build_tree, L.ubt_tree_mask):
+            f.restype = _i32
+        _lib = L
+    return _lib
+
+
+def _check(call: str, status: int) -> None:
+    if status != 0:
+        raise UbtError(call, status)
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return UBT_BF16
+    if t.dtype == torch.float32:
+        return UBT_F32
+    raise TypeError(f"unsupported dtype {t.dtype}: use torch.bfloat16 or torch.float32")
+
+
+def _ptr(t: torch.Tensor | None):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _need_gpu(*ts: torch.Tensor) -> None:
+    for t in ts:
+        if t is not None and not t.is_cuda:
+            raise ValueError("all tensors must live on the GPU")
+
+
+def _contig(t: torch.Tensor, name: str) -> torch.Tensor:
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t
+
+
+class TopkWorkspace:
+    """Device scratch for :func:`topk` (zeroed once; every call leaves it zeroed)."""
+
+    def __init__(self, B: int, gamma: int, V: int, K: int, dtype: torch.dtype, device="cuda"):
+        code = UBT_BF16 if dtype == torch.bfloat16 else UBT_F32
+        self.nbytes = int(lib().ubt_topk_workspace_bytes(B, gamma, V, K, code))
+        if self.nbytes == 0:
+            raise ValueError("invalid top-K shape")
+        self._buf = torch.zeros(self.nbytes + 256, dtype=torch.uint8, device=device)
+        off = (-self._buf.data_ptr()) % 256
+        self.tensor = self._buf[off:off + self.nbytes]
+        self.shape = (B, gamma, V, K, code)
+
+
+def topk(logits: torch.Tensor, K: int, workspace: TopkWorkspace | None = None, out: dict | None = None,
+         with_logprob: bool = True, stream=None) -> dict:
+    """Top-K candidates and softmax statistics of ``logits [B, gamma, V]`` (any strides with
+    unit stride along V; e.g. ``u[:, 1:, :]`` of a ``[B, L, V]`` block)."""
+    _need_gpu(logits)
+    if logits.dim() != 3 or logits.stride(2) != 1:
+        raise ValueError("logits must be [B, gamma, V] with unit stride along V")
+    B, gamma, V = logits.shape
+    code = _dtype_code(logits)
+    dev = logits.device
+    if workspace is None:
+        workspace = TopkWorkspace(B, gamma, V, K, logits.dtype, dev)
+    if out is None:
+        out = dict(cand_ids=torch.empty(B, gamma, K, dtype=torch.int32, device=dev),
+                   cand_logit=torch.empty(B, gamma, K, dtype=torch.float32, device=dev),
+                   cand_logprob=torch.empty(B, gamma, K, dtype=torch.float32, device=dev) if with_logprob else None,
+                   lse=torch.empty(B, gamma, dtype=torch.float32, device=dev))
+    st = lib().ubt_topk(_ptr(logits), code, B, gamma, V, logits.stride(0), logits.stride(1), K,
+                        _ptr(out["cand_ids"]), _ptr(out["cand_logit"]), _ptr(out.get("cand_logprob")),
+                        _ptr(out.get("lse")), _ptr(workspace.tensor), workspace.nbytes, _stream(stream))
+    _check("ubt_topk", st)
+    return out
+
+
+def _host_f32(x, n: int) -> ctypes.Array:
+    vals = [float(v) for v in (x.tolist() if hasattr(x, "tolist") else x)]
+    if len(vals) != n:
+        raise ValueError(f"expected {n} values, got {len(vals)}")
+    return (ctypes.c_float * n)(*vals)
+
+
+def bigram_scores(phi: torch.Tensor, psi: torch.Tensor, gate: torch.Tensor, anchor: torch.Tensor,
+                  cand_ids: torch.Tensor, cand_logit: torch.Tensor, alpha, lam, out: dict | None = None,
+                  with_delta: bool = True, stream=None) -> dict:
+    """Selector scores ``delta`` and ``logq`` ``[B, gamma, K, K]``; ``alpha``/``lam`` are
+    per-depth host values (sequences or CPU tensors)."""
+    _need_gpu(phi, psi, gate, anchor, cand_ids, cand_logit)
+    for n, t in (("phi", phi), ("psi", psi), ("gate", gate), ("anchor", anchor), ("cand_ids", cand_ids),
+                 ("cand_logit", cand_logit)):
+        _contig(t, n)
+    if not (phi.dtype == psi.dtype == gate.dtype):
+        raise TypeError("phi, psi and gate must share one dtype")
+    V, r = phi.shape
+    B, gamma, K = cand_ids.shape
+    dev = cand_ids.device
+    if out is None:
+        out = dict(delta=torch.empty(B, gamma, K, K, dtype=torch.float32, device=dev) if with_delta else None,
+                   logq=torch.empty(B, gamma, K, K, dtype=torch.float32, device=dev))
+    a, l = _host_f32(alpha, gamma), _host_f32(lam, gamma)
+    st = lib().ubt_bigram_scores(_ptr(phi), _ptr(psi), _ptr(gate), _dtype_code(phi), V, r, _ptr(anchor),
+                                 _ptr(cand_ids), _ptr(cand_logit), a, l, B, gamma, K, _ptr(out.get("delta")),
+                                 _ptr(out["logq"]), _stream(stream))
+    _check("ubt_bigram_scores", st)
+    return out
+
+
+def tree_outputs(B: int, gamma: int, W: int, budget: int, device="cuda", with_mask: bool = True,
+                 debug: bool = False) -> dict:
+    N = budget + 1
+    words = (N + 31) // 32
+    i32 = dict(dtype=torch.int32, device=device)
+    out = dict(n_nodes=torch.empty(B, **i32), token=torch.empty(B, N, **i32), parent=torch.empty(B, N, **i32),
+               depth=torch.empty(B, N, **i32), cand_rank=torch.empty(B, N, **i32),
+               score=torch.empty(B, N, dtype=torch.float32, device=device),
+               mask=torch.empty(B, N, words, **i32) if with_mask else None)
+    if debug:
+        out.update(f_count=torch.empty(B, gamma, **i32), f_parent=torch.empty(B, gamma, W, **i32),
+                   f_cand=torch.empty(B, gamma, W, **i32),
+                   f_score=torch.empty(B, gamma, W, dtype=torch.float32, device=device))
+    return out
+
+
+def build_tree(anchor: torch.Tensor, cand_ids: torch.Tensor, logq: torch.Tensor, W: int, budget: int,
+               zeta: float = 0.0, out: dict | None = None, with_mask: bool = True, debug: bool = False,
+               stream=None) -> dict:
+    """Algorithm 1 per sequence: tree slots ``[B, budget+1]``, the packed ancestor mask
+    (``int32`` view of the uint32 words) and, with ``debug``, the supertree F_d."""
+    _need_gpu(anchor, cand_ids, logq)
+    for n, t in (("anchor", anchor), ("cand_ids", cand_ids), ("logq", logq)):
+        _contig(t, n)
+    B, gamma, K = cand_ids.shape
+    if out is None:
+        out = tree_outputs(B, gamma, W, budget, cand_ids.device, with_mask, debug)
+    dbg = None
+    if "f_count" in out:
+        dbg = ctypes.byref(_Supertree(_ptr(out["f_count"]), _ptr(out["f_parent"]), _ptr(out["f_cand"]),
+                                      _ptr(out["f_score"])))
+    st = lib().ubt_build_tree(_ptr(anchor), _ptr(cand_ids), _ptr(logq), B, gamma, K, W, budget, float(zeta),
+                              _ptr(out["n_nodes"]), _ptr(out["token"]), _ptr(out["parent"]), _ptr(out["depth"]),
+                              _ptr(out["cand_rank"]), _ptr(out["score"]), _ptr(out.get("mask")), dbg,
+                              _stream(stream))
+    _check("ubt_build_tree", st)
+    return out
+
+
+def tree_mask(parent: torch.Tensor, n_nodes: torch.Tensor, out: torch.Tensor | None = None,
+              stream=None) -> torch.Tensor:
+    """Packed ancestor mask ``[B, N, ceil(N/32)]`` (int32 view of uint32 words)."""
+    _need_gpu(parent, n_nodes)
+    _contig(parent, "parent")
+    B, N = parent.shape
+    if out is None:
+        out = torch.empty(B, N, (N + 31) // 32, dtype=torch.int32, device=parent.device)
+    _check("ubt_tree_mask", lib().ubt_tree_mask(_ptr(parent), _ptr(n_nodes), B, N, _ptr(out), _stream(stream)))
+    return out
+
+
+class DraftStep:
+    """One draft step (top-K -> selector -> tree + mask) with every buffer preallocated.
+
+    ``run(logits)`` issues the three library calls on the current stream and allocates
+    nothing, so it can be captured into a HIP graph."""
+
+    def __init__(self, B: int, gamma: int, V: int, K: int, W: int, budget: int, phi: torch.Tensor,
+                 psi: torch.Tensor, gate: torch.Tensor, anchor: torch.Tensor, alpha, lam, zeta: float = 0.0,
+                 logits_dtype: torch.dtype = torch.bfloat16, with_delta: bool = False, debug: bool = False):
+        dev = phi.device
+        self.shape = (B, gamma, V, K, W, budget)
+        self.phi, self.psi, self.gate, self.anchor = phi, psi, gate, anchor
+        self.alpha, self.lam, self.zeta = alpha, lam, zeta
+        self.W, self.budget, self.K = W, budget, K
+        self.ws = TopkWorkspace(B, gamma, V, K, logits_dtype, dev)
+        f32 = dict(dtype=torch.float32, device=dev)
+        self.cand = dict(cand_ids=torch.empty(B, gamma, K, dtype=torch.int32, device=dev),
+                         cand_logit=torch.empty(B, gamma, K, **f32), cand_logprob=torch.empty(B, gamma, K, **f32),
+                         lse=torch.empty(B, gamma, **f32))
+        self.sel = dict(delta=torch.empty(B, gamma, K, K, **f32) if with_delta else None,
+                        logq=torch.empty(B, gamma, K, K, **f32))
+        self.tree = tree_outputs(B, gamma, W, budget, dev, True, debug)
+
+    def run(self, logits: torch.Tensor, stream=None) -> dict:
+        topk(logits, self.K, self.ws, self.cand, stream=stream)
+        bigram_scores(self.phi, self.psi, self.gate, self.anchor, self.cand["cand_ids"], self.cand["cand_logit"],
+                      self.alpha, self.lam, self.sel, stream=stream)
+        build_tree(self.anchor, self.cand["cand_ids"], self.sel["logq"], self.W, self.budget, self.zeta, self.tree,
+                   stream=stream)
+        return {**self.cand, **self.sel, **self.tree}
+
+
+def bf16_tensor_from_bits(bits, device="cuda") -> torch.Tensor:
+    """A bf16 tensor holding the given uint16 bit patterns (numpy array)."""
+    import numpy as np
+
+    a = np.ascontiguousarray(bits, dtype=np.uint16).view(np.int16)
+    return torch.from_numpy(a).to(device).view(torch.bfloat16)

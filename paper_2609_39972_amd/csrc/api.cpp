@@ -1,0 +1,138 @@
+// Host side of libubt.so: argument validation and kernel launches for the C ABI
+// declared in include/ubt.h.  Every check runs before any launch; on an error status
+// nothing is launched.
+#include <math.h>
+#include <stdint.h>
+
+#include "ubt.h"
+#include "ubt_launch.h"
+
+namespace {
+
+thread_local int g_last_hip_error = 0;
+
+ubt_status_t hip_status(hipError_t e) {
+  if (e == hipSuccess) return UBT_OK;
+  g_last_hip_error = static_cast<int>(e);
+  return UBT_ERR_HIP;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+bool valid_dtype(ubt_dtype_t dt) { return dt == UBT_F32 || dt == UBT_BF16; }
+
+}  // namespace
+
+extern "C" {
+
+const char* ubt_status_str(ubt_status_t s) {
+  switch (s) {
+    case UBT_OK: return "UBT_OK";
+    case UBT_ERR_NULL: return "UBT_ERR_NULL";
+    case UBT_ERR_SHAPE: return "UBT_ERR_SHAPE";
+    case UBT_ERR_VALUE: return "UBT_ERR_VALUE";
+    case UBT_ERR_UNSUPPORTED: return "UBT_ERR_UNSUPPORTED";
+    case UBT_ERR_WORKSPACE: return "UBT_ERR_WORKSPACE";
+    case UBT_ERR_HIP: return "UBT_ERR_HIP";
+  }
+  return "UBT_ERR_UNKNOWN";
+}
+
+int ubt_abi_version(void) { return UBT_ABI_VERSION; }
+
+int ubt_last_hip_error(void) { return g_last_hip_error; }
+
+size_t ubt_topk_workspace_bytes(int B, int gamma, int64_t V, int K, ubt_dtype_t dt) {
+  if (B < 1 || gamma < 1 || gamma > UBT_MAX_GAMMA || K < 1 || K > UBT_MAX_K || V < K || V >= (int64_t(1) << 31) ||
+      !valid_dtype(dt))
+    return 0;
+  return ubt::topk_plan(B, gamma, V, K, static_cast<int>(dt)).bytes;
+}
+
+ubt_status_t ubt_topk(const void* logits, ubt_dtype_t dt, int B, int gamma, int64_t V, int64_t stride_b,
+                      int64_t stride_i, int K, int32_t* cand_ids, float* cand_logit, float* cand_logprob, float* lse,
+                      void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (!logits || !cand_ids || !cand_logit) return UBT_ERR_NULL;
+  if (!valid_dtype(dt)) return UBT_ERR_VALUE;
+  if (B < 1 || gamma < 1 || gamma > UBT_MAX_GAMMA || K < 1 || K > UBT_MAX_K || V < K || V >= (int64_t(1) << 31))
+    return UBT_ERR_SHAPE;
+  if (stride_i < V || stride_b < static_cast<int64_t>(gamma) * stride_i) return UBT_ERR_SHAPE;
+  if (static_cast<int64_t>(B) * gamma > (int64_t(1) << 31) / 8) return UBT_ERR_SHAPE;
+  const ubt::TopkPlan plan = ubt::topk_plan(B, gamma, V, K, static_cast<int>(dt));
+  if (!workspace || workspace_bytes < plan.bytes || (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
+    return UBT_ERR_WORKSPACE;
+  const int64_t es = dt == UBT_BF16 ? 2 : 4;
+  const bool aligned = aligned16(logits) && (stride_b * es) % 16 == 0 && (stride_i * es) % 16 == 0;
+  return hip_status(ubt::launch_topk(logits, static_cast<int>(dt), aligned, B, gamma, V, stride_b, stride_i, K, plan,
+                                     workspace, cand_ids, cand_logit, cand_logprob, lse, stream));
+}
+
+ubt_status_t ubt_bigram_scores(const void* phi_tab, const void* psi_tab, const void* gate, ubt_dtype_t feat_dt,
+                               int64_t V, int r, const int32_t* anchor, const int32_t* cand_ids,
+                               const float* cand_logit, const float* alpha, const float* lambda, int B, int gamma,
+                               int K, float* delta, float* logq, hipStream_t stream) {
+  if (!phi_tab || !psi_tab || !gate || !anchor || !cand_ids || !cand_logit || !alpha || !lambda || !logq)
+    return UBT_ERR_NULL;
+  if (!valid_dtype(feat_dt)) return UBT_ERR_VALUE;
+  if (B < 1 || gamma < 1 || gamma > UBT_MAX_GAMMA || K < 1 || K > UBT_MAX_K || V < K || V >= (int64_t(1) << 31))
+    return UBT_ERR_SHAPE;
+  if (r < 16 || r > UBT_MAX_RANK || r % 16 != 0) return UBT_ERR_SHAPE;
+  for (int i = 0; i < gamma; ++i)
+    if (!(isfinite(alpha[i]) && alpha[i] > 0.f && isfinite(lambda[i]) && lambda[i] > 0.f)) return UBT_ERR_VALUE;
+  if (feat_dt == UBT_BF16 && !(aligned16(phi_tab) && aligned16(psi_tab) && aligned16(gate)))
+    return UBT_ERR_UNSUPPORTED;
+  ubt::Scales sc{};
+  for (int i = 0; i < gamma; ++i) {
+    sc.alpha[i] = alpha[i];
+    sc.lambda[i] = lambda[i];
+  }
+  return hip_status(ubt::launch_bigram(phi_tab, psi_tab, gate, static_cast<int>(feat_dt), V, r, anchor, cand_ids,
+                                       cand_logit, sc, B, gamma, K, delta, logq, stream));
+}
+
+ubt_status_t ubt_build_tree(const int32_t* anchor, const int32_t* cand_ids, const float* logq, int B, int gamma, int K,
+                            int W, int budget, float zeta, int32_t* n_nodes, int32_t* token, int32_t* parent,
+                            int32_t* depth, int32_t* cand_rank, float* score, uint32_t* mask,
+                            const ubt_supertree_t* dbg, hipStream_t stream) {
+  if (!anchor || !cand_ids || !logq || !n_nodes || !token || !parent || !depth || !cand_rank || !score)
+    return UBT_ERR_NULL;
+  if (dbg && !(dbg->f_count && dbg->f_parent_slot && dbg->f_cand && dbg->f_score)) return UBT_ERR_NULL;
+  if (B < 1 || gamma < 1 || gamma > UBT_MAX_GAMMA || K < 1 || K > UBT_MAX_K) return UBT_ERR_SHAPE;
+  if (W < 1 || W > UBT_MAX_WIDTH || budget < 1 || budget > UBT_MAX_BUDGET) return UBT_ERR_SHAPE;
+  if (static_cast<int64_t>(W) * K > UBT_MAX_EXPANSION || static_cast<int64_t>(gamma) * W > UBT_MAX_EXPANSION)
+    return UBT_ERR_UNSUPPORTED;
+  if (!(isfinite(zeta) && zeta <= 0.f)) return UBT_ERR_VALUE;
+  ubt::TreeArgs a{};
+  a.anchor = anchor;
+  a.cand_ids = cand_ids;
+  a.logq = logq;
+  a.B = B;
+  a.gamma = gamma;
+  a.K = K;
+  a.W = W;
+  a.budget = budget;
+  a.zeta = zeta;
+  a.n_nodes = n_nodes;
+  a.token = token;
+  a.parent = parent;
+  a.depth = depth;
+  a.cand_rank = cand_rank;
+  a.score = score;
+  a.mask = mask;
+  if (dbg) {
+    a.f_count = dbg->f_count;
+    a.f_parent = dbg->f_parent_slot;
+    a.f_cand = dbg->f_cand;
+    a.f_score = dbg->f_score;
+  }
+  return hip_status(ubt::launch_build_tree(a, stream));
+}
+
+ubt_status_t ubt_tree_mask(const int32_t* parent, const int32_t* n_nodes, int B, int N, uint32_t* mask,
+                           hipStream_t stream) {
+  if (!parent || !n_nodes || !mask) return UBT_ERR_NULL;
+  if (B < 1 || N < 1 || N > UBT_MAX_BUDGET + 1) return UBT_ERR_SHAPE;
+  return hip_status(ubt::launch_tree_mask(parent, n_nodes, B, N, mask, stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,403 @@
+// Draft-tree construction from precomputed transition scores, and the ancestor mask.
+//
+// Appendix A, Algorithm 1: F_0 = {root}; for d = 1..gamma, E_d = F_{d-1} x C_d with
+// l(y_{1:d}) = l(y_{1:d-1}) + log q_d^bi(y_d | y_{d-1}) + zeta (Eq. ubtree-depth-bonus),
+// F_d = Top_W(E_d) (Eq. ubtree-frontier, W best extensions over all parents); then
+// T = {root} + Top_budget(union of F_d) (Eq. ubtree-pruning).  Verification via
+// Tree-attention: node n attends to itself and its ancestors -> packed mask rows.
+//
+// One wavefront per sequence; everything between the first load and the final stores
+// lives in LDS and registers.  The score slabs of all depths are staged in LDS up front
+// (when they fit).  Per depth the |F_{d-1}| * K extensions are scored in registers and
+// Top_W is a ballot-driven radix selection on (score key, extension index); the W
+// survivors are ranked among themselves to give F_d in order.  The same selection over
+// the supertree gives the pruned tree, whose emission order is the ranking itself.
+// Ties: score desc, then the extension index (parent position in F_{d-1}, then the
+// candidate rank); across depths score desc, depth asc, position in F_d asc.
+#include "ubt_device.h"
+#include "ubt_launch.h"
+
+namespace ubt {
+namespace {
+
+constexpr int kMaxSlabFloats = 12288;  // 48 KB of staged score slabs
+constexpr int kMaxNodes = 256;
+
+struct TreeSmem {
+  float* slab;        // [gamma][K][K] when staged
+  float* f_score;     // [gamma][W]
+  uint32_t* f_info;   // [gamma][W]: parent position | candidate rank << 16
+  int32_t* f_slot;    // [gamma][W]: output slot (-1 if not selected)
+  uint32_t* s_key;    // [gamma][W]: key of the supertree entry (0 if empty)
+  uint2* stage;       // [256] (key, sub) of staged entries
+  float* stage_score; // [256] scores of staged frontier entries
+  int32_t* par_slot;  // [256] parent slot of each emitted node
+  int32_t* f_cnt;     // [gamma]
+};
+
+__host__ __device__ inline size_t tree_smem_bytes(int gamma, int K, int W, bool stage_slabs) {
+  const size_t gw = static_cast<size_t>(gamma) * W;
+  size_t bytes = 0;
+  if (stage_slabs) bytes += static_cast<size_t>(gamma) * K * K * sizeof(float);
+  bytes += gw * (sizeof(float) + sizeof(uint32_t) + sizeof(int32_t) + sizeof(uint32_t));
+  bytes += kMaxNodes * (sizeof(uint2) + sizeof(float) + sizeof(int32_t));
+  bytes += static_cast<size_t>(gamma) * sizeof(int32_t);
+  return bytes;
+}
+
+// e / K for 0 <= e < 2^16 and 1 <= K <= 64, with magic = ceil(2^32 / K).
+__device__ __forceinline__ int div_k(int e, uint64_t magic) {
+  return static_cast<int>((static_cast<uint64_t>(static_cast<uint32_t>(e)) * magic) >> 32);
+}
+
+// Ranks `n` staged (key, sub) entries by (key desc, sub asc) and calls emit(s, rank) for
+// each entry s.
+template <class Emit>
+__device__ __forceinline__ void rank_staged(const uint2* stage, int n, int lane, Emit emit) {
+  for (int s = lane; s < n; s += kWave) {
+    const uint2 me = stage[s];
+    int rank = 0;
+    for (int t = 0; t < n; ++t) {
+      const uint2 o = stage[t];
+      rank += (o.x > me.x) || (o.x == me.x && o.y < me.y);
+    }
+    emit(s, rank);
+  }
+}
+
+// Writes the selected entries (masks sel[]) of register rows into stage[0..); returns count.
+template <int R>
+__device__ __forceinline__ int stage_selected(uint2* stage, const uint32_t (&key)[R], const uint32_t (&sub)[R],
+                                              const uint64_t (&sel)[R], int lane) {
+  int n = 0;
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    if ((sel[r] >> lane) & 1ull) stage[n + lanes_below(sel[r])] = make_uint2(key[r], sub[r]);
+    n += popc(sel[r]);
+  }
+  __builtin_amdgcn_wave_barrier();
+  return n;
+}
+
+template <int R>
+__global__ __launch_bounds__(kWave) void build_tree_kernel(TreeArgs a, int stage_slabs, int vec_slabs,
+                                                           uint64_t magic_k) {
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  const int lane = threadIdx.x;
+  const int64_t b = blockIdx.x;
+  const int gamma = a.gamma, K = a.K, W = a.W;
+  const int GW = gamma * W;
+
+  TreeSmem sm;
+  {
+    unsigned char* p = smem_raw;
+    sm.slab = reinterpret_cast<float*>(p);
+    if (stage_slabs) p += static_cast<size_t>(gamma) * K * K * sizeof(float);
+    sm.f_score = reinterpret_cast<float*>(p);
+    p += GW * sizeof(float);
+    sm.f_info = reinterpret_cast<uint32_t*>(p);
+    p += GW * sizeof(uint32_t);
+    sm.f_slot = reinterpret_cast<int32_t*>(p);
+    p += GW * sizeof(int32_t);
+    sm.s_key = reinterpret_cast<uint32_t*>(p);
+    p += GW * sizeof(uint32_t);
+    sm.stage = reinterpret_cast<uint2*>(p);
+    p += kMaxNodes * sizeof(uint2);
+    sm.stage_score = reinterpret_cast<float*>(p);
+    p += kMaxNodes * sizeof(float);
+    sm.par_slot = reinterpret_cast<int32_t*>(p);
+    p += kMaxNodes * sizeof(int32_t);
+    sm.f_cnt = reinterpret_cast<int32_t*>(p);
+  }
+
+  const float* gslab = a.logq + b * gamma * K * K;
+  if (stage_slabs) {
+    const int n = gamma * K * K;  // a multiple of 4 floats when K is even
+    if (vec_slabs) {
+      const float4* src = reinterpret_cast<const float4*>(gslab);
+      float4* dst = reinterpret_cast<float4*>(sm.slab);
+      for (int e = lane; e < n / 4; e += kWave) dst[e] = src[e];
+    } else {
+      for (int e = lane; e < n; e += kWave) sm.slab[e] = gslab[e];
+    }
+  }
+  for (int e = lane; e < GW; e += kWave) {
+    sm.f_slot[e] = -1;
+    sm.s_key[e] = 0;
+  }
+  __syncthreads();
+  const float* slab = stage_slabs ? sm.slab : gslab;
+
+  // ---- depth-wise expansion --------------------------------------------------------
+  int np = 1;  // |F_{d-1}|
+  for (int d = 1; d <= gamma; ++d) {
+    const int n = np * K;
+    const float* q = slab + static_cast<int64_t>(d - 1) * K * K;
+    const float* prev_score = sm.f_score + (d > 1 ? (d - 2) * W : 0);
+    const uint32_t* prev_info = sm.f_info + (d > 1 ? (d - 2) * W : 0);
+    uint32_t key[R], sub[R];
+    uint64_t live[R], sel[R];
+    float sc[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const int e = r * kWave + lane;
+      const bool ok = e < n;
+      const int p = div_k(e, magic_k);
+      const int c = e - p * K;
+      float l = 0.f;
+      if (ok) {
+        const float base = d == 1 ? 0.f : prev_score[p];
+        const int row = d == 1 ? 0 : static_cast<int>(prev_info[p] >> 16);
+        l = (base + q[row * K + c]) + a.zeta;
+      }
+      sc[r] = l;
+      key[r] = ok ? f32_key(l) : 0u;
+      sub[r] = static_cast<uint32_t>(e);
+      live[r] = ballot(ok);
+    }
+    const int w_d = n < W ? n : W;
+    wave_select<R>(key, sub, live, w_d, 32, sel);
+    // Stage the survivors with their scores.
+    int cnt = 0;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      if ((sel[r] >> lane) & 1ull) {
+        const int pos = cnt + static_cast<int>(lanes_below(sel[r]));
+        sm.stage[pos] = make_uint2(key[r], sub[r]);
+        sm.stage_score[pos] = sc[r];
+      }
+      cnt += popc(sel[r]);
+    }
+    __builtin_amdgcn_wave_barrier();
+    float* fs = sm.f_score + (d - 1) * W;
+    uint32_t* fi = sm.f_info + (d - 1) * W;
+    uint32_t* fk = sm.s_key + (d - 1) * W;
+    rank_staged(sm.stage, cnt, lane, [&](int s, int rank) {
+      const uint32_t e = sm.stage[s].y;
+      const uint32_t p = static_cast<uint32_t>(div_k(static_cast<int>(e), magic_k));
+      const uint32_t c = e - p * K;
+      const float l = sm.stage_score[s];
+      fs[rank] = l;
+      fi[rank] = p | (c << 16);
+      fk[rank] = sm.stage[s].x;
+    });
+    __builtin_amdgcn_wave_barrier();
+    if (lane == 0) sm.f_cnt[d - 1] = cnt;
+    if (a.f_count) {
+      if (lane == 0) a.f_count[b * gamma + d - 1] = cnt;
+      for (int j = lane; j < W; j += kWave) {
+        const int64_t o = (b * gamma + d - 1) * W + j;
+        const bool have = j < cnt;
+        a.f_parent[o] = have ? static_cast<int32_t>(fi[j] & 0xFFFFu) : -1;
+        a.f_cand[o] = have ? static_cast<int32_t>(fi[j] >> 16) : -1;
+        a.f_score[o] = have ? fs[j] : neg_inf();
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+    np = cnt;
+  }
+
+  // ---- global pruning over the supertree --------------------------------------------
+  // Entry f = (d-1)*W + j; order key (score key, (d-1) << 8 | j) -> desc, asc.
+  int total = 0;
+  for (int d = 0; d < gamma; ++d) total += sm.f_cnt[d];
+  const int n_sel = total < a.budget ? total : a.budget;
+  const int rows = (GW + kWave - 1) / kWave;
+  uint32_t t = 0;
+  {
+    // Threshold on the score key: the n_sel-th largest.
+    for (int bit = 31; bit >= 0; --bit) {
+      const uint32_t cand = t | (1u << bit);
+      int c = 0;
+      for (int r = 0; r < rows; ++r) {
+        const int f = r * kWave + lane;
+        c += popc(ballot(f < GW && sm.s_key[f] >= cand));
+      }
+      if (c >= n_sel) t = cand;
+    }
+  }
+  int above = 0, equal = 0;
+  for (int r = 0; r < rows; ++r) {
+    const int f = r * kWave + lane;
+    const uint32_t k = f < GW ? sm.s_key[f] : 0u;
+    above += popc(ballot(k > t));
+    equal += popc(ballot(k == t && k != 0));
+  }
+  const int rest = n_sel - above;
+  // Among entries tied at t, keep the `rest` with the smallest (depth, position).
+  uint32_t t2 = 0xFFFFFFFFu;  // sub threshold: keep tied entries with sub <= t2
+  if (rest > 0 && rest < equal) {
+    uint32_t inv = 0;
+    for (int bit = 15; bit >= 0; --bit) {
+      const uint32_t cand = inv | (1u << bit);
+      int c = 0;
+      for (int r = 0; r < rows; ++r) {
+        const int f = r * kWave + lane;
+        const uint32_t k = f < GW ? sm.s_key[f] : 0u;
+        const uint32_t subv = static_cast<uint32_t>(((f / W) << 8) | (f % W));
+        c += popc(ballot(k == t && k != 0 && (0xFFFFu - subv) >= cand));
+      }
+      if (c >= rest) inv = cand;
+    }
+    t2 = 0xFFFFu - inv;
+  }
+  // Stage the selected supertree entries.
+  int cnt = 0;
+  for (int r = 0; r < rows; ++r) {
+    const int f = r * kWave + lane;
+    const uint32_t k = f < GW ? sm.s_key[f] : 0u;
+    const uint32_t subv = f < GW ? static_cast<uint32_t>(((f / W) << 8) | (f % W)) : 0u;
+    const bool take = k != 0 && (k > t || (k == t && rest > 0 && subv <= t2));
+    const uint64_t m = ballot(take);
+    if (take) sm.stage[cnt + lanes_below(m)] = make_uint2(k, subv);
+    cnt += popc(m);
+  }
+  __builtin_amdgcn_wave_barrier();
+  // cnt == n_sel.  Ranking gives the emission order; slot = 1 + rank.
+  rank_staged(sm.stage, cnt, lane, [&](int s, int rank) {
+    const uint32_t subv = sm.stage[s].y;
+    const int f = static_cast<int>(subv >> 8) * W + static_cast<int>(subv & 0xFFu);
+    sm.f_slot[f] = 1 + rank;
+  });
+  __syncthreads();
+
+  const int N = a.budget + 1;
+  const int words = (N + 31) / 32;
+  const int n_nodes = 1 + cnt;
+  int32_t* tok = a.token + b * N;
+  int32_t* par = a.parent + b * N;
+  int32_t* dep = a.depth + b * N;
+  int32_t* crk = a.cand_rank + b * N;
+  float* scr = a.score + b * N;
+  if (lane == 0) {
+    a.n_nodes[b] = n_nodes;
+    tok[0] = a.anchor[b];
+    par[0] = -1;
+    dep[0] = 0;
+    crk[0] = -1;
+    scr[0] = 0.f;
+    sm.par_slot[0] = -1;
+  }
+  for (int s = lane; s < cnt; s += kWave) {
+    const uint32_t subv = sm.stage[s].y;
+    const int d = static_cast<int>(subv >> 8) + 1;
+    const int j = static_cast<int>(subv & 0xFFu);
+    const int f = (d - 1) * W + j;
+    const int slot = sm.f_slot[f];
+    const uint32_t info = sm.f_info[f];
+    const int p = static_cast<int>(info & 0xFFFFu);
+    const int c = static_cast<int>(info >> 16);
+    const int ps = d == 1 ? 0 : sm.f_slot[(d - 2) * W + p];
+    tok[slot] = a.cand_ids[(b * gamma + d - 1) * K + c];
+    par[slot] = ps;
+    dep[slot] = d;
+    crk[slot] = c;
+    scr[slot] = sm.f_score[f];
+    sm.par_slot[slot] = ps;
+  }
+  for (int n = n_nodes + lane; n < N; n += kWave) {
+    tok[n] = -1;
+    par[n] = -1;
+    dep[n] = -1;
+    crk[n] = -1;
+    scr[n] = neg_inf();
+  }
+  __syncthreads();
+
+  // ---- ancestor mask ------------------------------------------------------------------
+  if (a.mask) {
+    uint32_t* mrow = a.mask + b * static_cast<int64_t>(N) * words;
+    for (int n = lane; n < N; n += kWave) {
+      uint32_t wv[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+      if (n < n_nodes) {
+        int m = n;
+        for (int step = 0; step <= gamma && m >= 0; ++step) {
+          const uint32_t bit = 1u << (m & 31);
+          const int wi = m >> 5;
+#pragma unroll
+          for (int w = 0; w < 8; ++w) wv[w] |= (w == wi) ? bit : 0u;
+          m = sm.par_slot[m];
+        }
+      }
+#pragma unroll
+      for (int w = 0; w < 8; ++w)
+        if (w < words) mrow[n * words + w] = wv[w];
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void tree_mask_kernel(const int32_t* __restrict__ parent,
+                                                        const int32_t* __restrict__ n_nodes, int N,
+                                                        uint32_t* __restrict__ mask) {
+  __shared__ int32_t s_par[kMaxNodes];
+  const int64_t b = blockIdx.x;
+  const int words = (N + 31) / 32;
+  int nn = n_nodes[b];
+  nn = nn < 0 ? 0 : (nn > N ? N : nn);
+  for (int n = threadIdx.x; n < N; n += blockDim.x) s_par[n] = parent[b * N + n];
+  __syncthreads();
+  uint32_t* mrow = mask + b * static_cast<int64_t>(N) * words;
+  for (int n = threadIdx.x; n < N; n += blockDim.x) {
+    uint32_t wv[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    if (n < nn) {
+      int m = n;
+      // Walk towards the root; a pointer that does not decrease ends the walk.
+      for (int step = 0; step < N; ++step) {
+        const uint32_t bit = 1u << (m & 31);
+        const int wi = m >> 5;
+#pragma unroll
+        for (int w = 0; w < 8; ++w) wv[w] |= (w == wi) ? bit : 0u;
+        if (m == 0) break;
+        const int p = s_par[m];
+        if (p < 0 || p >= m) break;
+        m = p;
+      }
+    }
+#pragma unroll
+    for (int w = 0; w < 8; ++w)
+      if (w < words) mrow[n * words + w] = wv[w];
+  }
+}
+
+}  // namespace
+
+hipError_t launch_build_tree(const TreeArgs& a, hipStream_t stream) {
+  const bool stage_slabs = static_cast<int64_t>(a.gamma) * a.K * a.K <= kMaxSlabFloats;
+  const size_t smem = tree_smem_bytes(a.gamma, a.K, a.W, stage_slabs);
+  const uint64_t magic_k = (0x100000000ull + a.K - 1) / a.K;  // ceil(2^32 / K)
+  const bool vec_slabs = (a.K % 2 == 0) && (reinterpret_cast<uintptr_t>(a.logq) % 16 == 0);
+  const int n_max = a.W * a.K;
+  const dim3 grid(static_cast<unsigned>(a.B)), block(kWave);
+#define UBT_TREE_LAUNCH(RR)                                                                                \
+  do {                                                                                                     \
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&build_tree_kernel<RR>),                       \
+                              hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(smem));         \
+    hipLaunchKernelGGL((build_tree_kernel<RR>), grid, block, smem, stream, a, stage_slabs ? 1 : 0,           \
+                       vec_slabs ? 1 : 0, magic_k);                                                        \
+  } while (0)
+  if (n_max <= 64)
+    UBT_TREE_LAUNCH(1);
+  else if (n_max <= 128)
+    UBT_TREE_LAUNCH(2);
+  else if (n_max <= 256)
+    UBT_TREE_LAUNCH(4);
+  else if (n_max <= 512)
+    UBT_TREE_LAUNCH(8);
+  else if (n_max <= 1024)
+    UBT_TREE_LAUNCH(16);
+  else if (n_max <= 2048)
+    UBT_TREE_LAUNCH(32);
+  else
+    UBT_TREE_LAUNCH(64);
+#undef UBT_TREE_LAUNCH
+  return hipGetLastError();
+}
+
+hipError_t launch_tree_mask(const int32_t* parent, const int32_t* n_nodes, int B, int N, uint32_t* mask,
+                            hipStream_t stream) {
+  hipLaunchKernelGGL(tree_mask_kernel, dim3(static_cast<unsigned>(B)), dim3(256), 0, stream, parent, n_nodes, N,
+                     mask);
+  return hipGetLastError();
+}
+
+}  // namespace ubt

@@ -1,0 +1,59 @@
+// Internal launch interface between the host API (api.cpp) and the HIP kernels.
+// Arguments have been validated by the caller.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace ubt {
+
+// ---- top-K sweep --------------------------------------------------------------------
+struct TopkPlan {
+  int chunk;      // elements per wave chunk
+  int parts;      // chunks per row (P)
+  size_t off_ms;  // workspace offsets (bytes)
+  size_t off_ent;
+  size_t bytes;   // total workspace bytes
+};
+TopkPlan topk_plan(int B, int gamma, int64_t V, int K, int dtype);
+hipError_t launch_topk(const void* logits, int dtype, bool aligned, int B, int gamma, int64_t V,
+                       int64_t stride_b, int64_t stride_i, int K, const TopkPlan& plan, void* workspace,
+                       int32_t* cand_ids, float* cand_logit, float* cand_logprob, float* lse,
+                       hipStream_t stream);
+
+// ---- selector scores ------------------------------------------------------------------
+struct Scales {
+  float alpha[64];
+  float lambda[64];
+};
+hipError_t launch_bigram(const void* phi, const void* psi, const void* gate, int feat_dtype, int64_t V, int r,
+                         const int32_t* anchor, const int32_t* cand_ids, const float* cand_logit,
+                         const Scales& scales, int B, int gamma, int K, float* delta, float* logq,
+                         hipStream_t stream);
+
+// ---- tree search --------------------------------------------------------------------
+struct TreeArgs {
+  const int32_t* anchor;
+  const int32_t* cand_ids;
+  const float* logq;
+  int B, gamma, K, W, budget;
+  float zeta;
+  int32_t* n_nodes;
+  int32_t* token;
+  int32_t* parent;
+  int32_t* depth;
+  int32_t* cand_rank;
+  float* score;
+  uint32_t* mask;
+  int32_t* f_count;
+  int32_t* f_parent;
+  int32_t* f_cand;
+  float* f_score;
+};
+hipError_t launch_build_tree(const TreeArgs& a, hipStream_t stream);
+
+hipError_t launch_tree_mask(const int32_t* parent, const int32_t* n_nodes, int B, int N, uint32_t* mask,
+                            hipStream_t stream);
+
+}  // namespace ubt

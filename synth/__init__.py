@@ -106,8 +106,8 @@ def round_f32(x: np.ndarray) -> np.ndarray:
 
 def round_bf16_bits(x: np.ndarray) -> np.ndarray:
     """fp64 -> fp32 (RNE) -> bf16 (RNE); returns the bf16 bit patterns as uint16."""
-    bits = round_f32(x).view(np.uint32).astype(np.uint64)
-    bias = ((bits >> 16) & 1) + 0x7FFF
+    bits = round_f32(x).view(np.uint32)
+    bias = ((bits >> 16) & 1) + np.uint32(0x7FFF)
     return ((bits + bias) >> 16).astype(np.uint16)
 
 

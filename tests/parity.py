@@ -1,0 +1,192 @@
+"""Comparison of GPU outputs with the fp64 oracle.
+
+Candidate ids, tree topology, tokens and masks are compared bit for bit.  Floating-point
+outputs are compared within ``EPS * max(1, |ref|)`` (EPS = 1e-5).
+
+Tree construction takes discrete decisions on floating-point scores.  The GPU scores in
+fp32, the oracle in fp64, so two candidates whose scores differ by less than the
+rounding can be ordered differently; both trees are then correct.  When the GPU tree is
+not identical to the oracle's, :func:`check_tree` validates the GPU's own selections
+against the oracle's fp64 scores step by step ("guided"): at every Top_W and at the
+final Top_budget, every node the GPU kept or dropped must be on the right side of the
+oracle's selection boundary, unless its fp64 score lies within ``EPS * max(1, |score|)``
+of that boundary (the tie gap).  Structure (parents, depths, tokens, mask) must still
+be exact for the GPU's tree.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+EPS = 1e-5
+
+
+def tol(ref: np.ndarray) -> np.ndarray:
+    return EPS * np.maximum(1.0, np.abs(ref))
+
+
+def close(gpu: np.ndarray, ref: np.ndarray, what: str) -> None:
+    gpu = np.asarray(gpu, np.float64)
+    ref = np.asarray(ref, np.float64)
+    same_inf = np.isinf(gpu) & np.isinf(ref) & (np.sign(gpu) == np.sign(ref))
+    with np.errstate(invalid="ignore"):
+        err = np.where(same_inf, 0.0, np.abs(gpu - ref))
+    bad = ~(err <= tol(np.where(np.isinf(ref), 0.0, ref)))
+    if bad.any():
+        i = np.argwhere(bad)[0]
+        raise AssertionError(f"{what}: {int(bad.sum())} entries out of tolerance; first at {tuple(i)}: "
+                             f"gpu={gpu[tuple(i)]!r} ref={ref[tuple(i)]!r}")
+
+
+def check_topk(g: dict, ref: dict, rows: np.ndarray | None = None) -> None:
+    """g: GPU outputs (numpy) for all rows; ref: oracle outputs for `rows` (flattened row
+    indices) or for all rows."""
+    K = g["cand_ids"].shape[-1]
+    gid = g["cand_ids"].reshape(-1, K)
+    glog = g["cand_logit"].reshape(-1, K)
+    glp = g["cand_logprob"].reshape(-1, K) if g.get("cand_logprob") is not None else None
+    glse = g["lse"].reshape(-1)
+    if rows is not None:
+        gid, glog, glse = gid[rows], glog[rows], glse[rows]
+        glp = glp[rows] if glp is not None else None
+    rid = ref["cand_ids"].reshape(-1, K)
+    if not np.array_equal(gid, rid):
+        r = int(np.argwhere((gid != rid).any(-1))[0][0])
+        raise AssertionError(f"candidate ids differ in row {r}: gpu={gid[r].tolist()} ref={rid[r].tolist()}")
+    np.testing.assert_array_equal(glog.astype(np.float64), ref["cand_logit"].reshape(-1, K), "candidate logits")
+    close(glse, ref["lse"].reshape(-1), "lse")
+    if glp is not None:
+        close(glp, ref["cand_logprob"].reshape(-1, K), "cand_logprob")
+
+
+def check_selector(g: dict, ref: dict, seqs: np.ndarray | None = None) -> None:
+    for k in ("delta", "logq"):
+        if g.get(k) is None:
+            continue
+        gv = g[k] if seqs is None else g[k][seqs]
+        close(gv, ref[k], k)
+
+
+def _paths_from_dump(g: dict, b: int) -> list:
+    gamma = g["f_count"].shape[1]
+    prev, out = [()], []
+    for d in range(gamma):
+        n = int(g["f_count"][b, d])
+        cur = [prev[int(g["f_parent"][b, d, j])] + (int(g["f_cand"][b, d, j]),) for j in range(n)]
+        out.append(cur)
+        prev = cur
+    return out
+
+
+def _mask_bits(mask_row: np.ndarray, N: int) -> set:
+    words = mask_row.view(np.uint32)
+    return {m for m in range(N) if (int(words[m // 32]) >> (m % 32)) & 1}
+
+
+def check_structure(g: dict, b: int, cand_ids: np.ndarray, anchor: int, budget: int, with_mask: bool = True) -> list:
+    """Exact structural checks of the GPU tree of sequence b; returns its node paths."""
+    N = budget + 1
+    n = int(g["n_nodes"][b])
+    par, dep, cr, tok = g["parent"][b], g["depth"][b], g["cand_rank"][b], g["token"][b]
+    assert 1 <= n <= N
+    assert par[0] == -1 and dep[0] == 0 and tok[0] == anchor and cr[0] == -1 and g["score"][b, 0] == 0
+    paths = [()]
+    for i in range(1, n):
+        p = int(par[i])
+        assert 0 <= p < i, f"slot {i}: parent {p} does not precede it"
+        assert dep[i] == dep[p] + 1, f"slot {i}: depth {dep[i]} vs parent depth {dep[p]}"
+        assert 0 <= cr[i] < cand_ids.shape[-1]
+        assert tok[i] == cand_ids[dep[i] - 1, cr[i]], f"slot {i}: token is not C_d[c]"
+        assert g["score"][b, i] <= g["score"][b, p], f"slot {i}: score above its parent's"
+        paths.append(paths[p] + (int(cr[i]),))
+    assert len(set(paths)) == len(paths), "a prefix appears twice"
+    assert (par[n:] == -1).all() and (dep[n:] == -1).all() and (tok[n:] == -1).all() and (cr[n:] == -1).all()
+    assert np.isneginf(g["score"][b, n:]).all()
+    if with_mask and g.get("mask") is not None:
+        for i in range(N):
+            bits = _mask_bits(g["mask"][b, i], N)
+            if i >= n:
+                assert not bits, f"mask row {i} beyond n_nodes is not zero"
+                continue
+            anc, m = set(), i
+            while m >= 0:
+                anc.add(m)
+                m = int(par[m])
+            assert bits == anc, f"mask row {i} is not the ancestor set"
+    return paths[1:]
+
+
+def check_tree(g: dict, ref: dict, logq: np.ndarray, cand_ids: np.ndarray, anchor: np.ndarray, W: int,
+               budget: int, zeta: float = 0.0, seqs=None, allow_ties: bool = True) -> dict:
+    """Compares GPU trees (all sequences in `g`, or `seqs` of them) with the oracle's
+    (`ref`, `logq` and `cand_ids` indexed like `seqs`).  Returns counts of exact and
+    excused sequences; raises on a failure."""
+    seqs = list(range(g["n_nodes"].shape[0])) if seqs is None else list(seqs)
+    counts = dict(exact=0, excused=0)
+    for j, b in enumerate(seqs):
+        paths = check_structure(g, b, cand_ids[j], int(anchor[j]), budget)
+        n = int(g["n_nodes"][b])
+        same = (n == int(ref["n_nodes"][j])
+                and np.array_equal(g["parent"][b], ref["parent"][j])
+                and np.array_equal(g["cand_rank"][b], ref["cand_rank"][j])
+                and np.array_equal(g["token"][b], ref["token"][j]))
+        if same and g.get("mask") is not None:
+            same = np.array_equal(g["mask"][b].view(np.uint32), ref["mask"][j])
+        if same:
+            close(g["score"][b, :n], ref["score"][j, :n], f"seq {b} scores")
+            counts["exact"] += 1
+            continue
+        if not allow_ties:
+            raise AssertionError(f"seq {b}: tree differs from the oracle and ties are not allowed here")
+        _guided(g, b, paths, logq[j], W, budget, zeta)
+        counts["excused"] += 1
+    return counts
+
+
+def _guided(g: dict, b: int, tree_paths: list, q: np.ndarray, W: int, budget: int, zeta: float) -> None:
+    if "f_count" not in g:
+        raise AssertionError(f"seq {b}: tree differs and no supertree dump is available to validate it")
+    gamma, K = q.shape[0], q.shape[2]
+    fr = _paths_from_dump(g, b)
+    score = {(): 0.0}
+    prev = [()]
+    for d in range(1, gamma + 1):
+        ext = []
+        for p, pp in enumerate(prev):
+            row = 0 if d == 1 else pp[-1]
+            for c in range(K):
+                path = pp + (c,)
+                score[path] = score[pp] + float(q[d - 1, row, c]) + zeta
+                ext.append(path)
+        keep = fr[d - 1]
+        assert len(keep) == min(W, len(ext)), f"seq {b} depth {d}: |F_d| = {len(keep)}"
+        assert set(keep) <= set(ext), f"seq {b} depth {d}: F_d holds a node outside E_d"
+        _validate_cut(ext, set(keep), score, len(keep), f"seq {b} depth {d}")
+        for x, y in zip(keep, keep[1:]):
+            assert score[x] >= score[y] - EPS * max(1.0, abs(score[y])), f"seq {b} depth {d}: F_d out of order"
+        for jj, x in enumerate(keep):
+            gs = float(g["f_score"][b, d - 1, jj])
+            assert abs(gs - score[x]) <= EPS * max(1.0, abs(score[x])), f"seq {b} depth {d}: F_d score {gs}"
+        prev = keep
+    sup = [p for f in fr for p in f]
+    n_sel = min(budget, len(sup))
+    assert len(tree_paths) == n_sel, f"seq {b}: {len(tree_paths)} nodes, expected {n_sel}"
+    assert set(tree_paths) <= set(sup)
+    _validate_cut(sup, set(tree_paths), score, n_sel, f"seq {b} pruning")
+    for x, y in zip(tree_paths, tree_paths[1:]):
+        assert score[x] >= score[y] - EPS * max(1.0, abs(score[y])), f"seq {b}: emission out of order"
+
+
+def _validate_cut(items: list, chosen: set, score: dict, n: int, where: str) -> None:
+    """`chosen` (n items) must be a top-n of `items` by fp64 score up to the tie gap."""
+    if n >= len(items):
+        assert len(chosen) == len(items)
+        return
+    vals = sorted((score[x] for x in items), reverse=True)
+    boundary = vals[n - 1]
+    for x in items:
+        s = score[x]
+        gap = EPS * max(1.0, abs(s), abs(boundary))
+        if s > boundary + gap:
+            assert x in chosen, f"{where}: dropped {x} with score {s} above the boundary {boundary}"
+        if s < boundary - gap:
+            assert x not in chosen, f"{where}: kept {x} with score {s} below the boundary {boundary}"

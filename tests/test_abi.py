@@ -1,0 +1,136 @@
+"""The C ABI of libubt.so on the host: exported symbols, status strings, workspace
+sizing, and argument validation, which returns an error before any device work (so
+these run without a GPU; the pointers passed are never dereferenced)."""
+from __future__ import annotations
+
+import ctypes
+import re
+import subprocess
+
+import pytest
+
+import paper_2609_39972_amd as ubt
+
+FAKE = ctypes.c_void_p(0x10000)  # never dereferenced: every call below fails validation first
+
+
+def _declared() -> set:
+    hdr = open(f"{ubt.PKG}/../include/ubt.h").read()
+    return set(re.findall(r"\b(ubt_[a-z_]+)\s*\(", hdr))
+
+
+def test_library_exports_every_declared_symbol():
+    L = ubt.lib()
+    declared = _declared()
+    assert declared == set(ubt.EXPORTS)
+    nm = subprocess.run(["nm", "-D", "--defined-only", ubt.LIB_PATH], capture_output=True, text=True, check=True)
+    exported = set(re.findall(r" T (ubt_\w+)", nm.stdout))
+    assert declared <= exported
+    for name in declared:
+        assert hasattr(L, name)
+
+
+def test_version_and_status_strings():
+    L = ubt.lib()
+    assert L.ubt_abi_version() == 1
+    for code, name in ubt.STATUS.items():
+        assert L.ubt_status_str(code).decode() == name
+    assert L.ubt_status_str(99).decode() == "UBT_ERR_UNKNOWN"
+
+
+def test_workspace_bytes():
+    L = ubt.lib()
+    n = L.ubt_topk_workspace_bytes(32, 15, 151936, 8, ubt.UBT_BF16)
+    P = -(-151936 // 8192)
+    assert n >= 32 * 15 * (4 + 8 * P + 8 * P * 8)
+    assert n % 256 == 0
+    for bad in [(0, 15, 100, 8, 1), (1, 65, 100, 8, 1), (1, 1, 7, 8, 1), (1, 1, 100, 65, 1), (1, 1, 100, 0, 1),
+                (1, 1, 100, 8, 2), (1, 1, 2 ** 31, 8, 1)]:
+        assert L.ubt_topk_workspace_bytes(*bad) == 0, bad
+
+
+def _topk(**kw):
+    a = dict(logits=FAKE, dt=1, B=2, gamma=3, V=1000, sb=3000, si=1000, K=8, ids=FAKE, val=FAKE, lp=None, lse=None,
+             ws=FAKE, wsb=1 << 20)
+    a.update(kw)
+    return ubt.lib().ubt_topk(a["logits"], a["dt"], a["B"], a["gamma"], a["V"], a["sb"], a["si"], a["K"], a["ids"],
+                              a["val"], a["lp"], a["lse"], a["ws"], a["wsb"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(logits=None), 1), (dict(ids=None), 1), (dict(val=None), 1),
+    (dict(dt=5), 3),
+    (dict(B=0), 2), (dict(gamma=0), 2), (dict(gamma=65), 2), (dict(K=0), 2), (dict(K=65), 2), (dict(V=7), 2),
+    (dict(si=999), 2), (dict(sb=2999), 2), (dict(V=2 ** 31, si=2 ** 31, sb=3 * 2 ** 31), 2),
+    (dict(ws=None), 5), (dict(wsb=100), 5), (dict(ws=ctypes.c_void_p(0x10010)), 5),
+])
+def test_topk_validation(kw, code):
+    assert _topk(**kw) == code
+
+
+def _bigram(alpha=None, lam=None, **kw):
+    g = kw.pop("gamma", 3)
+    a = (ctypes.c_float * 64)(*([1.0] * 64)) if alpha is None else alpha
+    l_ = (ctypes.c_float * 64)(*([1.0] * 64)) if lam is None else lam
+    args = dict(phi=FAKE, psi=FAKE, gate=FAKE, dt=1, V=1000, r=64, anchor=FAKE, ids=FAKE, logit=FAKE, B=2, K=8,
+                delta=None, logq=FAKE)
+    args.update(kw)
+    return ubt.lib().ubt_bigram_scores(args["phi"], args["psi"], args["gate"], args["dt"], args["V"], args["r"],
+                                       args["anchor"], args["ids"], args["logit"], a, l_, args["B"], g, args["K"],
+                                       args["delta"], args["logq"], None)
+
+
+def _arr(vals):
+    return (ctypes.c_float * len(vals))(*vals)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(phi=None), 1), (dict(gate=None), 1), (dict(anchor=None), 1), (dict(logq=None), 1),
+    (dict(dt=9), 3), (dict(r=8), 2), (dict(r=72), 2), (dict(r=528), 2), (dict(K=65), 2), (dict(gamma=65), 2),
+    (dict(V=5), 2), (dict(B=0), 2),
+    (dict(alpha=_arr([1.0, 0.0, 1.0])), 3), (dict(lam=_arr([1.0, 1.0, -2.0])), 3),
+    (dict(alpha=_arr([1.0, float("inf"), 1.0])), 3), (dict(lam=_arr([float("nan"), 1.0, 1.0])), 3),
+    (dict(phi=ctypes.c_void_p(0x10002)), 4),
+])
+def test_bigram_validation(kw, code):
+    assert _bigram(**kw) == code
+
+
+def _tree(dbg=None, **kw):
+    a = dict(anchor=FAKE, ids=FAKE, logq=FAKE, B=2, gamma=15, K=8, W=12, budget=64, zeta=0.0, nn=FAKE, tok=FAKE,
+             par=FAKE, dep=FAKE, cr=FAKE, sc=FAKE, mask=None)
+    a.update(kw)
+    return ubt.lib().ubt_build_tree(a["anchor"], a["ids"], a["logq"], a["B"], a["gamma"], a["K"], a["W"],
+                                    a["budget"], a["zeta"], a["nn"], a["tok"], a["par"], a["dep"], a["cr"], a["sc"],
+                                    a["mask"], dbg, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(anchor=None), 1), (dict(logq=None), 1), (dict(nn=None), 1), (dict(sc=None), 1),
+    (dict(B=0), 2), (dict(gamma=0), 2), (dict(gamma=65), 2), (dict(K=65), 2), (dict(W=0), 2), (dict(W=256), 2),
+    (dict(budget=0), 2), (dict(budget=256), 2),
+    (dict(W=65, K=64), 4), (dict(gamma=64, W=65, K=4), 4),
+    (dict(zeta=0.5), 3), (dict(zeta=float("-inf")), 3), (dict(zeta=float("nan")), 3),
+])
+def test_build_tree_validation(kw, code):
+    assert _tree(**kw) == code
+
+
+def test_build_tree_incomplete_debug_struct():
+    s = ubt._Supertree(FAKE, None, FAKE, FAKE)
+    assert _tree(dbg=ctypes.byref(s)) == 1
+
+
+@pytest.mark.parametrize("args,code", [
+    ((None, FAKE, 2, 65, FAKE), 1), ((FAKE, None, 2, 65, FAKE), 1), ((FAKE, FAKE, 2, 65, None), 1),
+    ((FAKE, FAKE, 0, 65, FAKE), 2), ((FAKE, FAKE, 2, 0, FAKE), 2), ((FAKE, FAKE, 2, 257, FAKE), 2),
+])
+def test_tree_mask_validation(args, code):
+    assert ubt.lib().ubt_tree_mask(*args, None) == code
+
+
+def test_binding_refuses_host_tensors():
+    import torch
+
+    with pytest.raises(ValueError):
+        ubt.topk(torch.zeros(1, 1, 16, dtype=torch.bfloat16), 4)

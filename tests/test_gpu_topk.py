@@ -1,0 +1,149 @@
+"""GPU parity of ubt_topk (softmax statistics and candidate sets) against the oracle."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+import oracle
+import parity
+import synth
+
+pytestmark = pytest.mark.gpu
+
+
+def _run(x: np.ndarray, K: int, view=None):
+    import torch
+
+    import paper_2609_39972_amd as ubt
+    from gpu_util import dev_values, to_np
+
+    t = dev_values(x)
+    if view is not None:
+        t = view(t)
+    out = ubt.topk(t, K)
+    torch.cuda.synchronize()
+    return to_np(out)
+
+
+def _rows(x: np.ndarray) -> np.ndarray:
+    return x.reshape(-1, x.shape[-1])
+
+
+def _check(x: np.ndarray, K: int):
+    from gpu_util import say
+
+    say(f"topk shape={x.shape} dtype={x.dtype} K={K}")
+    g = _run(x, K)
+    parity.check_topk(g, oracle.topk(x, K))
+    return g
+
+
+def _bf16(v: np.ndarray) -> np.ndarray:
+    return synth.round_bf16_bits(v)
+
+
+@pytest.mark.parametrize("V,K", [(1, 1), (8, 8), (33, 8), (100, 64), (1000, 1), (4095, 16), (4096, 4), (8191, 16),
+                                 (8192, 8), (8193, 16), (20000, 64), (151937, 16)])
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_shapes_and_ragged_tails(V, K, dt):
+    rng = np.random.default_rng(V + K)
+    x = synth.store(rng.normal(0, 2.5, (2, 3, V)), dt)
+    _check(x, K)
+
+
+@pytest.mark.parametrize("K", list(range(1, 65)))
+def test_every_k(K):
+    rng = np.random.default_rng(100 + K)
+    _check(synth.store(rng.normal(0, 1.5, (1, 2, 12345)), "bf16"), K)
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_all_equal_rows_take_lowest_ids(dt):
+    x = synth.store(np.full((1, 3, 30000), 0.75), dt)
+    g = _check(x, 64)
+    assert (g["cand_ids"] == np.arange(64)).all()
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_heavy_duplicates(dt):
+    rng = np.random.default_rng(7)
+    x = synth.store(np.round(rng.normal(0, 1, (2, 4, 50000)) * 2) / 2, dt)
+    _check(x, 32)
+
+
+def test_signed_zero_and_neg_inf():
+    x = np.full((1, 2, 9000), -np.inf, np.float32)
+    x[0, 0, [17, 4000, 8999]] = [-0.0, 0.0, -0.0]
+    x[0, 1, 5] = 3.0
+    x[0, 1, 8191] = -2.0
+    g = _check(x, 6)
+    assert g["cand_ids"][0, 0, :3].tolist() == [17, 4000, 8999]
+    xb = synth.round_bf16_bits(x.astype(np.float64))
+    _check(xb, 6)
+
+
+def test_zipf_rows_full_vocab():
+    w = synth.WORKLOADS[3]
+    x = synth.logits(w, 0, rows=np.arange(40)).reshape(4, 10, w.V)
+    _check(x, 8)
+    _check(x, 16)
+
+
+def test_high_entropy_rows():
+    w = synth.WORKLOADS[4]
+    x = synth.logits(w, 0, rows=np.arange(30)).reshape(2, 15, w.V)
+    _check(x, 16)
+
+
+def test_strided_block_view_and_padding():
+    """Rows taken from a [B, L, V] block (skip the anchor row) and rows with padded strides."""
+    import torch
+
+    rng = np.random.default_rng(3)
+    V = 10007
+    block = synth.store(rng.normal(0, 2, (3, 6, V)), "bf16")
+    g = _run(block, 8, view=lambda t: t[:, 1:, :])
+    parity.check_topk(g, oracle.topk(np.ascontiguousarray(block[:, 1:, :]), 8))
+    # padded rows: aligned (bf16 pad of 9 -> row stride 10016 elements = 20032 B) and unaligned (f32 pad of 3)
+    for dt, pad in (("bf16", 9), ("f32", 3)):
+        big = synth.store(rng.normal(0, 2, (2, 3, V + pad)), dt)
+        g = _run(big, 12, view=lambda t: t[:, :, :V])
+        parity.check_topk(g, oracle.topk(np.ascontiguousarray(big[:, :, :V]), 12))
+    del torch
+
+
+def test_workspace_reuse_across_shapes_and_determinism():
+    import torch
+
+    import paper_2609_39972_amd as ubt
+    from gpu_util import dev_values, to_np
+
+    rng = np.random.default_rng(11)
+    xa = synth.store(rng.normal(0, 2, (2, 5, 40000)), "bf16")
+    xb = synth.store(rng.normal(0, 2, (1, 3, 9000)), "bf16")
+    ws = ubt.TopkWorkspace(2, 5, 40000, 16, torch.bfloat16)
+    ta, tb = dev_values(xa), dev_values(xb)
+    outs = []
+    for t, K in ((ta, 16), (tb, 4), (ta, 16), (tb, 4)):
+        assert ws.nbytes >= ubt.TopkWorkspace(t.shape[0], t.shape[1], t.shape[2], K, torch.bfloat16).nbytes
+        o = to_np(ubt.topk(t, K, workspace=ws))
+        outs.append(o)
+    torch.cuda.synchronize()
+    parity.check_topk(outs[0], oracle.topk(xa, 16))
+    parity.check_topk(outs[1], oracle.topk(xb, 4))
+    for a, b in ((outs[0], outs[2]), (outs[1], outs[3])):
+        for k in a:
+            assert np.array_equal(a[k], b[k]), f"{k} not bitwise reproducible"
+    assert int(ws.tensor[: 4 * 10].view(torch.int32).abs().sum()) == 0, "row counters not returned to zero"
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+def test_workload_full_size(cfg):
+    """Every row of the workload at its full size (all buffers of one pool entry)."""
+    from gpu_util import say
+
+    w = synth.WORKLOADS[cfg]
+    say(f"topk workload {cfg}: {w.describe()}")
+    x = synth.logits(w, 0)
+    g = _run(x, w.K)
+    parity.check_topk(g, oracle.topk(x, w.K))

@@ -1,0 +1,98 @@
+"""GPU parity of ubt_build_tree and ubt_tree_mask.
+
+The scores fed here are dyadic (multiples of 2^-6), so every path sum is exact in fp32
+and fp64 alike: trees, supertrees and masks must equal the oracle's bit for bit, exact
+ties included (no tie gap is granted)."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+import oracle
+import parity
+import synth
+
+pytestmark = pytest.mark.gpu
+
+
+def _gpu_tree(anchor, ids, q, W, budget, zeta, with_mask=True):
+    import torch
+
+    import paper_2609_39972_amd as ubt
+    from gpu_util import dev_i32, dev_values, to_np
+
+    out = ubt.build_tree(dev_i32(anchor), dev_i32(ids), dev_values(q.astype(np.float32)), W, budget, zeta,
+                         with_mask=with_mask, debug=True)
+    torch.cuda.synchronize()
+    return to_np(out)
+
+
+def _compare(B, gamma, K, W, budget, zeta=0.0, seed=0, tie_frac=0.0, levels=64):
+    from gpu_util import say
+
+    say(f"tree B={B} gamma={gamma} K={K} W={W} budget={budget} zeta={zeta} ties={tie_frac}")
+    q = synth.dyadic_logq(B, gamma, K, seed=seed, levels=levels, tie_frac=tie_frac)
+    ids = synth.candidate_ids(B, gamma, K, 100000, seed)
+    anchor = np.arange(B, dtype=np.int32) * 7 + 1
+    g = _gpu_tree(anchor, ids, q, W, budget, zeta)
+    ref = oracle.build_tree(anchor, ids, q.astype(np.float64), W, budget, zeta)
+    for k in ("n_nodes", "token", "parent", "depth", "cand_rank", "f_count", "f_parent", "f_cand"):
+        assert np.array_equal(g[k], ref[k]), f"{k} differs"
+    assert np.array_equal(g["score"].astype(np.float64), ref["score"])
+    assert np.array_equal(g["f_score"].astype(np.float64), ref["f_score"])
+    assert np.array_equal(g["mask"], ref["mask"])
+    for b in range(B):
+        parity.check_structure(g, b, ids[b], int(anchor[b]), budget)
+    return g
+
+
+@pytest.mark.parametrize("B,gamma,K,W,budget", [
+    (2, 1, 1, 1, 1), (3, 1, 8, 3, 5), (2, 4, 1, 2, 10), (4, 7, 4, 3, 16), (4, 15, 8, 8, 32), (8, 15, 8, 12, 64),
+    (4, 15, 16, 24, 128), (2, 31, 16, 24, 128), (2, 15, 8, 64, 64), (2, 31, 16, 128, 128), (2, 15, 64, 12, 64),
+    (2, 5, 64, 64, 255), (2, 64, 4, 64, 255), (1, 16, 16, 255, 255), (2, 3, 5, 7, 100), (2, 9, 3, 2, 200),
+])
+def test_dyadic_exact(B, gamma, K, W, budget):
+    _compare(B, gamma, K, W, budget, seed=B + gamma + K)
+
+
+@pytest.mark.parametrize("tie_frac,levels", [(0.5, 8), (0.9, 4), (0.0, 1)])
+def test_exact_ties(tie_frac, levels):
+    _compare(4, 10, 8, 12, 64, seed=3, tie_frac=tie_frac, levels=levels)
+    _compare(2, 15, 16, 24, 128, seed=4, tie_frac=tie_frac, levels=levels)
+
+
+@pytest.mark.parametrize("zeta", [-0.125, -1.0, -1000.0])
+def test_depth_bonus(zeta):
+    _compare(4, 15, 8, 12, 64, zeta=zeta, seed=9)
+
+
+def test_wide_beam_equals_best_first():
+    """W >= budget: T is the global top-budget of the lattice, independent of W."""
+    g1 = _compare(3, 8, 4, 40, 40, seed=12)
+    g2 = _compare(3, 8, 4, 100, 40, seed=12)
+    for k in ("token", "parent", "depth", "cand_rank", "score", "mask"):
+        assert np.array_equal(g1[k], g2[k])
+
+
+def test_tree_mask_matches_fused_and_oracle():
+    import torch
+
+    import paper_2609_39972_amd as ubt
+    from gpu_util import dev_i32, to_np
+
+    g = _compare(5, 15, 16, 24, 128, seed=21)
+    par, nn = dev_i32(g["parent"]), dev_i32(g["n_nodes"])
+    m = ubt.tree_mask(par, nn).cpu().numpy().view(np.uint32)
+    assert np.array_equal(m, g["mask"])
+    # random forests in parent-before-child order, with fewer live nodes than slots
+    rng = np.random.default_rng(2)
+    B, N = 6, 200
+    parent = np.full((B, N), -1, np.int32)
+    for b in range(B):
+        for n in range(1, N):
+            parent[b, n] = rng.integers(0, n)
+    n_nodes = np.array([1, 2, 57, 199, 200, 0], np.int32)
+    m = ubt.tree_mask(dev_i32(parent), dev_i32(n_nodes)).cpu().numpy().view(np.uint32)
+    torch.cuda.synchronize()
+    assert np.array_equal(m, oracle.tree_mask(parent, n_nodes))
+    del to_np
