@@ -151,18 +151,20 @@ def main() -> int:
     torch.cuda.synchronize()
     replays = max(1, -(-args.steps // pool))
     steps = replays * pool
-    for _ in range(2):
-        graph.replay()
+    with torch.cuda.stream(stream):
+        for _ in range(2):
+            graph.replay()
     torch.cuda.synchronize()
 
     start = torch.cuda.Event(enable_timing=True)
     end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t_wall = time.perf_counter()
-    start.record(stream)
-    for _ in range(replays):
-        graph.replay()
-    end.record(stream)
+    with torch.cuda.stream(stream):
+        start.record(stream)
+        for _ in range(replays):
+            graph.replay()
+        end.record(stream)
     torch.cuda.synchronize()
     wall_ms = (time.perf_counter() - t_wall) * 1e3
     elapsed_ms = start.elapsed_time(end)

@@ -32,8 +32,7 @@ template <>
 struct Traits<uint16_t> {  // bf16 bit patterns
   static constexpr int kPer = 8;
   static constexpr int kKeyBits = 16;
-  static constexpr uint32_t kNegInfBits = 0xFF80u;
-  __device__ static float elem(const u32x4& v, int j) {
+    __device__ static float elem(const u32x4& v, int j) {
     const uint32_t w = v[j >> 1];
     return __uint_as_float((j & 1) ? (w & 0xFFFF0000u) : (w << 16));
   }
@@ -65,6 +64,18 @@ struct Traits<float> {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
+
+// Stores and loads that are coherent at device (agent) scope: partial results travel
+// between waves on different XCDs without cache-wide writeback or invalidation.
+__device__ __forceinline__ void store_agent(uint64_t* p, uint64_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint64_t load_agent(const uint64_t* p) {
+  return __hip_atomic_load(const_cast<uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint64_t pack(uint32_t lo, uint32_t hi) {
+  return static_cast<uint64_t>(lo) | (static_cast<uint64_t>(hi) << 32);
+}
 
 // Group of EPG elements starting at element e0 of row `rp`, elements >= lim read as -inf.
 template <typename T, bool kAligned>
@@ -154,24 +165,25 @@ __device__ __forceinline__ void flush(WaveLds& s, int nbuf, int64_t c0, int64_t 
 
 // The last wave of a row: merges the P partial results into LSE and the sorted top-K.
 template <typename T>
-__device__ void merge_row(int64_t row, int P, int K, int lane, WaveLds& s, const float2* __restrict__ part_ms,
-                          const uint2* __restrict__ part_ent, int32_t* __restrict__ cand_ids,
+__device__ void merge_row(int64_t row, int P, int K, int lane, WaveLds& s, const uint64_t* __restrict__ part_ms,
+                          const uint64_t* __restrict__ part_ent, int32_t* __restrict__ cand_ids,
                           float* __restrict__ cand_logit, float* __restrict__ cand_logprob, float* __restrict__ lse) {
-  const float2* ms = part_ms + row * P;
+  const uint64_t* ms = part_ms + row * P;
   float m = neg_inf();
-  for (int p = lane; p < P; p += kWave) m = fmaxf(m, __builtin_nontemporal_load(&ms[p].x));
+  for (int p = lane; p < P; p += kWave) m = fmaxf(m, __uint_as_float(static_cast<uint32_t>(load_agent(&ms[p]))));
   m = wave_max(m);
   float sum = 0.f;
   for (int p = lane; p < P; p += kWave) {
-    const float pm = __builtin_nontemporal_load(&ms[p].x);
-    const float ps = __builtin_nontemporal_load(&ms[p].y);
+    const uint64_t v = load_agent(&ms[p]);
+    const float pm = __uint_as_float(static_cast<uint32_t>(v));
+    const float ps = __uint_as_float(static_cast<uint32_t>(v >> 32));
     if (pm != neg_inf()) sum += ps * fast_exp2((pm - m) * kLog2e);
   }
   sum = wave_sum(sum);
   const float l = (m == neg_inf()) ? neg_inf() : m + fast_log2(sum) * kLn2;
 
   constexpr int RB = 4;
-  const uint2* ent = part_ent + row * static_cast<int64_t>(P) * K;
+  const uint64_t* ent = part_ent + row * static_cast<int64_t>(P) * K;
   const int total = P * K;
   uint32_t cur_key = 0, cur_id = 0;
   for (int base = 0; base < total; base += RB * kWave) {
@@ -185,8 +197,9 @@ __device__ void merge_row(int64_t row, int P, int K, int lane, WaveLds& s, const
       const int e = base + r * kWave + lane;
       uint32_t k = 0, id = 0;
       if (e < total) {
-        k = __builtin_nontemporal_load(&ent[e].x);
-        id = __builtin_nontemporal_load(&ent[e].y);
+        const uint64_t v = load_agent(&ent[e]);
+        k = static_cast<uint32_t>(v);
+        id = static_cast<uint32_t>(v >> 32);
       }
       key[r + 1] = k;
       sub[r + 1] = id;
@@ -215,7 +228,7 @@ __device__ void merge_row(int64_t row, int P, int K, int lane, WaveLds& s, const
 template <typename T, bool kAligned>
 __global__ __launch_bounds__(kWave* kWavesPerBlock) void topk_sweep_kernel(
     const T* __restrict__ logits, int gamma, int64_t V, int64_t stride_b, int64_t stride_i, int K, int P,
-    int64_t Q, uint32_t* __restrict__ counters, float2* __restrict__ part_ms, uint2* __restrict__ part_ent,
+    int64_t Q, uint32_t* __restrict__ counters, uint64_t* __restrict__ part_ms, uint64_t* __restrict__ part_ent,
     int32_t* __restrict__ cand_ids, float* __restrict__ cand_logit, float* __restrict__ cand_logprob,
     float* __restrict__ lse) {
   constexpr int EPG = Traits<T>::kPer;
@@ -313,20 +326,22 @@ __global__ __launch_bounds__(kWave* kWavesPerBlock) void topk_sweep_kernel(
     flush<T>(s, nbuf, c0, c1, tau, K, lane, cur_key, cur_id);
   }
 
-  // 6. Publish the partial result.
-  uint2* pe = part_ent + q * K;
-  if (lane < K) pe[lane] = make_uint2(cur_key, cur_id);
-  if (lane == 0) part_ms[q] = make_float2(wm, wsum);
+  // 6. Publish the partial result with stores that are coherent at device scope, and
+  //    wait until they have completed before counting this chunk as done.
+  if (lane < K) store_agent(&part_ent[q * K + lane], pack(cur_key, cur_id));
+  if (lane == 0) store_agent(&part_ms[q], pack(__float_as_uint(wm), __float_as_uint(wsum)));
+  __builtin_amdgcn_s_waitcnt(0);
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
 
-  // 7. The last wave of the row to arrive merges the row.
-  __threadfence();
+  // 7. The last wave of the row to arrive merges the row; its loads are device-coherent
+  //    too, so no cache-wide writeback or invalidation is needed.
   uint32_t prev = 0;
-  if (lane == 0) prev = atomicAdd(&counters[row], 1u);
+  if (lane == 0) prev = __hip_atomic_fetch_add(&counters[row], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   prev = __builtin_amdgcn_readfirstlane(prev);
   if (prev != static_cast<uint32_t>(P - 1)) return;
-  __threadfence();
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
   merge_row<T>(row, P, K, lane, s, part_ms, part_ent, cand_ids, cand_logit, cand_logprob, lse);
-  if (lane == 0) counters[row] = 0;  // leave the workspace ready for the next call
+  if (lane == 0) __hip_atomic_store(&counters[row], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
@@ -340,8 +355,8 @@ TopkPlan topk_plan(int B, int gamma, int64_t V, int K, int dtype) {
   p.parts = static_cast<int>((V + p.chunk - 1) / p.chunk);
   const size_t rows = static_cast<size_t>(B) * gamma;
   p.off_ms = align256(rows * sizeof(uint32_t));
-  p.off_ent = p.off_ms + align256(rows * p.parts * sizeof(float2));
-  p.bytes = p.off_ent + align256(rows * p.parts * static_cast<size_t>(K) * sizeof(uint2));
+  p.off_ent = p.off_ms + align256(rows * p.parts * sizeof(uint64_t));
+  p.bytes = p.off_ent + align256(rows * p.parts * static_cast<size_t>(K) * sizeof(uint64_t));
   return p;
 }
 
@@ -353,8 +368,8 @@ hipError_t launch_topk(const void* logits, int dtype, bool aligned, int B, int g
   const dim3 block(kWave * kWavesPerBlock);
   char* ws = static_cast<char*>(workspace);
   uint32_t* counters = reinterpret_cast<uint32_t*>(ws);
-  float2* ms = reinterpret_cast<float2*>(ws + plan.off_ms);
-  uint2* ent = reinterpret_cast<uint2*>(ws + plan.off_ent);
+  uint64_t* ms = reinterpret_cast<uint64_t*>(ws + plan.off_ms);
+  uint64_t* ent = reinterpret_cast<uint64_t*>(ws + plan.off_ent);
   if (dtype == 1) {
     const uint16_t* x = static_cast<const uint16_t*>(logits);
     if (aligned)

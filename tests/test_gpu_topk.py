@@ -147,3 +147,26 @@ def test_workload_full_size(cfg):
     x = synth.logits(w, 0)
     g = _run(x, w.K)
     parity.check_topk(g, oracle.topk(x, w.K))
+
+
+def test_many_launches_alternating_inputs_are_identical():
+    """Partial results cross waves (and XCDs) through the workspace.  Alternating two
+    inputs over many back-to-back launches on one workspace would expose a merge that
+    read another launch's partials: every output must equal that input's first result."""
+    import torch
+
+    import paper_2609_39972_amd as ubt
+    from gpu_util import dev_values, to_np
+
+    w = synth.WORKLOADS[3]
+    xs = [synth.logits(w, b, rows=np.arange(b * 64, b * 64 + 64)).reshape(4, 16, w.V) for b in range(2)]
+    ts = [dev_values(x) for x in xs]
+    ws = ubt.TopkWorkspace(4, 16, w.V, 8, torch.bfloat16)
+    outs = [ubt.topk(ts[j % 2], 8, workspace=ws) for j in range(200)]
+    torch.cuda.synchronize()
+    outs = [to_np(o) for o in outs]
+    for j in range(2):
+        parity.check_topk(outs[j], oracle.topk(xs[j], 8))
+    for j in range(2, 200):
+        for k in outs[j]:
+            assert np.array_equal(outs[j][k], outs[j % 2][k]), f"launch {j}: {k} differs"
