@@ -28,7 +28,7 @@ sys.path.insert(0, ROOT)
 METRIC = "draft trees/sec and µs/step at B=32, V=151936; achieved HBM GB/s vs peak"
 HBM_PEAK_GBPS = 8000.0
 POOL_BYTES = 512 << 20  # pool size that defeats the 256 MB Infinity Cache
-SWEEP_KERNEL = "topk_sweep_kernel"
+SWEEP_KERNEL = "topk_row_kernel"
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "topk_sweep_zipf-v151936-b32_counters.md")
 
 
@@ -129,8 +129,7 @@ def main() -> int:
         if p == 0:
             host0 = dict(d, phi=phi_np, psi=psi_np)
         step = ubt.DraftStep(w.B, w.gamma, w.V, w.K, w.W, w.budget, phi, psi, to_dev(d["gate"]),
-                             torch.from_numpy(d["anchor"]).to(dev), d["alpha"], d["lam"], w.zeta,
-                             logits_dtype=torch.bfloat16 if w.dtype == "bf16" else torch.float32)
+                             torch.from_numpy(d["anchor"]).to(dev), d["alpha"], d["lam"], w.zeta)
         bufs.append((to_dev_logits(d["logits"]), step))
     torch.cuda.synchronize()
     log(f"inputs resident in HBM ({time.perf_counter() - t0:.1f} s)")
@@ -183,7 +182,7 @@ def main() -> int:
         return float(np.mean([a.elapsed_time(b) for a, b in evs])) * 1e3  # us
 
     n = args.sweep_launches
-    sweep_us = timed(lambda j: ubt.topk(bufs[j % pool][0], w.K, bufs[j % pool][1].ws, bufs[j % pool][1].cand), n)
+    sweep_us = timed(lambda j: ubt.topk(bufs[j % pool][0], w.K, bufs[j % pool][1].cand), n)
     bigram_us = timed(lambda j: ubt.bigram_scores(bufs[j % pool][1].phi, bufs[j % pool][1].psi,
                                                   bufs[j % pool][1].gate, bufs[j % pool][1].anchor,
                                                   bufs[j % pool][1].cand["cand_ids"],

@@ -56,7 +56,7 @@ typedef enum ubt_status {
   UBT_ERR_SHAPE = 2,       /* a size, stride or limit is violated */
   UBT_ERR_VALUE = 3,       /* a scalar argument is out of range (zeta > 0, alpha <= 0, ...) */
   UBT_ERR_UNSUPPORTED = 4, /* a valid combination this build does not handle */
-  UBT_ERR_WORKSPACE = 5,   /* workspace missing, too small or misaligned */
+  UBT_ERR_WORKSPACE = 5,   /* reserved */
   UBT_ERR_HIP = 6          /* a HIP launch failed; see ubt_last_hip_error() */
 } ubt_status_t;
 
@@ -80,24 +80,17 @@ int ubt_last_hip_error(void);
  *            per row; NaN gives unspecified results.  stride_i >= V, stride_b >=
  *            gamma*stride_i.  Rows whose start is 16-byte aligned take the fast path.
  * B, gamma : sequences and rows per sequence, 1 <= gamma <= UBT_MAX_GAMMA, B >= 1.
- * V        : vocabulary size, K <= V < 2^31.
+ * V        : vocabulary size, K <= V, V * sizeof(element) < 2^32 bytes.
  * K        : candidates per row, 1 <= K <= UBT_MAX_K.
  * cand_ids : int32 [B, gamma, K]   token ids ordered by (logit desc, id asc); -0 == +0.
  * cand_logit : float [B, gamma, K] the candidates' logits (exact for both dtypes).
  * cand_logprob : float [B, gamma, K] log q_i(candidate) = logit - lse; may be NULL.
  * lse      : float [B, gamma]      log sum_v exp(u_v) (natural log); may be NULL.
- * workspace: device scratch of at least ubt_topk_workspace_bytes(...) bytes, 256-byte
- *            aligned.  Its first 4*B*gamma bytes are counters that must be zero before
- *            the first call that uses the buffer (hipMemset once after allocation);
- *            every call leaves them zero again.  Calls that may overlap in time need
- *            separate workspaces.
+ * No scratch memory is used: one workgroup handles one row end to end.
  * ------------------------------------------------------------------------------------ */
-size_t ubt_topk_workspace_bytes(int B, int gamma, int64_t V, int K, ubt_dtype_t dt);
-
 ubt_status_t ubt_topk(const void* logits, ubt_dtype_t dt, int B, int gamma, int64_t V,
                       int64_t stride_b, int64_t stride_i, int K, int32_t* cand_ids,
-                      float* cand_logit, float* cand_logprob, float* lse, void* workspace,
-                      size_t workspace_bytes, hipStream_t stream);
+                      float* cand_logit, float* cand_logprob, float* lse, hipStream_t stream);
 
 /* ------------------------------------------------------------------------------------
  * ubt_bigram_scores -- selector scores and normalised transition log-probabilities.

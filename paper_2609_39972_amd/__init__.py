@@ -33,7 +33,7 @@ STATUS = {0: "UBT_OK", 1: "UBT_ERR_NULL", 2: "UBT_ERR_SHAPE", 3: "UBT_ERR_VALUE"
           5: "UBT_ERR_WORKSPACE", 6: "UBT_ERR_HIP"}
 
 # Every symbol include/ubt.h declares.
-EXPORTS = ("ubt_status_str", "ubt_abi_version", "ubt_last_hip_error", "ubt_topk_workspace_bytes", "ubt_topk",
+EXPORTS = ("ubt_status_str", "ubt_abi_version", "ubt_last_hip_error", "ubt_topk",
            "ubt_bigram_scores", "ubt_build_tree", "ubt_tree_mask")
 
 _p = ctypes.c_void_p
@@ -64,9 +64,7 @@ def lib() -> ctypes.CDLL:
         L.ubt_status_str.restype = ctypes.c_char_p
         L.ubt_abi_version.restype = _i32
         L.ubt_last_hip_error.restype = _i32
-        L.ubt_topk_workspace_bytes.argtypes = [_i32, _i32, _i64, _i32, _i32]
-        L.ubt_topk_workspace_bytes.restype = ctypes.c_size_t
-        L.ubt_topk.argtypes = [_p, _i32, _i32, _i32, _i64, _i64, _i64, _i32, _p, _p, _p, _p, _p, ctypes.c_size_t, _p]
+        L.ubt_topk.argtypes = [_p, _i32, _i32, _i32, _i64, _i64, _i64, _i32, _p, _p, _p, _p, _p]
         L.ubt_bigram_scores.argtypes = [_p, _p, _p, _i32, _i64, _i32, _p, _p, _p, _p, _p, _i32, _i32, _i32, _p, _p,
                                         _p]
         L.ubt_build_tree.argtypes = [_p, _p, _p, _i32, _i32, _i32, _i32, _i32, _f32, _p, _p, _p, _p, _p, _p, _p,
@@ -112,22 +110,7 @@ def _contig(t: torch.Tensor, name: str) -> torch.Tensor:
     return t
 
 
-class TopkWorkspace:
-    """Device scratch for :func:`topk` (zeroed once; every call leaves it zeroed)."""
-
-    def __init__(self, B: int, gamma: int, V: int, K: int, dtype: torch.dtype, device="cuda"):
-        code = UBT_BF16 if dtype == torch.bfloat16 else UBT_F32
-        self.nbytes = int(lib().ubt_topk_workspace_bytes(B, gamma, V, K, code))
-        if self.nbytes == 0:
-            raise ValueError("invalid top-K shape")
-        self._buf = torch.zeros(self.nbytes + 256, dtype=torch.uint8, device=device)
-        off = (-self._buf.data_ptr()) % 256
-        self.tensor = self._buf[off:off + self.nbytes]
-        self.shape = (B, gamma, V, K, code)
-
-
-def topk(logits: torch.Tensor, K: int, workspace: TopkWorkspace | None = None, out: dict | None = None,
-         with_logprob: bool = True, stream=None) -> dict:
+def topk(logits: torch.Tensor, K: int, out: dict | None = None, with_logprob: bool = True, stream=None) -> dict:
     """Top-K candidates and softmax statistics of ``logits [B, gamma, V]`` (any strides with
     unit stride along V; e.g. ``u[:, 1:, :]`` of a ``[B, L, V]`` block)."""
     _need_gpu(logits)
@@ -136,8 +119,6 @@ def topk(logits: torch.Tensor, K: int, workspace: TopkWorkspace | None = None, o
     B, gamma, V = logits.shape
     code = _dtype_code(logits)
     dev = logits.device
-    if workspace is None:
-        workspace = TopkWorkspace(B, gamma, V, K, logits.dtype, dev)
     if out is None:
         out = dict(cand_ids=torch.empty(B, gamma, K, dtype=torch.int32, device=dev),
                    cand_logit=torch.empty(B, gamma, K, dtype=torch.float32, device=dev),
@@ -145,7 +126,7 @@ def topk(logits: torch.Tensor, K: int, workspace: TopkWorkspace | None = None, o
                    lse=torch.empty(B, gamma, dtype=torch.float32, device=dev))
     st = lib().ubt_topk(_ptr(logits), code, B, gamma, V, logits.stride(0), logits.stride(1), K,
                         _ptr(out["cand_ids"]), _ptr(out["cand_logit"]), _ptr(out.get("cand_logprob")),
-                        _ptr(out.get("lse")), _ptr(workspace.tensor), workspace.nbytes, _stream(stream))
+                        _ptr(out.get("lse")), _stream(stream))
     _check("ubt_topk", st)
     return out
 
@@ -241,13 +222,12 @@ class DraftStep:
 
     def __init__(self, B: int, gamma: int, V: int, K: int, W: int, budget: int, phi: torch.Tensor,
                  psi: torch.Tensor, gate: torch.Tensor, anchor: torch.Tensor, alpha, lam, zeta: float = 0.0,
-                 logits_dtype: torch.dtype = torch.bfloat16, with_delta: bool = False, debug: bool = False):
+                 with_delta: bool = False, debug: bool = False):
         dev = phi.device
         self.shape = (B, gamma, V, K, W, budget)
         self.phi, self.psi, self.gate, self.anchor = phi, psi, gate, anchor
         self.alpha, self.lam, self.zeta = alpha, lam, zeta
         self.W, self.budget, self.K = W, budget, K
-        self.ws = TopkWorkspace(B, gamma, V, K, logits_dtype, dev)
         f32 = dict(dtype=torch.float32, device=dev)
         self.cand = dict(cand_ids=torch.empty(B, gamma, K, dtype=torch.int32, device=dev),
                          cand_logit=torch.empty(B, gamma, K, **f32), cand_logprob=torch.empty(B, gamma, K, **f32),
@@ -257,7 +237,7 @@ class DraftStep:
         self.tree = tree_outputs(B, gamma, W, budget, dev, True, debug)
 
     def run(self, logits: torch.Tensor, stream=None) -> dict:
-        topk(logits, self.K, self.ws, self.cand, stream=stream)
+        topk(logits, self.K, self.cand, stream=stream)
         bigram_scores(self.phi, self.psi, self.gate, self.anchor, self.cand["cand_ids"], self.cand["cand_logit"],
                       self.alpha, self.lam, self.sel, stream=stream)
         build_tree(self.anchor, self.cand["cand_ids"], self.sel["logq"], self.W, self.budget, self.zeta, self.tree,

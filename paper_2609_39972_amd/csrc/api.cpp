@@ -42,29 +42,20 @@ int ubt_abi_version(void) { return UBT_ABI_VERSION; }
 
 int ubt_last_hip_error(void) { return g_last_hip_error; }
 
-size_t ubt_topk_workspace_bytes(int B, int gamma, int64_t V, int K, ubt_dtype_t dt) {
-  if (B < 1 || gamma < 1 || gamma > UBT_MAX_GAMMA || K < 1 || K > UBT_MAX_K || V < K || V >= (int64_t(1) << 31) ||
-      !valid_dtype(dt))
-    return 0;
-  return ubt::topk_plan(B, gamma, V, K, static_cast<int>(dt)).bytes;
-}
-
 ubt_status_t ubt_topk(const void* logits, ubt_dtype_t dt, int B, int gamma, int64_t V, int64_t stride_b,
                       int64_t stride_i, int K, int32_t* cand_ids, float* cand_logit, float* cand_logprob, float* lse,
-                      void* workspace, size_t workspace_bytes, hipStream_t stream) {
+                      hipStream_t stream) {
   if (!logits || !cand_ids || !cand_logit) return UBT_ERR_NULL;
   if (!valid_dtype(dt)) return UBT_ERR_VALUE;
   if (B < 1 || gamma < 1 || gamma > UBT_MAX_GAMMA || K < 1 || K > UBT_MAX_K || V < K || V >= (int64_t(1) << 31))
     return UBT_ERR_SHAPE;
   if (stride_i < V || stride_b < static_cast<int64_t>(gamma) * stride_i) return UBT_ERR_SHAPE;
-  if (static_cast<int64_t>(B) * gamma > (int64_t(1) << 31) / 8) return UBT_ERR_SHAPE;
-  const ubt::TopkPlan plan = ubt::topk_plan(B, gamma, V, K, static_cast<int>(dt));
-  if (!workspace || workspace_bytes < plan.bytes || (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
-    return UBT_ERR_WORKSPACE;
+  if (static_cast<int64_t>(B) * gamma > 0x7FFFFFFF) return UBT_ERR_SHAPE;
+  if (V * (dt == UBT_BF16 ? 2 : 4) >= (int64_t(1) << 32)) return UBT_ERR_SHAPE;  // a row is one buffer range
   const int64_t es = dt == UBT_BF16 ? 2 : 4;
   const bool aligned = aligned16(logits) && (stride_b * es) % 16 == 0 && (stride_i * es) % 16 == 0;
-  return hip_status(ubt::launch_topk(logits, static_cast<int>(dt), aligned, B, gamma, V, stride_b, stride_i, K, plan,
-                                     workspace, cand_ids, cand_logit, cand_logprob, lse, stream));
+  return hip_status(ubt::launch_topk(logits, static_cast<int>(dt), aligned, B, gamma, V, stride_b, stride_i, K,
+                                     cand_ids, cand_logit, cand_logprob, lse, stream));
 }
 
 ubt_status_t ubt_bigram_scores(const void* phi_tab, const void* psi_tab, const void* gate, ubt_dtype_t feat_dt,

@@ -4,24 +4,30 @@
 // Sets": C_i = the K tokens of largest q_i, ranked here on the logits (softmax is
 // increasing) with ties to the lower token id.
 //
-// One HBM pass.  A row of V logits is cut into P chunks of 64 lanes x 16 groups x 16 B
-// (8192 bf16 or 4096 fp32 elements); each wavefront owns one chunk and keeps it in
-// registers.  Per 16-byte group it takes the group maximum and the exp-sum relative to
-// it, folds both into a running per-lane (max, sum), and remembers the group maximum.
-// The K-th largest lane maximum tau bounds the chunk's K-th largest element from below,
-// so only groups whose maximum reaches tau can hold a top-K element; those few groups
-// go to LDS, and a ballot-driven radix selection picks the chunk's top K.  Every wave
-// writes (max, sum) and its K candidates to the workspace; the last wave of a row to
-// finish (atomic counter) merges the P partials into the row's LSE and sorted top-K.
+// One HBM pass, one workgroup per row.  The row is cut into sub-chunks of 64 lanes x 4
+// groups x 16 B (2048 bf16 or 1024 fp32 elements), dealt round-robin to the waves of
+// the workgroup; each wave streams its sub-chunks with the next one already in flight
+// (two register buffers, nontemporal 16-byte loads).  Per 16-byte group a lane takes the
+// maximum and the exp-sum relative to it and folds both into its running (max, sum).
+//
+// Top-K: a group can hold a top-K element only if its maximum reaches a threshold that
+// is known to be at most the row's K-th largest element.  After every wave has
+// streamed its first sub-chunk, the workgroup takes T = the K-th largest of all lane
+// maxima seen so far (at least K elements reach it); from then on only groups whose
+// maximum reaches T are buffered in LDS.  A wave whose buffer fills merges it into its
+// running top-K with a ballot-driven radix selection and from then on needs strictly
+// more than its K-th candidate (its later sub-chunks hold larger token ids).  At the
+// end every wave merges what is left, and the waves' (max, sum) and candidates meet in
+// LDS, where one wave writes the row's LSE and sorted top-K.
 #include "ubt_device.h"
 #include "ubt_launch.h"
 
 namespace ubt {
 namespace {
 
-constexpr int kGroups = 16;         // 16-byte groups per lane per chunk
-constexpr int kWavesPerBlock = 4;   // independent waves per workgroup
-constexpr int kCapGroups = 32;      // LDS candidate-group buffer per wave and round
+constexpr int kSubGroups = 4;     // 16-byte groups per lane per sub-chunk
+constexpr int kWaves = 8;         // waves per workgroup
+constexpr int kCapGroups = 64;    // LDS candidate-group buffer per wave
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
@@ -32,11 +38,11 @@ template <>
 struct Traits<uint16_t> {  // bf16 bit patterns
   static constexpr int kPer = 8;
   static constexpr int kKeyBits = 16;
-    __device__ static float elem(const u32x4& v, int j) {
+  static constexpr uint32_t kNegInfBits = 0xFF80u;
+  __device__ static float elem(const u32x4& v, int j) {
     const uint32_t w = v[j >> 1];
     return __uint_as_float((j & 1) ? (w & 0xFFFF0000u) : (w << 16));
   }
-  __device__ static uint32_t elem_bits(const u32x4& v, int j) { return (v[j >> 1] >> (16 * (j & 1))) & 0xFFFFu; }
   __device__ static uint32_t key_bits(uint32_t bits) { return bf16_key(bits); }
   __device__ static uint32_t key_value(float f) { return bf16_key(__float_as_uint(f) >> 16); }
   __device__ static float from_key(uint32_t k) { return bf16_key_value(k); }
@@ -52,8 +58,8 @@ template <>
 struct Traits<float> {
   static constexpr int kPer = 4;
   static constexpr int kKeyBits = 32;
+  static constexpr uint32_t kNegInfBits = 0xFF800000u;
   __device__ static float elem(const u32x4& v, int j) { return __uint_as_float(v[j]); }
-  __device__ static uint32_t elem_bits(const u32x4& v, int j) { return v[j]; }
   __device__ static uint32_t key_bits(uint32_t bits) { return f32_key(__uint_as_float(bits)); }
   __device__ static uint32_t key_value(float f) { return f32_key(f); }
   __device__ static float from_key(uint32_t k) { return f32_key_value(k); }
@@ -65,41 +71,70 @@ struct Traits<float> {
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
 
-// Stores and loads that are coherent at device (agent) scope: partial results travel
-// between waves on different XCDs without cache-wide writeback or invalidation.
-__device__ __forceinline__ void store_agent(uint64_t* p, uint64_t v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ uint64_t load_agent(const uint64_t* p) {
-  return __hip_atomic_load(const_cast<uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ uint64_t pack(uint32_t lo, uint32_t hi) {
-  return static_cast<uint64_t>(lo) | (static_cast<uint64_t>(hi) << 32);
-}
-
-// Group of EPG elements starting at element e0 of row `rp`, elements >= lim read as -inf.
-template <typename T, bool kAligned>
-__device__ __forceinline__ u32x4 load_group_checked(const T* rp, int64_t e0, int64_t lim) {
-  constexpr int EPG = Traits<T>::kPer;
-  u32x4 v;
-  if (kAligned && e0 + EPG <= lim) return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(rp + e0));
-  Traits<T>::set_neg_inf(v);
-#pragma unroll
-  for (int j = 0; j < EPG; ++j)
-    if (e0 + j < lim) Traits<T>::set_elem(v, j, Traits<T>::load_elem(rp + e0 + j));
-  return v;
-}
-
 struct WaveLds {
-  u32x4 data[kCapGroups];      // buffered candidate groups
-  uint32_t base[kCapGroups];   // chunk-relative index of each group's first element
-  uint2 stage[kWave];          // compaction staging (key, id)
+  u32x4 data[kCapGroups];     // buffered candidate groups
+  uint32_t base[kCapGroups];  // row index of each group's first element
+  uint2 stage[kWave];         // compaction staging (key, id)
 };
+
+struct RowLds {
+  WaveLds wave[kWaves];
+  uint2 part[kWaves][kWave];      // each wave's candidates (key, id)
+  float2 ms[kWaves];              // each wave's (max, sum)
+  uint32_t lane_max[kWaves * kWave];  // the largest lane maxima of every wave's first sub-chunk
+  uint32_t n_lane_max;
+};
+
+// A buffer resource covering one row: loads address it with a 32-bit offset in a scalar
+// descriptor instead of a 64-bit address per lane, and offsets past the row read zero.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t row_resource(const void* row, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(row), 0, static_cast<int>(bytes), 0x00020000);
+}
+
+constexpr int kNontemporal = 2;  // cache policy of the streaming loads (read once)
+
+// Loads a full sub-chunk [c0, c0 + SUB) of an aligned row.  With `live` false the loads
+// are still issued, at an offset past the buffer range: they read zeros without touching
+// memory, and keep the number of loads in flight the same on every path, so the waits for
+// the current sub-chunk never include the prefetched one.
+template <typename T>
+__device__ __forceinline__ void load_full(u32x4 (&buf)[kSubGroups], __amdgpu_buffer_rsrc_t rsrc, int64_t c0,
+                                          int lane, bool live = true) {
+  constexpr int EPG = Traits<T>::kPer;
+  const uint32_t off = live ? static_cast<uint32_t>((c0 + lane * EPG) * sizeof(T)) : 0xFFFF0000u;
+#pragma unroll
+  for (int g = 0; g < kSubGroups; ++g)
+    buf[g] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                           rsrc, off + g * kWave * EPG * sizeof(T), 0, kNontemporal));
+}
+
+// Loads sub-chunk elements [c0, c0 + SUB) of a row that may end inside it or be
+// unaligned; elements >= V read as -inf.  A 16-byte load that would cross the end of the
+// row is replaced by element loads.
+template <typename T, bool kAligned>
+__device__ __forceinline__ void load_checked(u32x4 (&buf)[kSubGroups], __amdgpu_buffer_rsrc_t rsrc, const T* rp,
+                                             int64_t c0, int64_t V, int lane) {
+  constexpr int EPG = Traits<T>::kPer;
+  constexpr int64_t SUB = static_cast<int64_t>(kSubGroups) * kWave * EPG;
+  const int lim = static_cast<int>(V - c0 < SUB ? V - c0 : SUB);
+#pragma unroll
+  for (int g = 0; g < kSubGroups; ++g) {
+    const int r0 = (g * kWave + lane) * EPG;
+    if (kAligned && r0 + EPG <= lim) {
+      buf[g] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                             rsrc, static_cast<uint32_t>((c0 + r0) * sizeof(T)), 0, kNontemporal));
+    } else {
+      Traits<T>::set_neg_inf(buf[g]);
+      for (int j = 0; j < EPG; ++j)
+        if (r0 + j < lim) Traits<T>::set_elem(buf[g], j, Traits<T>::load_elem(rp + c0 + r0 + j));
+    }
+  }
+}
 
 // Compacts the selected entries (at most 64) into lanes 0.. of (out_key, out_id).
 template <int R>
-__device__ __forceinline__ int compact(WaveLds& s, const uint32_t (&key)[R], const uint32_t (&sub)[R],
-                                       const uint64_t (&sel)[R], int lane, uint32_t& out_key, uint32_t& out_id) {
+__device__ __forceinline__ void compact(WaveLds& s, const uint32_t (&key)[R], const uint32_t (&sub)[R],
+                                        const uint64_t (&sel)[R], int lane, uint32_t& out_key, uint32_t& out_id) {
   int n = 0;
 #pragma unroll
   for (int r = 0; r < R; ++r) {
@@ -111,12 +146,13 @@ __device__ __forceinline__ int compact(WaveLds& s, const uint32_t (&key)[R], con
   __builtin_amdgcn_wave_barrier();
   out_key = v.x;
   out_id = v.y;
-  return n;
 }
 
-// Merges the buffered candidate groups into the running top-K (lanes 0..K-1).
+// Merges the buffered candidate groups into the running top-K (lanes 0..K-1).  Elements
+// whose key does not pass the threshold (key >= thr, or key > thr when strict) are
+// dropped: they cannot be in the top K.
 template <typename T, int RB>
-__device__ __forceinline__ void flush_buffer(WaveLds& s, int nbuf, int64_t c0, int64_t c1, uint32_t tau, int K,
+__device__ __forceinline__ void flush_buffer(WaveLds& s, int g0, int nbuf, int64_t V, uint32_t thr, bool strict, int K,
                                              int lane, uint32_t& cur_key, uint32_t& cur_id) {
   constexpr int EPG = Traits<T>::kPer;
   uint32_t key[RB + 1], sub[RB + 1];
@@ -127,16 +163,16 @@ __device__ __forceinline__ void flush_buffer(WaveLds& s, int nbuf, int64_t c0, i
 #pragma unroll
   for (int r = 0; r < RB; ++r) {
     const int e = r * kWave + lane;
-    const int g = e / EPG, j = e % EPG;
+    const int g = g0 + e / EPG, j = e % EPG;
     uint32_t k = 0, id = 0;
     if (g < nbuf) {
       const uint32_t word = reinterpret_cast<const uint32_t*>(&s.data[g])[j * 4 / EPG];
       const uint32_t bits = EPG == 8 ? (word >> (16 * (j & 1))) & 0xFFFFu : word;
-      const int64_t gid = c0 + s.base[g] + j;
-      if (gid < c1) {
+      const int64_t gid = static_cast<int64_t>(s.base[g]) + j;
+      if (gid < V) {
         k = Traits<T>::key_bits(bits);
         id = static_cast<uint32_t>(gid);
-        if (k < tau) k = 0;  // below the chunk's K-th largest: never selected
+        if (strict ? k <= thr : k < thr) k = 0;
       }
     }
     key[r + 1] = k;
@@ -147,45 +183,318 @@ __device__ __forceinline__ void flush_buffer(WaveLds& s, int nbuf, int64_t c0, i
   compact<RB + 1>(s, key, sub, sel, lane, cur_key, cur_id);
 }
 
+// Merges nbuf buffered groups into the running top-K; returns the new (key, id) pair of
+// this lane (lanes 0..K-1 hold the top K).
 template <typename T>
-__device__ __forceinline__ void flush(WaveLds& s, int nbuf, int64_t c0, int64_t c1, uint32_t tau, int K, int lane,
-                                      uint32_t& cur_key, uint32_t& cur_id) {
+__device__ __forceinline__ uint2 flush(WaveLds& s, int nbuf, int64_t V, uint32_t thr, bool strict, int K, int lane,
+                                       uint32_t cur_key, uint32_t cur_id) {
   constexpr int EPG = Traits<T>::kPer;
-  if (nbuf == 0) return;
-  const int elems = nbuf * EPG;
-  if (elems <= kWave)
-    flush_buffer<T, 1>(s, nbuf, c0, c1, tau, K, lane, cur_key, cur_id);
-  else if (elems <= 2 * kWave)
-    flush_buffer<T, 2>(s, nbuf, c0, c1, tau, K, lane, cur_key, cur_id);
-  else if (elems <= 4 * kWave)
-    flush_buffer<T, 4>(s, nbuf, c0, c1, tau, K, lane, cur_key, cur_id);
-  else
-    flush_buffer<T, kCapGroups * EPG / kWave>(s, nbuf, c0, c1, tau, K, lane, cur_key, cur_id);
+  constexpr int kSlice = 4 * kWave / EPG;  // groups per selection pass (four register rows)
+  for (int g0 = 0; g0 < nbuf; g0 += kSlice) {
+    const int elems = (nbuf - g0 < kSlice ? nbuf - g0 : kSlice) * EPG;
+    if (elems <= kWave)
+      flush_buffer<T, 1>(s, g0, nbuf, V, thr, strict, K, lane, cur_key, cur_id);
+    else if (elems <= 2 * kWave)
+      flush_buffer<T, 2>(s, g0, nbuf, V, thr, strict, K, lane, cur_key, cur_id);
+    else
+      flush_buffer<T, 4>(s, g0, nbuf, V, thr, strict, K, lane, cur_key, cur_id);
+  }
+  return make_uint2(cur_key, cur_id);
 }
 
-// The last wave of a row: merges the P partial results into LSE and the sorted top-K.
+// Smallest key among the K candidates held in lanes 0..K-1.
+__device__ __forceinline__ uint32_t kth_key(uint32_t cur_key, int K, int lane) {
+  uint32_t mn = lane < K ? cur_key : 0xFFFFFFFFu;
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) mn = min(mn, static_cast<uint32_t>(__shfl_xor(static_cast<int>(mn), o, kWave)));
+  return mn;
+}
+
+// Per-wave running state of the streaming pass.
+struct WaveState {
+  float lm, ls;   // lane's running max and exp-sum relative to it
+  uint32_t thr;   // candidate threshold key (0 = none): groups need max key >= thr
+  int nbuf;       // groups waiting in the LDS buffer
+  bool overflow;  // a group that passed could not be buffered
+};
+
+// Max and exp-sum of one sub-chunk, folded into the lane's running (max, sum); returns
+// the group maxima in gmax and the lane's maximum over the sub-chunk.
 template <typename T>
-__device__ void merge_row(int64_t row, int P, int K, int lane, WaveLds& s, const uint64_t* __restrict__ part_ms,
-                          const uint64_t* __restrict__ part_ent, int32_t* __restrict__ cand_ids,
-                          float* __restrict__ cand_logit, float* __restrict__ cand_logprob, float* __restrict__ lse) {
-  const uint64_t* ms = part_ms + row * P;
-  float m = neg_inf();
-  for (int p = lane; p < P; p += kWave) m = fmaxf(m, __uint_as_float(static_cast<uint32_t>(load_agent(&ms[p]))));
-  m = wave_max(m);
-  float sum = 0.f;
-  for (int p = lane; p < P; p += kWave) {
-    const uint64_t v = load_agent(&ms[p]);
-    const float pm = __uint_as_float(static_cast<uint32_t>(v));
-    const float ps = __uint_as_float(static_cast<uint32_t>(v >> 32));
-    if (pm != neg_inf()) sum += ps * fast_exp2((pm - m) * kLog2e);
+__device__ __forceinline__ float reduce_sub(const u32x4 (&buf)[kSubGroups], float (&gmax)[kSubGroups], float& lm,
+                                            float& ls) {
+  constexpr int EPG = Traits<T>::kPer;
+  float sub_max = neg_inf();
+#pragma unroll
+  for (int g = 0; g < kSubGroups; ++g) {
+    float x[EPG];
+#pragma unroll
+    for (int j = 0; j < EPG; ++j) x[j] = Traits<T>::elem(buf[g], j);
+    float gm = x[0];
+#pragma unroll
+    for (int j = 1; j + 1 < EPG; j += 2) gm = fmaxf(gm, fmaxf(x[j], x[j + 1]));
+    if (EPG % 2 == 0) gm = fmaxf(gm, x[EPG - 1]);
+    gmax[g] = gm;
+    sub_max = fmaxf(sub_max, gm);
+    // exp-sum relative to the group maximum (0 for a group of -inf values)
+    const bool finite = gm != neg_inf();
+    const float off = finite ? gm * kLog2e : 0.f;
+    float gs = 0.f;
+#pragma unroll
+    for (int j = 0; j < EPG; ++j) gs += fast_exp2(fmaf(x[j], kLog2e, -off));
+    // fold (gm, gs) into (lm, ls) with one exponential: the smaller maximum is rescaled
+    const float hi = fmaxf(lm, gm);
+    const float e = fast_exp2(-fabsf(gm - lm) * kLog2e);
+    const float up = fmaf(ls, e, gs);  // gm is the new maximum
+    const float keep = fmaf(gs, e, ls);
+    const float nls = gm > lm ? up : keep;
+    ls = finite ? nls : ls;
+    lm = finite ? hi : lm;
   }
-  sum = wave_sum(sum);
-  const float l = (m == neg_inf()) ? neg_inf() : m + fast_log2(sum) * kLn2;
+  return sub_max;
+}
+
+// Group maxima of one sub-chunk (re-scan path).
+template <typename T>
+__device__ __forceinline__ void group_max_sub(const u32x4 (&buf)[kSubGroups], float (&gmax)[kSubGroups]) {
+  constexpr int EPG = Traits<T>::kPer;
+#pragma unroll
+  for (int g = 0; g < kSubGroups; ++g) {
+    float gm = Traits<T>::elem(buf[g], 0);
+#pragma unroll
+    for (int j = 1; j < EPG; ++j) gm = fmaxf(gm, Traits<T>::elem(buf[g], j));
+    gmax[g] = gm;
+  }
+}
+
+// Bit g set if group g of this lane is inside the row and its maximum passes the
+// threshold (key >= thr, or key > thr when strict; thr = 0 passes everything).
+template <typename T>
+__device__ __forceinline__ uint32_t passing_groups(const float (&gmax)[kSubGroups], int64_t c0, int64_t V,
+                                                   uint32_t thr, bool strict, int lane) {
+  constexpr int EPG = Traits<T>::kPer;
+  constexpr int64_t SUB = static_cast<int64_t>(kSubGroups) * kWave * EPG;
+  const float thr_v = Traits<T>::from_key(thr);
+  const bool full = c0 + SUB <= V;
+  const int lim = full ? static_cast<int>(SUB) : static_cast<int>(V - c0);
+  uint32_t pending = 0;
+#pragma unroll
+  for (int g = 0; g < kSubGroups; ++g) {
+    const bool valid = full || (g * kWave + lane) * EPG < lim;
+    const bool pass = thr == 0 || (strict ? gmax[g] > thr_v : gmax[g] >= thr_v);
+    if (valid && pass) pending |= 1u << g;
+  }
+  return pending;
+}
+
+// Appends this lane's pending groups to the wave's LDS buffer; returns the groups that
+// did not fit.
+template <typename T>
+__device__ __forceinline__ uint32_t buffer_groups(const u32x4 (&buf)[kSubGroups], uint32_t pending, int64_t c0,
+                                                  int lane, WaveLds& s, int& nbuf) {
+  constexpr int EPG = Traits<T>::kPer;
+#pragma unroll
+  for (int g = 0; g < kSubGroups; ++g) {
+    const bool hit = (pending >> g) & 1u;
+    const uint64_t m = ballot(hit);
+    if (m) {
+      const int pos = nbuf + static_cast<int>(lanes_below(m));
+      if (hit && pos < kCapGroups) {
+        s.data[pos] = buf[g];
+        s.base[pos] = static_cast<uint32_t>(c0) + static_cast<uint32_t>((g * kWave + lane) * EPG);
+        pending &= ~(1u << g);
+      }
+      nbuf = nbuf + popc(m) < kCapGroups ? nbuf + popc(m) : kCapGroups;
+    }
+  }
+  return pending;
+}
+
+// Exact fallback for a wave whose buffer overflowed (e.g. rows with long runs of equal
+// values): re-reads its sub-chunks and keeps a running top-K, merging the buffer each
+// time it fills and tightening the threshold once K candidates are held (later groups
+// carry larger ids, so they must beat the K-th candidate strictly).
+template <typename T, bool kAligned>
+__device__ uint2 rescan(__amdgpu_buffer_rsrc_t rsrc, const T* rp, int64_t first, int64_t nsub, int nw, int64_t V,
+                        uint32_t thr, int K, int lane, WaveLds& s) {
+  constexpr int64_t SUB = static_cast<int64_t>(kSubGroups) * kWave * Traits<T>::kPer;
+  uint32_t cur_key = 0, cur_id = 0;
+  bool strict = false;
+  int nbuf = 0;
+  for (int64_t sc = first; sc < nsub; sc += nw) {
+    u32x4 buf[kSubGroups];
+    float gmax[kSubGroups];
+    load_checked<T, kAligned>(buf, rsrc, rp, sc * SUB, V, lane);
+    group_max_sub<T>(buf, gmax);
+    uint32_t pending = passing_groups<T>(gmax, sc * SUB, V, thr, strict, lane);
+    while (ballot(pending != 0)) {
+      pending = buffer_groups<T>(buf, pending, sc * SUB, lane, s, nbuf);
+      if (ballot(pending != 0)) {
+        __builtin_amdgcn_wave_barrier();
+        const uint2 c = flush<T>(s, nbuf, V, thr, strict, K, lane, cur_key, cur_id);
+        cur_key = c.x;
+        cur_id = c.y;
+        nbuf = 0;
+      }
+    }
+    if (nbuf > 0) {
+      __builtin_amdgcn_wave_barrier();
+      const uint2 c = flush<T>(s, nbuf, V, thr, strict, K, lane, cur_key, cur_id);
+      cur_key = c.x;
+      cur_id = c.y;
+      nbuf = 0;
+    }
+    if (popc(ballot(cur_key != 0)) >= K) {
+      const uint32_t mn = kth_key(cur_key, K, lane);
+      if (mn > thr || (mn == thr && !strict)) {
+        thr = mn;
+        strict = true;
+      }
+    }
+  }
+  return make_uint2(cur_key, cur_id);
+}
+
+template <typename T, bool kAligned>
+__global__ __launch_bounds__(kWave* kWaves, 4) void topk_row_kernel(const T* __restrict__ logits, int gamma,
+                                                                    int64_t V, int64_t stride_b, int64_t stride_i,
+                                                                    int K, int32_t* __restrict__ cand_ids,
+                                                                    float* __restrict__ cand_logit,
+                                                                    float* __restrict__ cand_logprob,
+                                                                    float* __restrict__ lse) {
+  constexpr int EPG = Traits<T>::kPer;
+  constexpr int64_t SUB = static_cast<int64_t>(kSubGroups) * kWave * EPG;
+  __shared__ RowLds lds;
+  const int nw = blockDim.x / kWave;
+  // Wave-uniform, and known to be: the sub-chunk indices and offsets derived from it
+  // then live in scalar registers.
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const int lane = threadIdx.x % kWave;
+  const int64_t row = blockIdx.x;
+  const int64_t b = row / gamma, i = row - b * gamma;
+  const T* rp = logits + b * stride_b + i * stride_i;
+  const __amdgpu_buffer_rsrc_t rsrc = row_resource(rp, static_cast<uint32_t>(V * static_cast<int64_t>(sizeof(T))));
+  const int64_t nsub = (V + SUB - 1) / SUB;
+  WaveLds& s = lds.wave[w];
+
+  if (threadIdx.x == 0) lds.n_lane_max = 0;
+  WaveState st{neg_inf(), 0.f, 0u, 0, false};
+  u32x4 bufA[kSubGroups], bufB[kSubGroups];
+  float gmax[kSubGroups];
+  // Full sub-chunks stream through the fast path (aligned rows only); the ragged last
+  // sub-chunk, or every sub-chunk of an unaligned row, goes through checked loads.
+  const int64_t nfull = kAligned ? V / SUB : 0;
+  int64_t sc = w;
+
+  // First full sub-chunk of every wave, then one workgroup-wide threshold.
+  load_full<T>(bufA, rsrc, sc * SUB, lane, sc < nfull);
+  load_full<T>(bufB, rsrc, (sc + nw) * SUB, lane, sc + nw < nfull);
+  __syncthreads();  // n_lane_max is cleared
+  {
+    uint32_t lkey = 0;
+    if (sc < nfull) lkey = Traits<T>::key_value(reduce_sub<T>(bufA, gmax, st.lm, st.ls));
+    // This wave's K largest lane maxima (more with ties) join the workgroup's union.
+    const uint32_t lk[1] = {lkey};
+    const uint64_t all[1] = {~0ull};
+    const uint32_t tw = wave_kth_largest<1>(lk, all, K, Traits<T>::kKeyBits);
+    const bool mine = lkey != 0 && lkey >= tw;
+    const uint64_t m = ballot(mine);
+    uint32_t base = 0;
+    if (lane == 0 && m) base = atomicAdd(&lds.n_lane_max, static_cast<uint32_t>(popc(m)));
+    base = __builtin_amdgcn_readfirstlane(base);
+    if (mine) lds.lane_max[base + lanes_below(m)] = lkey;
+  }
+  __syncthreads();
+  {
+    // T = the K-th largest lane maximum of the workgroup: a lower bound of the row's
+    // K-th largest element, so every top-K element sits in a group reaching it.
+    const int n = static_cast<int>(lds.n_lane_max);
+    if (n <= kWave) {
+      const uint32_t k1[1] = {lane < n ? lds.lane_max[lane] : 0u};
+      const uint64_t l1[1] = {~0ull};
+      st.thr = wave_kth_largest<1>(k1, l1, K, Traits<T>::kKeyBits);
+    } else {
+      // Many ties among the lane maxima: count straight from LDS.
+      uint32_t t = 0;
+      for (int bit = Traits<T>::kKeyBits - 1; bit >= 0; --bit) {
+        const uint32_t cand = t | (1u << bit);
+        int cnt = 0;
+        for (int e0 = 0; e0 < n; e0 += kWave) cnt += popc(ballot(e0 + lane < n && lds.lane_max[e0 + lane] >= cand));
+        if (cnt >= K) t = cand;
+      }
+      st.thr = t;
+    }
+  }
+  if (sc < nfull) {
+    const uint32_t p = passing_groups<T>(gmax, sc * SUB, V, st.thr, false, lane);
+    if (ballot(p != 0) && ballot(buffer_groups<T>(bufA, p, sc * SUB, lane, s, st.nbuf) != 0)) st.overflow = true;
+  }
+  sc += nw;
+
+  // Remaining full sub-chunks, the next one always in flight.
+  while (sc < nfull) {
+    load_full<T>(bufA, rsrc, (sc + nw) * SUB, lane, sc + nw < nfull);
+    reduce_sub<T>(bufB, gmax, st.lm, st.ls);
+    if (!st.overflow) {
+      const uint32_t p = passing_groups<T>(gmax, sc * SUB, V, st.thr, false, lane);
+      if (ballot(p != 0) && ballot(buffer_groups<T>(bufB, p, sc * SUB, lane, s, st.nbuf) != 0)) st.overflow = true;
+    }
+    sc += nw;
+    if (sc >= nfull) break;
+    load_full<T>(bufB, rsrc, (sc + nw) * SUB, lane, sc + nw < nfull);
+    reduce_sub<T>(bufA, gmax, st.lm, st.ls);
+    if (!st.overflow) {
+      const uint32_t p = passing_groups<T>(gmax, sc * SUB, V, st.thr, false, lane);
+      if (ballot(p != 0) && ballot(buffer_groups<T>(bufA, p, sc * SUB, lane, s, st.nbuf) != 0)) st.overflow = true;
+    }
+    sc += nw;
+  }
+
+  // Ragged or unaligned sub-chunks: this wave's share of [nfull, nsub).
+  for (int64_t sr = nfull + ((w - nfull % nw) + nw) % nw; sr < nsub; sr += nw) {
+    load_checked<T, kAligned>(bufA, rsrc, rp, sr * SUB, V, lane);
+    reduce_sub<T>(bufA, gmax, st.lm, st.ls);
+    if (!st.overflow) {
+      const uint32_t p = passing_groups<T>(gmax, sr * SUB, V, st.thr, false, lane);
+      if (ballot(p != 0) && ballot(buffer_groups<T>(bufA, p, sr * SUB, lane, s, st.nbuf) != 0)) st.overflow = true;
+    }
+  }
+
+  // This wave's top-K: one selection over the buffered groups, or the exact re-scan.
+  uint32_t cur_key = 0, cur_id = 0;
+  if (!st.overflow) {
+    if (st.nbuf > 0) {
+      __builtin_amdgcn_wave_barrier();
+      const uint2 c = flush<T>(s, st.nbuf, V, st.thr, false, K, lane, 0u, 0u);
+      cur_key = c.x;
+      cur_id = c.y;
+    }
+  } else {
+    const uint2 c = rescan<T, kAligned>(rsrc, rp, w, nsub, nw, V, st.thr, K, lane, s);
+    cur_key = c.x;
+    cur_id = c.y;
+  }
+
+  // The wave's (max, sum) and candidates.
+  const float wm = wave_max(st.lm);
+  const float wsum = wave_sum((st.lm == neg_inf()) ? 0.f : st.ls * fast_exp2((st.lm - wm) * kLog2e));
+  lds.part[w][lane] = make_uint2(lane < K ? cur_key : 0u, cur_id);
+  if (lane == 0) lds.ms[w] = make_float2(wm, wsum);
+  __syncthreads();
+  if (w != 0) return;
+
+  // Wave 0 merges the row.
+  float m = lane < nw ? lds.ms[lane].x : neg_inf();
+  m = wave_max(m);
+  float e = 0.f;
+  if (lane < nw && lds.ms[lane].x != neg_inf()) e = lds.ms[lane].y * fast_exp2((lds.ms[lane].x - m) * kLog2e);
+  e = wave_sum(e);
+  const float l = (m == neg_inf()) ? neg_inf() : m + fast_log2(e) * kLn2;
 
   constexpr int RB = 4;
-  const uint64_t* ent = part_ent + row * static_cast<int64_t>(P) * K;
-  const int total = P * K;
-  uint32_t cur_key = 0, cur_id = 0;
+  const int total = nw * K;
+  cur_key = 0;
+  cur_id = 0;
   for (int base = 0; base < total; base += RB * kWave) {
     uint32_t key[RB + 1], sub[RB + 1];
     uint64_t live[RB + 1], sel[RB + 1];
@@ -194,16 +503,12 @@ __device__ void merge_row(int64_t row, int P, int K, int lane, WaveLds& s, const
     live[0] = ballot(cur_key != 0);
 #pragma unroll
     for (int r = 0; r < RB; ++r) {
-      const int e = base + r * kWave + lane;
-      uint32_t k = 0, id = 0;
-      if (e < total) {
-        const uint64_t v = load_agent(&ent[e]);
-        k = static_cast<uint32_t>(v);
-        id = static_cast<uint32_t>(v >> 32);
-      }
-      key[r + 1] = k;
-      sub[r + 1] = id;
-      live[r + 1] = ballot(k != 0);
+      const int en = base + r * kWave + lane;
+      uint2 v = make_uint2(0u, 0u);
+      if (en < total) v = lds.part[en / K][en % K];
+      key[r + 1] = v.x;
+      sub[r + 1] = v.y;
+      live[r + 1] = ballot(v.x != 0);
     }
     wave_select<RB + 1>(key, sub, live, K, Traits<T>::kKeyBits, sel);
     compact<RB + 1>(s, key, sub, sel, lane, cur_key, cur_id);
@@ -226,166 +531,33 @@ __device__ void merge_row(int64_t row, int P, int K, int lane, WaveLds& s, const
 }
 
 template <typename T, bool kAligned>
-__global__ __launch_bounds__(kWave* kWavesPerBlock) void topk_sweep_kernel(
-    const T* __restrict__ logits, int gamma, int64_t V, int64_t stride_b, int64_t stride_i, int K, int P,
-    int64_t Q, uint32_t* __restrict__ counters, uint64_t* __restrict__ part_ms, uint64_t* __restrict__ part_ent,
-    int32_t* __restrict__ cand_ids, float* __restrict__ cand_logit, float* __restrict__ cand_logprob,
-    float* __restrict__ lse) {
-  constexpr int EPG = Traits<T>::kPer;
-  constexpr int64_t CH = static_cast<int64_t>(kGroups) * kWave * EPG;
-  __shared__ WaveLds lds[kWavesPerBlock];
-
-  const int w = threadIdx.x / kWave;
-  const int lane = threadIdx.x % kWave;
-  const int64_t q = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + w;
-  if (q >= Q) return;
-  WaveLds& s = lds[w];
-  const int64_t row = q / P;
-  const int chunk = static_cast<int>(q - row * P);
-  const int64_t b = row / gamma, i = row - b * gamma;
-  const T* rp = logits + b * stride_b + i * stride_i;
-  const int64_t c0 = chunk * CH;
-  const int64_t c1 = c0 + CH < V ? c0 + CH : V;
-
-  // 1. Stream the chunk into registers: group g of this lane covers elements
-  //    c0 + (g*64 + lane)*EPG .. +EPG, so every load instruction reads 1 KB contiguous.
-  u32x4 data[kGroups];
-  if (kAligned && c0 + CH <= V) {
-#pragma unroll
-    for (int g = 0; g < kGroups; ++g)
-      data[g] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(rp + c0 + (g * kWave + lane) * EPG));
-  } else {
-#pragma unroll
-    for (int g = 0; g < kGroups; ++g)
-      data[g] = load_group_checked<T, kAligned>(rp, c0 + (g * kWave + lane) * EPG, c1);
-  }
-
-  // 2. Per group: maximum and exp-sum relative to it; fold into the lane's (max, sum).
-  float gmax[kGroups];
-  float lm = neg_inf(), ls = 0.f;
-#pragma unroll
-  for (int g = 0; g < kGroups; ++g) {
-    float x[EPG];
-#pragma unroll
-    for (int j = 0; j < EPG; ++j) x[j] = Traits<T>::elem(data[g], j);
-    float gm = x[0];
-#pragma unroll
-    for (int j = 1; j < EPG; ++j) gm = fmaxf(gm, x[j]);
-    gmax[g] = gm;
-    if (gm != neg_inf()) {
-      const float off = gm * kLog2e;
-      float gs = 0.f;
-#pragma unroll
-      for (int j = 0; j < EPG; ++j) gs += fast_exp2(fmaf(x[j], kLog2e, -off));
-      if (gm > lm) {
-        ls = fmaf(ls, fast_exp2((lm - gm) * kLog2e), gs);
-        lm = gm;
-      } else {
-        ls = fmaf(gs, fast_exp2((gm - lm) * kLog2e), ls);
-      }
-    }
-  }
-
-  // 3. The chunk's (max, sum).
-  const float wm = wave_max(lm);
-  const float wsum = wave_sum((lm == neg_inf()) ? 0.f : ls * fast_exp2((lm - wm) * kLog2e));
-
-  // 4. tau = K-th largest lane maximum (key 0 for lanes without elements).
-  const bool lane_valid = c0 + static_cast<int64_t>(lane) * EPG < c1;
-  const uint32_t lkey[1] = {lane_valid ? Traits<T>::key_value(lm) : 0u};
-  const uint64_t all[1] = {~0ull};
-  const uint32_t tau = wave_kth_largest<1>(lkey, all, K, Traits<T>::kKeyBits);
-
-  // 5. Groups whose maximum reaches tau can hold a top-K element.  They go to the LDS
-  //    buffer in rounds of at most kCapGroups groups; each round is merged into the
-  //    running top-K held in lanes 0..K-1.  Typical chunks need one round.
-  uint32_t pending = 0;
-#pragma unroll
-  for (int g = 0; g < kGroups; ++g) {
-    const int64_t rel = static_cast<int64_t>(g * kWave + lane) * EPG;
-    if (c0 + rel < c1 && Traits<T>::key_value(gmax[g]) >= tau) pending |= 1u << g;
-  }
-  uint32_t cur_key = 0, cur_id = 0;
-  while (ballot(pending != 0)) {
-    int nbuf = 0;
-#pragma unroll
-    for (int g = 0; g < kGroups; ++g) {
-      const bool hit = (pending >> g) & 1u;
-      const uint64_t m = ballot(hit);
-      if (m) {
-        const int pos = nbuf + static_cast<int>(lanes_below(m));
-        if (hit && pos < kCapGroups) {
-          s.data[pos] = data[g];
-          s.base[pos] = static_cast<uint32_t>((g * kWave + lane) * EPG);
-          pending &= ~(1u << g);
-        }
-        nbuf = nbuf + popc(m) < kCapGroups ? nbuf + popc(m) : kCapGroups;
-      }
-    }
-    __builtin_amdgcn_wave_barrier();
-    flush<T>(s, nbuf, c0, c1, tau, K, lane, cur_key, cur_id);
-  }
-
-  // 6. Publish the partial result with stores that are coherent at device scope, and
-  //    wait until they have completed before counting this chunk as done.
-  if (lane < K) store_agent(&part_ent[q * K + lane], pack(cur_key, cur_id));
-  if (lane == 0) store_agent(&part_ms[q], pack(__float_as_uint(wm), __float_as_uint(wsum)));
-  __builtin_amdgcn_s_waitcnt(0);
-  __atomic_signal_fence(__ATOMIC_SEQ_CST);
-
-  // 7. The last wave of the row to arrive merges the row; its loads are device-coherent
-  //    too, so no cache-wide writeback or invalidation is needed.
-  uint32_t prev = 0;
-  if (lane == 0) prev = __hip_atomic_fetch_add(&counters[row], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  prev = __builtin_amdgcn_readfirstlane(prev);
-  if (prev != static_cast<uint32_t>(P - 1)) return;
-  __atomic_signal_fence(__ATOMIC_SEQ_CST);
-  merge_row<T>(row, P, K, lane, s, part_ms, part_ent, cand_ids, cand_logit, cand_logprob, lse);
-  if (lane == 0) __hip_atomic_store(&counters[row], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+void launch_typed(const void* logits, int B, int gamma, int64_t V, int64_t stride_b, int64_t stride_i, int K,
+                  int32_t* cand_ids, float* cand_logit, float* cand_logprob, float* lse, hipStream_t stream) {
+  const int64_t rows = static_cast<int64_t>(B) * gamma;
+  hipLaunchKernelGGL((topk_row_kernel<T, kAligned>), dim3(static_cast<unsigned>(rows)), dim3(kWave * kWaves), 0,
+                     stream, static_cast<const T*>(logits), gamma, V, stride_b, stride_i, K, cand_ids, cand_logit,
+                     cand_logprob, lse);
 }
-
-size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
 }  // namespace
 
-TopkPlan topk_plan(int B, int gamma, int64_t V, int K, int dtype) {
-  TopkPlan p{};
-  const int epg = dtype == 1 ? 8 : 4;
-  p.chunk = kGroups * kWave * epg;
-  p.parts = static_cast<int>((V + p.chunk - 1) / p.chunk);
-  const size_t rows = static_cast<size_t>(B) * gamma;
-  p.off_ms = align256(rows * sizeof(uint32_t));
-  p.off_ent = p.off_ms + align256(rows * p.parts * sizeof(uint64_t));
-  p.bytes = p.off_ent + align256(rows * p.parts * static_cast<size_t>(K) * sizeof(uint64_t));
-  return p;
-}
-
 hipError_t launch_topk(const void* logits, int dtype, bool aligned, int B, int gamma, int64_t V, int64_t stride_b,
-                       int64_t stride_i, int K, const TopkPlan& plan, void* workspace, int32_t* cand_ids,
-                       float* cand_logit, float* cand_logprob, float* lse, hipStream_t stream) {
-  const int64_t Q = static_cast<int64_t>(B) * gamma * plan.parts;
-  const dim3 grid(static_cast<unsigned>((Q + kWavesPerBlock - 1) / kWavesPerBlock));
-  const dim3 block(kWave * kWavesPerBlock);
-  char* ws = static_cast<char*>(workspace);
-  uint32_t* counters = reinterpret_cast<uint32_t*>(ws);
-  uint64_t* ms = reinterpret_cast<uint64_t*>(ws + plan.off_ms);
-  uint64_t* ent = reinterpret_cast<uint64_t*>(ws + plan.off_ent);
+                       int64_t stride_i, int K, int32_t* cand_ids, float* cand_logit, float* cand_logprob, float* lse,
+                       hipStream_t stream) {
   if (dtype == 1) {
-    const uint16_t* x = static_cast<const uint16_t*>(logits);
     if (aligned)
-      hipLaunchKernelGGL((topk_sweep_kernel<uint16_t, true>), grid, block, 0, stream, x, gamma, V, stride_b, stride_i,
-                         K, plan.parts, Q, counters, ms, ent, cand_ids, cand_logit, cand_logprob, lse);
+      launch_typed<uint16_t, true>(logits, B, gamma, V, stride_b, stride_i, K, cand_ids, cand_logit, cand_logprob,
+                                   lse, stream);
     else
-      hipLaunchKernelGGL((topk_sweep_kernel<uint16_t, false>), grid, block, 0, stream, x, gamma, V, stride_b,
-                         stride_i, K, plan.parts, Q, counters, ms, ent, cand_ids, cand_logit, cand_logprob, lse);
+      launch_typed<uint16_t, false>(logits, B, gamma, V, stride_b, stride_i, K, cand_ids, cand_logit, cand_logprob,
+                                    lse, stream);
   } else {
-    const float* x = static_cast<const float*>(logits);
     if (aligned)
-      hipLaunchKernelGGL((topk_sweep_kernel<float, true>), grid, block, 0, stream, x, gamma, V, stride_b, stride_i, K,
-                         plan.parts, Q, counters, ms, ent, cand_ids, cand_logit, cand_logprob, lse);
+      launch_typed<float, true>(logits, B, gamma, V, stride_b, stride_i, K, cand_ids, cand_logit, cand_logprob, lse,
+                                stream);
     else
-      hipLaunchKernelGGL((topk_sweep_kernel<float, false>), grid, block, 0, stream, x, gamma, V, stride_b, stride_i,
-                         K, plan.parts, Q, counters, ms, ent, cand_ids, cand_logit, cand_logprob, lse);
+      launch_typed<float, false>(logits, B, gamma, V, stride_b, stride_i, K, cand_ids, cand_logit, cand_logprob, lse,
+                                 stream);
   }
   return hipGetLastError();
 }

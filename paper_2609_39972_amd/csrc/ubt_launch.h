@@ -9,18 +9,9 @@
 namespace ubt {
 
 // ---- top-K sweep --------------------------------------------------------------------
-struct TopkPlan {
-  int chunk;      // elements per wave chunk
-  int parts;      // chunks per row (P)
-  size_t off_ms;  // workspace offsets (bytes)
-  size_t off_ent;
-  size_t bytes;   // total workspace bytes
-};
-TopkPlan topk_plan(int B, int gamma, int64_t V, int K, int dtype);
 hipError_t launch_topk(const void* logits, int dtype, bool aligned, int B, int gamma, int64_t V,
-                       int64_t stride_b, int64_t stride_i, int K, const TopkPlan& plan, void* workspace,
-                       int32_t* cand_ids, float* cand_logit, float* cand_logprob, float* lse,
-                       hipStream_t stream);
+                       int64_t stride_b, int64_t stride_i, int K, int32_t* cand_ids, float* cand_logit,
+                       float* cand_logprob, float* lse, hipStream_t stream);
 
 // ---- selector scores ------------------------------------------------------------------
 struct Scales {

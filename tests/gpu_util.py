@@ -47,7 +47,7 @@ def run_pipeline(w: synth.Workload, d: dict, W: int | None = None, debug: bool =
     logits = dev_values(d["logits"]) if logits_t is None else logits_t
     step = ubt.DraftStep(w.B, w.gamma, w.V, w.K, W, w.budget, dev_values(d["phi"]), dev_values(d["psi"]),
                          dev_values(d["gate"]), dev_i32(d["anchor"]), d["alpha"], d["lam"], w.zeta,
-                         logits_dtype=logits.dtype, with_delta=True, debug=debug)
+                         with_delta=True, debug=debug)
     out = step.run(logits)
     torch.cuda.synchronize()
     return to_np(out)

@@ -1,5 +1,5 @@
-"""The C ABI of libubt.so on the host: exported symbols, status strings, workspace
-sizing, and argument validation, which returns an error before any device work (so
+"""The C ABI of libubt.so on the host: exported symbols, status strings and
+argument validation, which returns an error before any device work (so
 these run without a GPU; the pointers passed are never dereferenced)."""
 from __future__ import annotations
 
@@ -38,23 +38,11 @@ def test_version_and_status_strings():
     assert L.ubt_status_str(99).decode() == "UBT_ERR_UNKNOWN"
 
 
-def test_workspace_bytes():
-    L = ubt.lib()
-    n = L.ubt_topk_workspace_bytes(32, 15, 151936, 8, ubt.UBT_BF16)
-    P = -(-151936 // 8192)
-    assert n >= 32 * 15 * (4 + 8 * P + 8 * P * 8)
-    assert n % 256 == 0
-    for bad in [(0, 15, 100, 8, 1), (1, 65, 100, 8, 1), (1, 1, 7, 8, 1), (1, 1, 100, 65, 1), (1, 1, 100, 0, 1),
-                (1, 1, 100, 8, 2), (1, 1, 2 ** 31, 8, 1)]:
-        assert L.ubt_topk_workspace_bytes(*bad) == 0, bad
-
-
 def _topk(**kw):
-    a = dict(logits=FAKE, dt=1, B=2, gamma=3, V=1000, sb=3000, si=1000, K=8, ids=FAKE, val=FAKE, lp=None, lse=None,
-             ws=FAKE, wsb=1 << 20)
+    a = dict(logits=FAKE, dt=1, B=2, gamma=3, V=1000, sb=3000, si=1000, K=8, ids=FAKE, val=FAKE, lp=None, lse=None)
     a.update(kw)
     return ubt.lib().ubt_topk(a["logits"], a["dt"], a["B"], a["gamma"], a["V"], a["sb"], a["si"], a["K"], a["ids"],
-                              a["val"], a["lp"], a["lse"], a["ws"], a["wsb"], None)
+                              a["val"], a["lp"], a["lse"], None)
 
 
 @pytest.mark.parametrize("kw,code", [
@@ -62,7 +50,6 @@ def _topk(**kw):
     (dict(dt=5), 3),
     (dict(B=0), 2), (dict(gamma=0), 2), (dict(gamma=65), 2), (dict(K=0), 2), (dict(K=65), 2), (dict(V=7), 2),
     (dict(si=999), 2), (dict(sb=2999), 2), (dict(V=2 ** 31, si=2 ** 31, sb=3 * 2 ** 31), 2),
-    (dict(ws=None), 5), (dict(wsb=100), 5), (dict(ws=ctypes.c_void_p(0x10010)), 5),
 ])
 def test_topk_validation(kw, code):
     assert _topk(**kw) == code
