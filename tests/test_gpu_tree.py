@@ -50,6 +50,10 @@ def _compare(B, gamma, K, W, budget, zeta=0.0, seed=0, tie_frac=0.0, levels=64):
     (2, 1, 1, 1, 1), (3, 1, 8, 3, 5), (2, 4, 1, 2, 10), (4, 7, 4, 3, 16), (4, 15, 8, 8, 32), (8, 15, 8, 12, 64),
     (4, 15, 16, 24, 128), (2, 31, 16, 24, 128), (2, 15, 8, 64, 64), (2, 31, 16, 128, 128), (2, 15, 64, 12, 64),
     (2, 5, 64, 64, 255), (2, 64, 4, 64, 255), (1, 16, 16, 255, 255), (2, 3, 5, 7, 100), (2, 9, 3, 2, 200),
+    # register-resident search (K in {4, 8, 16}) at the edges of its range: W*K = 512 and 384, gamma*W = 1024,
+    # 255 nodes, gamma = 64; and the general search just outside it (K = 13, 17, 7; W = 65)
+    (2, 16, 8, 64, 255), (3, 32, 4, 32, 255), (2, 12, 16, 32, 200), (2, 64, 4, 16, 255), (2, 9, 16, 24, 200),
+    (2, 20, 13, 30, 150), (2, 6, 7, 9, 40), (2, 10, 17, 12, 64), (2, 6, 4, 65, 100), (2, 64, 2, 16, 255),
 ])
 def test_dyadic_exact(B, gamma, K, W, budget):
     _compare(B, gamma, K, W, budget, seed=B + gamma + K)
@@ -59,6 +63,8 @@ def test_dyadic_exact(B, gamma, K, W, budget):
 def test_exact_ties(tie_frac, levels):
     _compare(4, 10, 8, 12, 64, seed=3, tie_frac=tie_frac, levels=levels)
     _compare(2, 15, 16, 24, 128, seed=4, tie_frac=tie_frac, levels=levels)
+    _compare(2, 16, 8, 64, 255, seed=5, tie_frac=tie_frac, levels=levels)
+    _compare(2, 8, 20, 12, 64, seed=6, tie_frac=tie_frac, levels=levels)
 
 
 @pytest.mark.parametrize("zeta", [-0.125, -1.0, -1000.0])
