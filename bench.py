@@ -82,7 +82,7 @@ def main() -> int:
     ap.add_argument("--workload", type=int, default=3, help="synthetic workload id (3 = B=32, V=151936 headline)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="minimum oracle time for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--sweep-launches", type=int, default=200, help="individually timed sweep launches")
+    ap.add_argument("--sweep-launches", type=int, default=200, help="launches per kernel in the per-kernel timing")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run a plain device copy of known size (counter calibration) and exit")
     args = ap.parse_args()
@@ -170,18 +170,28 @@ def main() -> int:
     ms_per_step = elapsed_ms / steps
     log(f"{steps} steps in {elapsed_ms:.2f} ms (wall {wall_ms:.2f} ms): {ms_per_step * 1e3:.2f} us/step")
 
-    # Per-kernel durations: each launch bracketed by its own events on the launch stream.
-    def timed(fn, n):
-        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
-        with torch.cuda.stream(stream):
+    # Per-kernel durations: `n` launches of one kernel (rotating over the pool buffers, so
+    # each sweep reads its logits from HBM) captured back to back in a graph, replayed
+    # between two events on the launch stream; duration = elapsed / launches.
+    def timed(fn, n, replays=4):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=stream):
             for j in range(n):
-                evs[j][0].record(stream)
                 fn(j)
-                evs[j][1].record(stream)
         torch.cuda.synchronize()
-        return float(np.mean([a.elapsed_time(b) for a, b in evs])) * 1e3  # us
+        with torch.cuda.stream(stream):
+            g.replay()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        with torch.cuda.stream(stream):
+            a.record(stream)
+            for _ in range(replays):
+                g.replay()
+            b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) * 1e3 / (n * replays)  # us
 
-    n = args.sweep_launches
+    n = max(pool, args.sweep_launches - args.sweep_launches % pool)
     sweep_us = timed(lambda j: ubt.topk(bufs[j % pool][0], w.K, bufs[j % pool][1].cand), n)
     bigram_us = timed(lambda j: ubt.bigram_scores(bufs[j % pool][1].phi, bufs[j % pool][1].psi,
                                                   bufs[j % pool][1].gate, bufs[j % pool][1].anchor,
