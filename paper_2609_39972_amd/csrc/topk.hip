@@ -6,19 +6,21 @@
 //
 // One HBM pass, one workgroup per row.  The row is cut into sub-chunks of 64 lanes x 4
 // groups x 16 B (2048 bf16 or 1024 fp32 elements), dealt round-robin to the waves of
-// the workgroup; each wave streams its sub-chunks with the next one already in flight
-// (two register buffers, nontemporal 16-byte loads).  Per 16-byte group a lane takes the
-// maximum and the exp-sum relative to it and folds both into its running (max, sum).
+// the workgroup; each wave streams its sub-chunks with the next two already in flight
+// (three register buffers, nontemporal 16-byte buffer loads addressed by a fixed lane
+// offset plus a wave-uniform scalar base).  Only the first sub-chunk is requested before
+// it arrives, so first sub-chunks never queue behind other waves' prefetches.  A lane
+// keeps a running (max, sum of exp(x - max)) whose max may trail the true one by a
+// bounded slack, so most sub-chunks need no rescale: one exp per element.
 //
 // Top-K: a group can hold a top-K element only if its maximum reaches a threshold that
 // is known to be at most the row's K-th largest element.  After every wave has
 // streamed its first sub-chunk, the workgroup takes T = the K-th largest of all lane
 // maxima seen so far (at least K elements reach it); from then on only groups whose
-// maximum reaches T are buffered in LDS.  A wave whose buffer fills merges it into its
-// running top-K with a ballot-driven radix selection and from then on needs strictly
-// more than its K-th candidate (its later sub-chunks hold larger token ids).  At the
-// end every wave merges what is left, and the waves' (max, sum) and candidates meet in
-// LDS, where one wave writes the row's LSE and sorted top-K.
+// maximum reaches T are buffered in LDS.  A wave whose buffer overflows re-scans its
+// sub-chunks exactly at the end.  Every wave then selects its top K from its buffer,
+// and the waves' (max, sum) and candidates meet in LDS, where one wave writes the row's
+// LSE and sorted top-K.
 #include "ubt_device.h"
 #include "ubt_launch.h"
 
@@ -97,15 +99,23 @@ constexpr int kNontemporal = 2;  // cache policy of the streaming loads (read on
 // are still issued, at an offset past the buffer range: they read zeros without touching
 // memory, and keep the number of loads in flight the same on every path, so the waits for
 // the current sub-chunk never include the prefetched one.
+//
+// The lane's byte offset goes in the vector offset (the same register for every load of
+// the pass) and the wave-uniform sub-chunk base in the scalar offset, so issuing a load
+// writes no vector register other than its destination.
 template <typename T>
 __device__ __forceinline__ void load_full(u32x4 (&buf)[kSubGroups], __amdgpu_buffer_rsrc_t rsrc, int64_t c0,
-                                          int lane, bool live = true) {
+                                          uint32_t lane_off, bool live = true) {
   constexpr int EPG = Traits<T>::kPer;
-  const uint32_t off = live ? static_cast<uint32_t>((c0 + lane * EPG) * sizeof(T)) : 0xFFFF0000u;
+  const uint32_t base = live ? static_cast<uint32_t>(c0 * sizeof(T)) : 0xFFFF0000u;
+  // Issued in group order on every path (no reordering across the barriers): the waits
+  // for group g then count exactly the loads issued after it.
 #pragma unroll
-  for (int g = 0; g < kSubGroups; ++g)
+  for (int g = 0; g < kSubGroups; ++g) {
     buf[g] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                                           rsrc, off + g * kWave * EPG * sizeof(T), 0, kNontemporal));
+                                           rsrc, lane_off + g * kWave * EPG * sizeof(T), base, kNontemporal));
+    __builtin_amdgcn_sched_barrier(0);
+  }
 }
 
 // Loads sub-chunk elements [c0, c0 + SUB) of a row that may end inside it or be
@@ -218,39 +228,47 @@ struct WaveState {
   bool overflow;  // a group that passed could not be buffered
 };
 
-// Max and exp-sum of one sub-chunk, folded into the lane's running (max, sum); returns
-// the group maxima in gmax and the lane's maximum over the sub-chunk.
+// Max and exp-sum of one sub-chunk, folded into the lane's running (lm, ls): ls is the
+// sum of exp(x - lm) over the lane's elements so far, where lm may trail the lane's true
+// maximum by up to kSlack (terms stay below e^kSlack, far from fp32 overflow).  lm is
+// raised, with one rescale of ls, only when a sub-chunk would break that bound.
+constexpr float kSlack = 32.f;
 template <typename T>
 __device__ __forceinline__ float reduce_sub(const u32x4 (&buf)[kSubGroups], float (&gmax)[kSubGroups], float& lm,
                                             float& ls) {
   constexpr int EPG = Traits<T>::kPer;
-  float sub_max = neg_inf();
+  float x[kSubGroups][EPG];
+#pragma unroll
+  for (int g = 0; g < kSubGroups; ++g)
+#pragma unroll
+    for (int j = 0; j < EPG; ++j) x[g][j] = Traits<T>::elem(buf[g], j);
+  // maximum() needs no NaN canonicalisation of its inputs (maxnum does); logits are
+  // never NaN, so the two agree here.
+  float sub_max;
 #pragma unroll
   for (int g = 0; g < kSubGroups; ++g) {
-    float x[EPG];
+    float gm = x[g][0];
 #pragma unroll
-    for (int j = 0; j < EPG; ++j) x[j] = Traits<T>::elem(buf[g], j);
-    float gm = x[0];
-#pragma unroll
-    for (int j = 1; j + 1 < EPG; j += 2) gm = fmaxf(gm, fmaxf(x[j], x[j + 1]));
-    if (EPG % 2 == 0) gm = fmaxf(gm, x[EPG - 1]);
+    for (int j = 1; j + 1 < EPG; j += 2)
+      gm = __builtin_elementwise_maximum(gm, __builtin_elementwise_maximum(x[g][j], x[g][j + 1]));
+    if (EPG % 2 == 0) gm = __builtin_elementwise_maximum(gm, x[g][EPG - 1]);
     gmax[g] = gm;
-    sub_max = fmaxf(sub_max, gm);
-    // exp-sum relative to the group maximum (0 for a group of -inf values)
-    const bool finite = gm != neg_inf();
-    const float off = finite ? gm * kLog2e : 0.f;
-    float gs = 0.f;
-#pragma unroll
-    for (int j = 0; j < EPG; ++j) gs += fast_exp2(fmaf(x[j], kLog2e, -off));
-    // fold (gm, gs) into (lm, ls) with one exponential: the smaller maximum is rescaled
-    const float hi = fmaxf(lm, gm);
-    const float e = fast_exp2(-fabsf(gm - lm) * kLog2e);
-    const float up = fmaf(ls, e, gs);  // gm is the new maximum
-    const float keep = fmaf(gs, e, ls);
-    const float nls = gm > lm ? up : keep;
-    ls = finite ? nls : ls;
-    lm = finite ? hi : lm;
+    sub_max = g == 0 ? gm : __builtin_elementwise_maximum(sub_max, gm);
   }
+  const float nlm = fmaxf(lm, sub_max - kSlack);
+  const float f = fast_exp2((lm - nlm) * kLog2e);
+  ls = lm == nlm ? ls : ls * f;  // lm == nlm == -inf keeps ls (= 0)
+  lm = nlm;
+  const float off = nlm == neg_inf() ? 0.f : nlm * kLog2e;  // every x is -inf while nlm is
+  float s0 = fast_exp2(fmaf(x[0][0], kLog2e, -off)), s1 = fast_exp2(fmaf(x[0][1], kLog2e, -off));
+#pragma unroll
+  for (int g = 0; g < kSubGroups; ++g)
+#pragma unroll
+    for (int j = (g == 0 ? 2 : 0); j < EPG; j += 2) {
+      s0 += fast_exp2(fmaf(x[g][j], kLog2e, -off));
+      s1 += fast_exp2(fmaf(x[g][j + 1], kLog2e, -off));
+    }
+  ls += s0 + s1;
   return sub_max;
 }
 
@@ -265,6 +283,16 @@ __device__ __forceinline__ void group_max_sub(const u32x4 (&buf)[kSubGroups], fl
     for (int j = 1; j < EPG; ++j) gm = fmaxf(gm, Traits<T>::elem(buf[g], j));
     gmax[g] = gm;
   }
+}
+
+// True if any lane of the wave has a group of a full sub-chunk whose maximum reaches thr.
+template <typename T>
+__device__ __forceinline__ bool any_pass_full(const float (&gmax)[kSubGroups], uint32_t thr) {
+  const float thr_v = thr == 0 ? neg_inf() : Traits<T>::from_key(thr);
+  uint64_t m = 0;
+#pragma unroll
+  for (int g = 0; g < kSubGroups; ++g) m |= ballot(gmax[g] >= thr_v);
+  return m != 0;
 }
 
 // Bit g set if group g of this lane is inside the row and its maximum passes the
@@ -375,11 +403,12 @@ __global__ __launch_bounds__(kWave* kWaves, 4) void topk_row_kernel(const T* __r
   const T* rp = logits + b * stride_b + i * stride_i;
   const __amdgpu_buffer_rsrc_t rsrc = row_resource(rp, static_cast<uint32_t>(V * static_cast<int64_t>(sizeof(T))));
   const int64_t nsub = (V + SUB - 1) / SUB;
+  const uint32_t lane_off = static_cast<uint32_t>(lane * EPG * sizeof(T));
   WaveLds& s = lds.wave[w];
 
   if (threadIdx.x == 0) lds.n_lane_max = 0;
   WaveState st{neg_inf(), 0.f, 0u, 0, false};
-  u32x4 bufA[kSubGroups], bufB[kSubGroups];
+  u32x4 bufA[kSubGroups], bufB[kSubGroups], bufC[kSubGroups];
   float gmax[kSubGroups];
   // Full sub-chunks stream through the fast path (aligned rows only); the ragged last
   // sub-chunk, or every sub-chunk of an unaligned row, goes through checked loads.
@@ -387,8 +416,18 @@ __global__ __launch_bounds__(kWave* kWaves, 4) void topk_row_kernel(const T* __r
   int64_t sc = w;
 
   // First full sub-chunk of every wave, then one workgroup-wide threshold.
-  load_full<T>(bufA, rsrc, sc * SUB, lane, sc < nfull);
-  load_full<T>(bufB, rsrc, (sc + nw) * SUB, lane, sc + nw < nfull);
+  // Only the first sub-chunk is requested up front: every wave of the launch needs its
+  // first sub-chunk before its workgroup can agree on a threshold, so those requests
+  // must not queue behind other waves' prefetches.  The next two follow as soon as it
+  // has arrived.
+  load_full<T>(bufA, rsrc, sc * SUB, lane_off, sc < nfull);
+  {
+    uint32_t x = bufA[kSubGroups - 1][0];
+    asm volatile("" : "+v"(x));  // the first sub-chunk has arrived
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  load_full<T>(bufB, rsrc, (sc + nw) * SUB, lane_off, sc + nw < nfull);
+  load_full<T>(bufC, rsrc, (sc + 2 * nw) * SUB, lane_off, sc + 2 * nw < nfull);
   __syncthreads();  // n_lane_max is cleared
   {
     uint32_t lkey = 0;
@@ -396,7 +435,7 @@ __global__ __launch_bounds__(kWave* kWaves, 4) void topk_row_kernel(const T* __r
     // This wave's K largest lane maxima (more with ties) join the workgroup's union.
     const uint32_t lk[1] = {lkey};
     const uint64_t all[1] = {~0ull};
-    const uint32_t tw = wave_kth_largest<1>(lk, all, K, Traits<T>::kKeyBits);
+    const uint32_t tw = wave_threshold<1>(lk, all, K, K);
     const bool mine = lkey != 0 && lkey >= tw;
     const uint64_t m = ballot(mine);
     uint32_t base = 0;
@@ -409,10 +448,11 @@ __global__ __launch_bounds__(kWave* kWaves, 4) void topk_row_kernel(const T* __r
     // T = the K-th largest lane maximum of the workgroup: a lower bound of the row's
     // K-th largest element, so every top-K element sits in a group reaching it.
     const int n = static_cast<int>(lds.n_lane_max);
-    if (n <= kWave) {
-      const uint32_t k1[1] = {lane < n ? lds.lane_max[lane] : 0u};
-      const uint64_t l1[1] = {~0ull};
-      st.thr = wave_kth_largest<1>(k1, l1, K, Traits<T>::kKeyBits);
+    if (n <= 2 * kWave) {
+      const uint32_t v0 = lds.lane_max[lane], v1 = lds.lane_max[kWave + lane];
+      const uint32_t k2[2] = {lane < n ? v0 : 0u, kWave + lane < n ? v1 : 0u};
+      const uint64_t l2[2] = {ballot(lane < n), ballot(kWave + lane < n)};
+      st.thr = wave_threshold<2>(k2, l2, K, K);
     } else {
       // Many ties among the lane maxima: count straight from LDS.
       uint32_t t = 0;
@@ -431,21 +471,29 @@ __global__ __launch_bounds__(kWave* kWaves, 4) void topk_row_kernel(const T* __r
   }
   sc += nw;
 
-  // Remaining full sub-chunks, the next one always in flight.
+  // Remaining full sub-chunks, the next two always in flight.
   while (sc < nfull) {
-    load_full<T>(bufA, rsrc, (sc + nw) * SUB, lane, sc + nw < nfull);
+    load_full<T>(bufA, rsrc, (sc + 2 * nw) * SUB, lane_off, sc + 2 * nw < nfull);
     reduce_sub<T>(bufB, gmax, st.lm, st.ls);
-    if (!st.overflow) {
+    if (!st.overflow && any_pass_full<T>(gmax, st.thr)) {
       const uint32_t p = passing_groups<T>(gmax, sc * SUB, V, st.thr, false, lane);
-      if (ballot(p != 0) && ballot(buffer_groups<T>(bufB, p, sc * SUB, lane, s, st.nbuf) != 0)) st.overflow = true;
+      if (ballot(buffer_groups<T>(bufB, p, sc * SUB, lane, s, st.nbuf) != 0)) st.overflow = true;
     }
     sc += nw;
     if (sc >= nfull) break;
-    load_full<T>(bufB, rsrc, (sc + nw) * SUB, lane, sc + nw < nfull);
-    reduce_sub<T>(bufA, gmax, st.lm, st.ls);
-    if (!st.overflow) {
+    load_full<T>(bufB, rsrc, (sc + 2 * nw) * SUB, lane_off, sc + 2 * nw < nfull);
+    reduce_sub<T>(bufC, gmax, st.lm, st.ls);
+    if (!st.overflow && any_pass_full<T>(gmax, st.thr)) {
       const uint32_t p = passing_groups<T>(gmax, sc * SUB, V, st.thr, false, lane);
-      if (ballot(p != 0) && ballot(buffer_groups<T>(bufA, p, sc * SUB, lane, s, st.nbuf) != 0)) st.overflow = true;
+      if (ballot(buffer_groups<T>(bufC, p, sc * SUB, lane, s, st.nbuf) != 0)) st.overflow = true;
+    }
+    sc += nw;
+    if (sc >= nfull) break;
+    load_full<T>(bufC, rsrc, (sc + 2 * nw) * SUB, lane_off, sc + 2 * nw < nfull);
+    reduce_sub<T>(bufA, gmax, st.lm, st.ls);
+    if (!st.overflow && any_pass_full<T>(gmax, st.thr)) {
+      const uint32_t p = passing_groups<T>(gmax, sc * SUB, V, st.thr, false, lane);
+      if (ballot(buffer_groups<T>(bufA, p, sc * SUB, lane, s, st.nbuf) != 0)) st.overflow = true;
     }
     sc += nw;
   }
@@ -483,12 +531,18 @@ __global__ __launch_bounds__(kWave* kWaves, 4) void topk_row_kernel(const T* __r
   __syncthreads();
   if (w != 0) return;
 
-  // Wave 0 merges the row.
-  float m = lane < nw ? lds.ms[lane].x : neg_inf();
-  m = wave_max(m);
+  // Wave 0 merges the row.  The waves' (max, sum) pairs are read by every lane (LDS
+  // broadcast) and combined without crossing lanes.
+  float2 ms[kWaves];
+#pragma unroll
+  for (int j = 0; j < kWaves; ++j) ms[j] = lds.ms[j];
+  float m = neg_inf();
+#pragma unroll
+  for (int j = 0; j < kWaves; ++j) m = j < nw ? fmaxf(m, ms[j].x) : m;
   float e = 0.f;
-  if (lane < nw && lds.ms[lane].x != neg_inf()) e = lds.ms[lane].y * fast_exp2((lds.ms[lane].x - m) * kLog2e);
-  e = wave_sum(e);
+#pragma unroll
+  for (int j = 0; j < kWaves; ++j)
+    if (j < nw && ms[j].x != neg_inf()) e += ms[j].y * fast_exp2((ms[j].x - m) * kLog2e);
   const float l = (m == neg_inf()) ? neg_inf() : m + fast_log2(e) * kLn2;
 
   constexpr int RB = 4;

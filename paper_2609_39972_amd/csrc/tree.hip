@@ -379,36 +379,6 @@ __host__ __device__ inline bool fast_tree_fits(int gamma, int K, int W) {
   return (K == 4 || K == 8 || K == 16) && W <= kFastMaxW && W * K <= kFastMaxWK && gamma * W <= kFastMaxGW;
 }
 
-// Lane predicate from a wave mask (the mask is used directly as the lane condition).
-__device__ __forceinline__ bool lane_in(uint64_t mask) { return __builtin_amdgcn_inverse_ballot_w64(mask); }
-
-// Max / min over the wave, returned as wave-uniform values: DPP inside rows of 16 lanes,
-// then the four row results combined on the scalar unit.
-__device__ __forceinline__ uint32_t dpp_row_umax(uint32_t v) {
-  v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0xB1, 0xF, 0xF, false)));
-  v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x4E, 0xF, 0xF, false)));
-  v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x141, 0xF, 0xF, false)));
-  v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x140, 0xF, 0xF, false)));
-  return v;
-}
-__device__ __forceinline__ uint32_t dpp_row_umin(uint32_t v) {
-  v = min(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0xB1, 0xF, 0xF, false)));
-  v = min(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x4E, 0xF, 0xF, false)));
-  v = min(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x141, 0xF, 0xF, false)));
-  v = min(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x140, 0xF, 0xF, false)));
-  return v;
-}
-__device__ __forceinline__ uint32_t rows_umax(uint32_t v) {
-  const uint32_t a = __builtin_amdgcn_readlane(v, 0), b = __builtin_amdgcn_readlane(v, 16);
-  const uint32_t c = __builtin_amdgcn_readlane(v, 32), d = __builtin_amdgcn_readlane(v, 48);
-  return max(max(a, b), max(c, d));
-}
-__device__ __forceinline__ uint32_t rows_umin(uint32_t v) {
-  const uint32_t a = __builtin_amdgcn_readlane(v, 0), b = __builtin_amdgcn_readlane(v, 16);
-  const uint32_t c = __builtin_amdgcn_readlane(v, 32), d = __builtin_amdgcn_readlane(v, 48);
-  return min(min(a, b), min(c, d));
-}
-
 // Selects the `need` best live entries under (key desc, index asc), where entry (r, lane)
 // has index r*64 + lane and key 0 marks a dead entry (rows past the data hold key 0).
 template <int R>
@@ -424,8 +394,8 @@ __device__ __forceinline__ void select_best(const uint32_t (&key)[R], int n_live
     hi = max(hi, key[r]);
     lo = min(lo, key[r] != 0u ? key[r] : ~0u);
   }
-  const uint32_t kmax = rows_umax(dpp_row_umax(hi));
-  const uint32_t kmin = rows_umin(dpp_row_umin(lo));
+  const uint32_t kmax = wave_umax(hi);
+  const uint32_t kmin = wave_umin(lo);
   // Live keys share the bits above the highest bit where kmax and kmin differ.
   uint32_t t = kmax;
   if (kmax != kmin) {

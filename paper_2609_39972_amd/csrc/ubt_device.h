@@ -54,41 +54,171 @@ __device__ __forceinline__ uint32_t lanes_below(uint64_t mask) {
 __device__ __forceinline__ uint64_t ballot(bool p) { return __ballot(p); }
 __device__ __forceinline__ int popc(uint64_t m) { return __popcll(m); }
 
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
+// Float reductions.  DPP patterns inside a row of 16 lanes: xor 1 and xor 2 within a
+// quad, then the mirrors of each half row and of the row; every lane of the row ends
+// with the row's result.
+template <class Op>
+__device__ __forceinline__ float dpp_row_reduce(float v, Op op) {
+  v = op(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false)));
+  v = op(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xF, 0xF, false)));
+  v = op(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x141, 0xF, 0xF, false)));
+  v = op(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x140, 0xF, 0xF, false)));
   return v;
+}
+struct FMax {
+  __device__ float operator()(float a, float b) const { return fmaxf(a, b); }
+};
+struct FAdd {
+  __device__ float operator()(float a, float b) const { return a + b; }
+};
+// Over the wave (every lane active); the result is wave-uniform.
+__device__ __forceinline__ float wave_max(float v) {
+  v = dpp_row_reduce(v, FMax{});
+  const float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
+  const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
+  const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
+  const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
+  return fmaxf(fmaxf(r0, r1), fmaxf(r2, r3));
 }
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, kWave);
-  return v;
+  v = dpp_row_reduce(v, FAdd{});
+  const float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
+  const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
+  const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
+  const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
+  return (r0 + r1) + (r2 + r3);
 }
 // Reductions inside aligned groups of 16 lanes.
-__device__ __forceinline__ float group16_max(float v) {
-#pragma unroll
-  for (int o = 8; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
+__device__ __forceinline__ float group16_max(float v) { return dpp_row_reduce(v, FMax{}); }
+__device__ __forceinline__ float group16_sum(float v) { return dpp_row_reduce(v, FAdd{}); }
+
+// Lane predicate from a wave mask: the mask is used directly as the lane condition.
+__device__ __forceinline__ bool lane_in(uint64_t mask) { return __builtin_amdgcn_inverse_ballot_w64(mask); }
+
+// Max / min of a 32-bit unsigned value over the wave, returned wave-uniform.  Every lane
+// must be active: DPP inside rows of 16 lanes, then the four row results on the scalar
+// unit.
+__device__ __forceinline__ uint32_t dpp_row_umax(uint32_t v) {
+  v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0xB1, 0xF, 0xF, false)));
+  v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x4E, 0xF, 0xF, false)));
+  v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x141, 0xF, 0xF, false)));
+  v = max(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x140, 0xF, 0xF, false)));
   return v;
 }
-__device__ __forceinline__ float group16_sum(float v) {
-#pragma unroll
-  for (int o = 8; o >= 1; o >>= 1) v += __shfl_xor(v, o, kWave);
+__device__ __forceinline__ uint32_t dpp_row_umin(uint32_t v) {
+  v = min(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0xB1, 0xF, 0xF, false)));
+  v = min(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x4E, 0xF, 0xF, false)));
+  v = min(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x141, 0xF, 0xF, false)));
+  v = min(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x140, 0xF, 0xF, false)));
   return v;
+}
+__device__ __forceinline__ uint32_t wave_umax(uint32_t v) {
+  v = dpp_row_umax(v);
+  const uint32_t a = __builtin_amdgcn_readlane(v, 0), b = __builtin_amdgcn_readlane(v, 16);
+  const uint32_t c = __builtin_amdgcn_readlane(v, 32), d = __builtin_amdgcn_readlane(v, 48);
+  return max(max(a, b), max(c, d));
+}
+__device__ __forceinline__ uint32_t wave_umin(uint32_t v) {
+  v = dpp_row_umin(v);
+  const uint32_t a = __builtin_amdgcn_readlane(v, 0), b = __builtin_amdgcn_readlane(v, 16);
+  const uint32_t c = __builtin_amdgcn_readlane(v, 32), d = __builtin_amdgcn_readlane(v, 48);
+  return min(min(a, b), min(c, d));
 }
 
-// Largest t (over the bits below `nbits`) such that at least `need` of the live entries
-// have key >= t, i.e. the need-th largest live key (0 if fewer than `need` are live).
-// Entries are key[r] on every lane, r < R; `live[r]` masks entries in or out.
+// Largest and smallest live key (0 and ~0 when none is live).
+template <int R>
+__device__ __forceinline__ void live_key_range(const uint32_t (&key)[R], const uint64_t (&live)[R], uint32_t& kmax,
+                                               uint32_t& kmin) {
+  uint32_t hi = 0u, lo = ~0u;
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const bool l = lane_in(live[r]);
+    hi = max(hi, l ? key[r] : 0u);
+    lo = min(lo, l ? key[r] : ~0u);
+  }
+  kmax = wave_umax(hi);
+  kmin = wave_umin(lo);
+}
+
+// Radix search for the need-th largest live key, for need < the number of live keys.
+// Live keys share the bits above the highest bit where the largest and the smallest of
+// them differ, so the search starts below that common prefix.  Returns true, with sel =
+// the live entries with key >= s, at the first s that splits off exactly `need` of them;
+// otherwise returns false with t = the need-th largest key (then more than `need` keys
+// are >= t: the boundary is a tie).
+template <int R>
+__device__ __forceinline__ bool radix_split(const uint32_t (&key)[R], const uint64_t (&live)[R], int need,
+                                            uint64_t (&sel)[R], uint32_t& t) {
+  uint32_t kmax, kmin;
+  live_key_range<R>(key, live, kmax, kmin);
+  t = kmax;
+  if (kmax == kmin) return false;
+  uint32_t m = 0x80000000u >> __clz(kmax ^ kmin);
+  t = kmax & ~(m | (m - 1u));
+  for (; m != 0u; m >>= 1) {
+    const uint32_t cand = t | m;
+    int cnt = 0;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      sel[r] = ballot(key[r] >= cand) & live[r];
+      cnt += popc(sel[r]);
+    }
+    if (cnt == need) return true;
+    t = cnt > need ? cand : t;
+  }
+  return false;
+}
+
+// Largest t such that at least `need` of the live entries have key >= t, i.e. the
+// need-th largest live key (0 if fewer than `need` are live).  Entries are key[r] on
+// every lane, r < R; `live[r]` masks entries in or out.  Keys use at most `nbits` bits.
 template <int R>
 __device__ __forceinline__ uint32_t wave_kth_largest(const uint32_t (&key)[R], const uint64_t (&live)[R],
                                                      int need, int nbits) {
-  uint32_t t = 0;
-  for (int bit = nbits - 1; bit >= 0; --bit) {
-    const uint32_t cand = t | (1u << bit);
+  (void)nbits;
+  int n_live = 0;
+#pragma unroll
+  for (int r = 0; r < R; ++r) n_live += popc(live[r]);
+  if (n_live < need) return 0u;
+  uint32_t kmax, kmin;
+  live_key_range<R>(key, live, kmax, kmin);
+  if (kmax == kmin) return kmax;
+  uint32_t m = 0x80000000u >> __clz(kmax ^ kmin);
+  uint32_t t = kmax & ~(m | (m - 1u));
+  for (; m != 0u; m >>= 1) {
+    const uint32_t cand = t | m;
     int cnt = 0;
 #pragma unroll
     for (int r = 0; r < R; ++r) cnt += popc(ballot(key[r] >= cand) & live[r]);
-    if (cnt >= need) t = cand;
+    t = cnt >= need ? cand : t;
+  }
+  return t;
+}
+
+// A threshold t with at least `need` live keys >= t, refined only until at most `cap` of
+// them are (cap >= need); 0 if fewer than `need` are live.  Cheaper than the exact
+// need-th largest key when a slightly lower bound will do.
+template <int R>
+__device__ __forceinline__ uint32_t wave_threshold(const uint32_t (&key)[R], const uint64_t (&live)[R], int need,
+                                                   int cap) {
+  int n_live = 0;
+#pragma unroll
+  for (int r = 0; r < R; ++r) n_live += popc(live[r]);
+  if (n_live < need) return 0u;
+  uint32_t kmax, kmin;
+  live_key_range<R>(key, live, kmax, kmin);
+  if (n_live <= cap || kmax == kmin) return kmin;
+  uint32_t m = 0x80000000u >> __clz(kmax ^ kmin);
+  uint32_t t = kmax & ~(m | (m - 1u));
+  for (; m != 0u; m >>= 1) {
+    const uint32_t cand = t | m;
+    int cnt = 0;
+#pragma unroll
+    for (int r = 0; r < R; ++r) cnt += popc(ballot(key[r] >= cand) & live[r]);
+    if (cnt >= need) {
+      t = cand;
+      if (cnt <= cap) break;
+    }
   }
   return t;
 }
@@ -96,11 +226,12 @@ __device__ __forceinline__ uint32_t wave_kth_largest(const uint32_t (&key)[R], c
 // Selects the `need` largest entries under the order (key desc, sub asc) among the live
 // entries of 64*R (key, sub) pairs.  `sub` values are unique among entries with equal
 // key.  Returns per row the ballot mask of selected entries.  If fewer than `need`
-// entries are live, every live entry is selected.
+// entries are live, every live entry is selected.  Every lane must be active.
 template <int R>
 __device__ __forceinline__ void wave_select(const uint32_t (&key)[R], const uint32_t (&sub)[R],
                                             const uint64_t (&live)[R], int need, int key_bits,
                                             uint64_t (&sel)[R]) {
+  (void)key_bits;
   int n_live = 0;
 #pragma unroll
   for (int r = 0; r < R; ++r) n_live += popc(live[r]);
@@ -109,29 +240,29 @@ __device__ __forceinline__ void wave_select(const uint32_t (&key)[R], const uint
     for (int r = 0; r < R; ++r) sel[r] = live[r];
     return;
   }
-  const uint32_t t = wave_kth_largest<R>(key, live, need, key_bits);
-  int above = 0, equal = 0;
+  uint32_t t;
+  if (radix_split<R>(key, live, need, sel, t)) return;
+  int above = 0;
   uint64_t eq[R];
 #pragma unroll
   for (int r = 0; r < R; ++r) {
     sel[r] = ballot(key[r] > t) & live[r];
     eq[r] = ballot(key[r] == t) & live[r];
     above += popc(sel[r]);
-    equal += popc(eq[r]);
-  }
-  const int rest = need - above;  // 1 <= rest <= equal
-  if (rest == equal) {
-#pragma unroll
-    for (int r = 0; r < R; ++r) sel[r] |= eq[r];
-    return;
   }
   // Ties at the threshold: keep the `rest` smallest `sub` values (largest ~sub).
+  const int rest = need - above;  // 1 <= rest < entries tied at t
   uint32_t inv[R];
 #pragma unroll
   for (int r = 0; r < R; ++r) inv[r] = ~sub[r];
-  const uint32_t t2 = wave_kth_largest<R>(inv, eq, rest, 32);
+  uint64_t tie[R];
+  uint32_t u;
+  if (!radix_split<R>(inv, eq, rest, tie, u)) {
 #pragma unroll
-  for (int r = 0; r < R; ++r) sel[r] |= ballot(inv[r] >= t2) & eq[r];
+    for (int r = 0; r < R; ++r) tie[r] = ballot(inv[r] >= u) & eq[r];
+  }
+#pragma unroll
+  for (int r = 0; r < R; ++r) sel[r] |= tie[r];
 }
 
 }  // namespace ubt
