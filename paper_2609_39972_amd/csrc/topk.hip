@@ -109,11 +109,12 @@ __device__ __forceinline__ void load_full(u32x4 (&buf)[kSubGroups], __amdgpu_buf
   constexpr int EPG = Traits<T>::kPer;
   const uint32_t base = live ? static_cast<uint32_t>(c0 * sizeof(T)) : 0xFFFF0000u;
   // Issued in group order on every path (no reordering across the barriers): the waits
-  // for group g then count exactly the loads issued after it.
+  // for group g then count exactly the loads issued after it.  The group's offset goes
+  // into the scalar operand, so all loads share one vector offset register.
 #pragma unroll
   for (int g = 0; g < kSubGroups; ++g) {
     buf[g] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                                           rsrc, lane_off + g * kWave * EPG * sizeof(T), base, kNontemporal));
+                                           rsrc, lane_off, base + g * kWave * EPG * sizeof(T), kNontemporal));
     __builtin_amdgcn_sched_barrier(0);
   }
 }
