@@ -81,7 +81,7 @@ struct WaveLds {
 
 struct RowLds {
   WaveLds wave[kWaves];
-  uint2 part[kWaves][kWave];      // each wave's candidates (key, id)
+  uint2 part[kWaves * kWave];     // wave w's K candidates (key, id) at [w*K, w*K + K)
   float2 ms[kWaves];              // each wave's (max, sum)
   uint32_t lane_max[kWaves * kWave];  // the largest lane maxima of every wave's first sub-chunk
   uint32_t n_lane_max;
@@ -159,18 +159,22 @@ __device__ __forceinline__ void compact(WaveLds& s, const uint32_t (&key)[R], co
   out_id = v.y;
 }
 
-// Merges the buffered candidate groups into the running top-K (lanes 0..K-1).  Elements
-// whose key does not pass the threshold (key >= thr, or key > thr when strict) are
-// dropped: they cannot be in the top K.
-template <typename T, int RB>
+// Merges the buffered candidate groups into the running top-K (lanes 0..K-1), or, with
+// kCarry false, selects the top K of the groups alone (the running top-K is empty).
+// Elements whose key does not pass the threshold (key >= thr, or key > thr when strict)
+// are dropped: they cannot be in the top K.
+template <typename T, int RB, bool kCarry>
 __device__ __forceinline__ void flush_buffer(WaveLds& s, int g0, int nbuf, int64_t V, uint32_t thr, bool strict, int K,
                                              int lane, uint32_t& cur_key, uint32_t& cur_id) {
   constexpr int EPG = Traits<T>::kPer;
-  uint32_t key[RB + 1], sub[RB + 1];
-  uint64_t live[RB + 1], sel[RB + 1];
-  key[0] = cur_key;
-  sub[0] = cur_id;
-  live[0] = ballot(cur_key != 0);
+  constexpr int C = kCarry ? 1 : 0;
+  uint32_t key[RB + C], sub[RB + C];
+  uint64_t live[RB + C], sel[RB + C];
+  if (kCarry) {
+    key[0] = cur_key;
+    sub[0] = cur_id;
+    live[0] = ballot(cur_key != 0);
+  }
 #pragma unroll
   for (int r = 0; r < RB; ++r) {
     const int e = r * kWave + lane;
@@ -186,31 +190,58 @@ __device__ __forceinline__ void flush_buffer(WaveLds& s, int g0, int nbuf, int64
         if (strict ? k <= thr : k < thr) k = 0;
       }
     }
-    key[r + 1] = k;
-    sub[r + 1] = id;
-    live[r + 1] = ballot(k != 0);
+    key[r + C] = k;
+    sub[r + C] = id;
+    live[r + C] = ballot(k != 0);
   }
-  wave_select<RB + 1>(key, sub, live, K, Traits<T>::kKeyBits, sel);
-  compact<RB + 1>(s, key, sub, sel, lane, cur_key, cur_id);
+  wave_select<RB + C>(key, sub, live, K, Traits<T>::kKeyBits, sel);
+  compact<RB + C>(s, key, sub, sel, lane, cur_key, cur_id);
 }
 
 // Merges nbuf buffered groups into the running top-K; returns the new (key, id) pair of
-// this lane (lanes 0..K-1 hold the top K).
-template <typename T>
+// this lane (lanes 0..K-1 hold the top K).  kFresh: the running top-K is empty.
+template <typename T, bool kFresh>
 __device__ __forceinline__ uint2 flush(WaveLds& s, int nbuf, int64_t V, uint32_t thr, bool strict, int K, int lane,
                                        uint32_t cur_key, uint32_t cur_id) {
   constexpr int EPG = Traits<T>::kPer;
   constexpr int kSlice = 4 * kWave / EPG;  // groups per selection pass (four register rows)
   for (int g0 = 0; g0 < nbuf; g0 += kSlice) {
     const int elems = (nbuf - g0 < kSlice ? nbuf - g0 : kSlice) * EPG;
-    if (elems <= kWave)
-      flush_buffer<T, 1>(s, g0, nbuf, V, thr, strict, K, lane, cur_key, cur_id);
-    else if (elems <= 2 * kWave)
-      flush_buffer<T, 2>(s, g0, nbuf, V, thr, strict, K, lane, cur_key, cur_id);
-    else
-      flush_buffer<T, 4>(s, g0, nbuf, V, thr, strict, K, lane, cur_key, cur_id);
+    if (kFresh && g0 == 0) {
+      if (elems <= kWave)
+        flush_buffer<T, 1, false>(s, g0, nbuf, V, thr, strict, K, lane, cur_key, cur_id);
+      else if (elems <= 2 * kWave)
+        flush_buffer<T, 2, false>(s, g0, nbuf, V, thr, strict, K, lane, cur_key, cur_id);
+      else
+        flush_buffer<T, 4, false>(s, g0, nbuf, V, thr, strict, K, lane, cur_key, cur_id);
+    } else {
+      if (elems <= kWave)
+        flush_buffer<T, 1, true>(s, g0, nbuf, V, thr, strict, K, lane, cur_key, cur_id);
+      else if (elems <= 2 * kWave)
+        flush_buffer<T, 2, true>(s, g0, nbuf, V, thr, strict, K, lane, cur_key, cur_id);
+      else
+        flush_buffer<T, 4, true>(s, g0, nbuf, V, thr, strict, K, lane, cur_key, cur_id);
+    }
   }
   return make_uint2(cur_key, cur_id);
+}
+
+// The top K of the waves' candidates part[0..total), total <= 64 R, into lanes 0..K-1.
+template <typename T, int R>
+__device__ __forceinline__ void merge_parts(const uint2* part, int total, int K, int lane, WaveLds& s,
+                                            uint32_t& cur_key, uint32_t& cur_id) {
+  uint32_t key[R], sub[R];
+  uint64_t live[R], sel[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int e = r * kWave + lane;
+    const uint2 v = e < total ? part[e] : make_uint2(0u, 0u);
+    key[r] = v.x;
+    sub[r] = v.y;
+    live[r] = ballot(v.x != 0);
+  }
+  wave_select<R>(key, sub, live, K, Traits<T>::kKeyBits, sel);
+  compact<R>(s, key, sub, sel, lane, cur_key, cur_id);
 }
 
 // Smallest key among the K candidates held in lanes 0..K-1.
@@ -360,7 +391,7 @@ __device__ uint2 rescan(__amdgpu_buffer_rsrc_t rsrc, const T* rp, int64_t first,
       pending = buffer_groups<T>(buf, pending, sc * SUB, lane, s, nbuf);
       if (ballot(pending != 0)) {
         __builtin_amdgcn_wave_barrier();
-        const uint2 c = flush<T>(s, nbuf, V, thr, strict, K, lane, cur_key, cur_id);
+        const uint2 c = flush<T, false>(s, nbuf, V, thr, strict, K, lane, cur_key, cur_id);
         cur_key = c.x;
         cur_id = c.y;
         nbuf = 0;
@@ -368,7 +399,7 @@ __device__ uint2 rescan(__amdgpu_buffer_rsrc_t rsrc, const T* rp, int64_t first,
     }
     if (nbuf > 0) {
       __builtin_amdgcn_wave_barrier();
-      const uint2 c = flush<T>(s, nbuf, V, thr, strict, K, lane, cur_key, cur_id);
+      const uint2 c = flush<T, false>(s, nbuf, V, thr, strict, K, lane, cur_key, cur_id);
       cur_key = c.x;
       cur_id = c.y;
       nbuf = 0;
@@ -514,7 +545,7 @@ __global__ __launch_bounds__(kWave* kWaves, 4) void topk_row_kernel(const T* __r
   if (!st.overflow) {
     if (st.nbuf > 0) {
       __builtin_amdgcn_wave_barrier();
-      const uint2 c = flush<T>(s, st.nbuf, V, st.thr, false, K, lane, 0u, 0u);
+      const uint2 c = flush<T, true>(s, st.nbuf, V, st.thr, false, K, lane, 0u, 0u);
       cur_key = c.x;
       cur_id = c.y;
     }
@@ -527,7 +558,7 @@ __global__ __launch_bounds__(kWave* kWaves, 4) void topk_row_kernel(const T* __r
   // The wave's (max, sum) and candidates.
   const float wm = wave_max(st.lm);
   const float wsum = wave_sum((st.lm == neg_inf()) ? 0.f : st.ls * fast_exp2((st.lm - wm) * kLog2e));
-  lds.part[w][lane] = make_uint2(lane < K ? cur_key : 0u, cur_id);
+  if (lane < K) lds.part[w * K + lane] = make_uint2(cur_key, cur_id);
   if (lane == 0) lds.ms[w] = make_float2(wm, wsum);
   __syncthreads();
   if (w != 0) return;
@@ -546,28 +577,15 @@ __global__ __launch_bounds__(kWave* kWaves, 4) void topk_row_kernel(const T* __r
     if (j < nw && ms[j].x != neg_inf()) e += ms[j].y * fast_exp2((ms[j].x - m) * kLog2e);
   const float l = (m == neg_inf()) ? neg_inf() : m + fast_log2(e) * kLn2;
 
-  constexpr int RB = 4;
-  const int total = nw * K;
-  cur_key = 0;
-  cur_id = 0;
-  for (int base = 0; base < total; base += RB * kWave) {
-    uint32_t key[RB + 1], sub[RB + 1];
-    uint64_t live[RB + 1], sel[RB + 1];
-    key[0] = cur_key;
-    sub[0] = cur_id;
-    live[0] = ballot(cur_key != 0);
-#pragma unroll
-    for (int r = 0; r < RB; ++r) {
-      const int en = base + r * kWave + lane;
-      uint2 v = make_uint2(0u, 0u);
-      if (en < total) v = lds.part[en / K][en % K];
-      key[r + 1] = v.x;
-      sub[r + 1] = v.y;
-      live[r + 1] = ballot(v.x != 0);
-    }
-    wave_select<RB + 1>(key, sub, live, K, Traits<T>::kKeyBits, sel);
-    compact<RB + 1>(s, key, sub, sel, lane, cur_key, cur_id);
-  }
+  const int total = nw * K;  // <= kWaves * kWave
+  if (total <= kWave)
+    merge_parts<T, 1>(lds.part, total, K, lane, s, cur_key, cur_id);
+  else if (total <= 2 * kWave)
+    merge_parts<T, 2>(lds.part, total, K, lane, s, cur_key, cur_id);
+  else if (total <= 4 * kWave)
+    merge_parts<T, 4>(lds.part, total, K, lane, s, cur_key, cur_id);
+  else
+    merge_parts<T, 8>(lds.part, total, K, lane, s, cur_key, cur_id);
   // Position of each selected entry in the (value desc, id asc) order.
   int rank = 0;
   for (int j = 0; j < K; ++j) {
