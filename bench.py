@@ -1,9 +1,9 @@
 """Benchmark of one UBTree draft step on one MI355X.
 
 A step is the whole hot path on one batch of synthetic proposer outputs:
-ubt_topk (softmax statistics + top-K over the vocabulary), ubt_bigram_scores
-(selector scores + normalisation) and ubt_build_tree (beam search, pruning, tree and
-ancestor mask).  Steps rotate over a pool of distinct logit buffers whose total size
+ubt_topk (softmax statistics + top-K over the vocabulary), then ubt_draft_tree, which
+does ubt_bigram_scores (selector scores + normalisation) and ubt_build_tree (beam
+search, pruning, tree and ancestor mask) in one launch (``--separate``: the two calls).  Steps rotate over a pool of distinct logit buffers whose total size
 exceeds the 256 MB last-level cache, so every step reads its logits from HBM.  Inputs
 are resident in HBM before the timed region; the steps are captured once into a HIP
 graph and replayed.
@@ -82,6 +82,8 @@ def main() -> int:
     ap.add_argument("--workload", type=int, default=3, help="synthetic workload id (3 = B=32, V=151936 headline)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="minimum oracle time for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--separate", action="store_true",
+                    help="run the selector and the search as two calls instead of ubt_draft_tree")
     ap.add_argument("--sweep-launches", type=int, default=200, help="launches per kernel in the per-kernel timing")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run a plain device copy of known size (counter calibration) and exit")
@@ -129,7 +131,8 @@ def main() -> int:
         if p == 0:
             host0 = dict(d, phi=phi_np, psi=psi_np)
         step = ubt.DraftStep(w.B, w.gamma, w.V, w.K, w.W, w.budget, phi, psi, to_dev(d["gate"]),
-                             torch.from_numpy(d["anchor"]).to(dev), d["alpha"], d["lam"], w.zeta)
+                             torch.from_numpy(d["anchor"]).to(dev), d["alpha"], d["lam"], w.zeta,
+                             fused=not args.separate)
         bufs.append((to_dev_logits(d["logits"]), step))
     torch.cuda.synchronize()
     log(f"inputs resident in HBM ({time.perf_counter() - t0:.1f} s)")
@@ -201,9 +204,15 @@ def main() -> int:
     tree_us = timed(lambda j: ubt.build_tree(bufs[j % pool][1].anchor, bufs[j % pool][1].cand["cand_ids"],
                                              bufs[j % pool][1].sel["logq"], w.W, w.budget, w.zeta,
                                              bufs[j % pool][1].tree), n)
+    draft_us = timed(lambda j: ubt.draft_tree(bufs[j % pool][1].phi, bufs[j % pool][1].psi, bufs[j % pool][1].gate,
+                                              bufs[j % pool][1].anchor, bufs[j % pool][1].cand["cand_ids"],
+                                              bufs[j % pool][1].cand["cand_logit"], bufs[j % pool][1].alpha,
+                                              bufs[j % pool][1].lam, w.W, w.budget, w.zeta,
+                                              bufs[j % pool][1].sel["logq"], bufs[j % pool][1].tree), n)
     sweep_bytes = w.logit_bytes
     achieved = sweep_bytes / (sweep_us * 1e-6) / 1e9
-    log(f"sweep {sweep_us:.2f} us ({achieved:.0f} GB/s), selector {bigram_us:.2f} us, tree {tree_us:.2f} us")
+    log(f"sweep {sweep_us:.2f} us ({achieved:.0f} GB/s), selector {bigram_us:.2f} us, tree {tree_us:.2f} us, "
+        f"selector + tree in one launch {draft_us:.2f} us")
 
     traffic = measured_traffic()
     cpu = None
@@ -230,7 +239,9 @@ def main() -> int:
         "config": {"workload": w.name, "B": w.B, "L": w.L, "gamma": w.gamma, "V": w.V, "K": w.K, "r": w.r,
                    "budget": w.budget, "W": w.W, "logits": f"{w.dtype} {w.logits}", "features": w.feat_dtype,
                    "pool_buffers": pool, "graph": f"{pool} steps per HIP graph, replayed {replays} times"},
-        "kernels_us": {"topk_sweep": round(sweep_us, 3), "bigram": round(bigram_us, 3), "build_tree": round(tree_us, 3)},
+        "kernels_us": {"topk_sweep": round(sweep_us, 3), "bigram": round(bigram_us, 3), "build_tree": round(tree_us, 3),
+                       "draft_tree": round(draft_us, 3)},
+        "step_calls": "ubt_bigram_scores + ubt_build_tree" if args.separate else "ubt_draft_tree",
         "roofline": {"bound": "hbm", "kernel": SWEEP_KERNEL, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": None if traffic is None else traffic["bytes"],

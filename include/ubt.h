@@ -11,6 +11,9 @@
  *   ubt_build_tree     per sequence: beam search + global pruning -> tree and mask
  *   ubt_tree_mask      (optional) the ancestor mask of any parent-pointer tree
  *
+ * ubt_draft_tree does ubt_bigram_scores + ubt_build_tree in one call (one launch for
+ * the common shapes).
+ *
  * Conventions shared by every call:
  *   - Every pointer is device memory unless marked [host].  The caller owns every
  *     buffer; the library never allocates or frees device memory.
@@ -161,6 +164,26 @@ ubt_status_t ubt_build_tree(const int32_t* anchor, const int32_t* cand_ids, cons
                             int32_t* n_nodes, int32_t* token, int32_t* parent, int32_t* depth,
                             int32_t* cand_rank, float* score, uint32_t* mask,
                             const ubt_supertree_t* dbg, hipStream_t stream);
+
+/* ------------------------------------------------------------------------------------
+ * ubt_draft_tree -- ubt_bigram_scores (without delta) followed by ubt_build_tree
+ * (without the supertree) in one call: Method / Parallel Computation, then Algorithm 1.
+ * The arguments are those of the two calls, with the same meaning, layout and checks;
+ * logq is required and receives the same values.  Every output is bit-identical to
+ * that of the two calls.
+ *
+ * With bf16 features, K in {4, 8, 16}, W <= 64, W*K <= 512 and gamma*W <= 1024, one
+ * kernel launch computes each sequence's score slabs in on-chip memory and searches
+ * them there (logq is still written out).  Other shapes launch the two calls' kernels
+ * in order on `stream`.
+ * ------------------------------------------------------------------------------------ */
+ubt_status_t ubt_draft_tree(const void* phi_tab, const void* psi_tab, const void* gate,
+                            ubt_dtype_t feat_dt, int64_t V, int r, const int32_t* anchor,
+                            const int32_t* cand_ids, const float* cand_logit, const float* alpha,
+                            const float* lambda, int B, int gamma, int K, int W, int budget,
+                            float zeta, float* logq, int32_t* n_nodes, int32_t* token,
+                            int32_t* parent, int32_t* depth, int32_t* cand_rank, float* score,
+                            uint32_t* mask, hipStream_t stream);
 
 /* ------------------------------------------------------------------------------------
  * ubt_tree_mask -- the ancestor ("tree attention") mask of a tree given by parent

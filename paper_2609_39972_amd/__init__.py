@@ -34,7 +34,7 @@ STATUS = {0: "UBT_OK", 1: "UBT_ERR_NULL", 2: "UBT_ERR_SHAPE", 3: "UBT_ERR_VALUE"
 
 # Every symbol include/ubt.h declares.
 EXPORTS = ("ubt_status_str", "ubt_abi_version", "ubt_last_hip_error", "ubt_topk",
-           "ubt_bigram_scores", "ubt_build_tree", "ubt_tree_mask")
+           "ubt_bigram_scores", "ubt_build_tree", "ubt_draft_tree", "ubt_tree_mask")
 
 _p = ctypes.c_void_p
 _i32 = ctypes.c_int
@@ -69,8 +69,10 @@ def lib() -> ctypes.CDLL:
                                         _p]
         L.ubt_build_tree.argtypes = [_p, _p, _p, _i32, _i32, _i32, _i32, _i32, _f32, _p, _p, _p, _p, _p, _p, _p,
                                      ctypes.POINTER(_Supertree), _p]
+        L.ubt_draft_tree.argtypes = [_p, _p, _p, _i32, _i64, _i32, _p, _p, _p, _p, _p, _i32, _i32, _i32, _i32, _i32,
+                                     _f32, _p, _p, _p, _p, _p, _p, _p, _p, _p]
         L.ubt_tree_mask.argtypes = [_p, _p, _i32, _i32, _p, _p]
-        for f in (L.ubt_topk, L.ubt_bigram_scores, L.ubt_build_tree, L.ubt_tree_mask):
+        for f in (L.ubt_topk, L.ubt_bigram_scores, L.ubt_build_tree, L.ubt_draft_tree, L.ubt_tree_mask):
             f.restype = _i32
         _lib = L
     return _lib
@@ -202,6 +204,34 @@ def build_tree(anchor: torch.Tensor, cand_ids: torch.Tensor, logq: torch.Tensor,
     return out
 
 
+def draft_tree(phi: torch.Tensor, psi: torch.Tensor, gate: torch.Tensor, anchor: torch.Tensor,
+               cand_ids: torch.Tensor, cand_logit: torch.Tensor, alpha, lam, W: int, budget: int,
+               zeta: float = 0.0, logq: torch.Tensor | None = None, out: dict | None = None,
+               with_mask: bool = True, stream=None) -> dict:
+    """``bigram_scores`` (no delta) + ``build_tree`` in one library call; returns the tree
+    outputs and ``logq``."""
+    _need_gpu(phi, psi, gate, anchor, cand_ids, cand_logit)
+    for n, t in (("phi", phi), ("psi", psi), ("gate", gate), ("anchor", anchor), ("cand_ids", cand_ids),
+                 ("cand_logit", cand_logit)):
+        _contig(t, n)
+    if not (phi.dtype == psi.dtype == gate.dtype):
+        raise TypeError("phi, psi and gate must share one dtype")
+    V, r = phi.shape
+    B, gamma, K = cand_ids.shape
+    if logq is None:
+        logq = torch.empty(B, gamma, K, K, dtype=torch.float32, device=cand_ids.device)
+    _contig(logq, "logq")
+    if out is None:
+        out = tree_outputs(B, gamma, W, budget, cand_ids.device, with_mask)
+    a, l = _host_f32(alpha, gamma), _host_f32(lam, gamma)
+    st = lib().ubt_draft_tree(_ptr(phi), _ptr(psi), _ptr(gate), _dtype_code(phi), V, r, _ptr(anchor), _ptr(cand_ids),
+                              _ptr(cand_logit), a, l, B, gamma, K, W, budget, float(zeta), _ptr(logq),
+                              _ptr(out["n_nodes"]), _ptr(out["token"]), _ptr(out["parent"]), _ptr(out["depth"]),
+                              _ptr(out["cand_rank"]), _ptr(out["score"]), _ptr(out.get("mask")), _stream(stream))
+    _check("ubt_draft_tree", st)
+    return {**out, "logq": logq}
+
+
 def tree_mask(parent: torch.Tensor, n_nodes: torch.Tensor, out: torch.Tensor | None = None,
               stream=None) -> torch.Tensor:
     """Packed ancestor mask ``[B, N, ceil(N/32)]`` (int32 view of uint32 words)."""
@@ -217,12 +247,14 @@ def tree_mask(parent: torch.Tensor, n_nodes: torch.Tensor, out: torch.Tensor | N
 class DraftStep:
     """One draft step (top-K -> selector -> tree + mask) with every buffer preallocated.
 
-    ``run(logits)`` issues the three library calls on the current stream and allocates
-    nothing, so it can be captured into a HIP graph."""
+    ``run(logits)`` issues the library calls on the current stream and allocates nothing,
+    so it can be captured into a HIP graph.  By default the selector and the search go
+    through ``ubt_draft_tree`` (one call); ``fused=False``, ``with_delta`` or ``debug``
+    use the separate ``ubt_bigram_scores`` and ``ubt_build_tree`` calls."""
 
     def __init__(self, B: int, gamma: int, V: int, K: int, W: int, budget: int, phi: torch.Tensor,
                  psi: torch.Tensor, gate: torch.Tensor, anchor: torch.Tensor, alpha, lam, zeta: float = 0.0,
-                 with_delta: bool = False, debug: bool = False):
+                 with_delta: bool = False, debug: bool = False, fused: bool = True):
         dev = phi.device
         self.shape = (B, gamma, V, K, W, budget)
         self.phi, self.psi, self.gate, self.anchor = phi, psi, gate, anchor
@@ -235,9 +267,15 @@ class DraftStep:
         self.sel = dict(delta=torch.empty(B, gamma, K, K, **f32) if with_delta else None,
                         logq=torch.empty(B, gamma, K, K, **f32))
         self.tree = tree_outputs(B, gamma, W, budget, dev, True, debug)
+        self.fused = fused and not with_delta and not debug
 
     def run(self, logits: torch.Tensor, stream=None) -> dict:
         topk(logits, self.K, self.cand, stream=stream)
+        if self.fused:
+            draft_tree(self.phi, self.psi, self.gate, self.anchor, self.cand["cand_ids"], self.cand["cand_logit"],
+                       self.alpha, self.lam, self.W, self.budget, self.zeta, self.sel["logq"], self.tree,
+                       stream=stream)
+            return {**self.cand, **self.sel, **self.tree}
         bigram_scores(self.phi, self.psi, self.gate, self.anchor, self.cand["cand_ids"], self.cand["cand_logit"],
                       self.alpha, self.lam, self.sel, stream=stream)
         build_tree(self.anchor, self.cand["cand_ids"], self.sel["logq"], self.W, self.budget, self.zeta, self.tree,

@@ -21,6 +21,56 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 
 bool valid_dtype(ubt_dtype_t dt) { return dt == UBT_F32 || dt == UBT_BF16; }
 
+// Checks of ubt_bigram_scores' arguments (logq and delta aside); fills the scales.
+ubt_status_t check_selector(const void* phi_tab, const void* psi_tab, const void* gate, ubt_dtype_t feat_dt, int64_t V,
+                            int r, const int32_t* anchor, const int32_t* cand_ids, const float* cand_logit,
+                            const float* alpha, const float* lambda, int B, int gamma, int K, ubt::Scales& sc) {
+  if (!phi_tab || !psi_tab || !gate || !anchor || !cand_ids || !cand_logit || !alpha || !lambda) return UBT_ERR_NULL;
+  if (!valid_dtype(feat_dt)) return UBT_ERR_VALUE;
+  if (B < 1 || gamma < 1 || gamma > UBT_MAX_GAMMA || K < 1 || K > UBT_MAX_K || V < K || V >= (int64_t(1) << 31))
+    return UBT_ERR_SHAPE;
+  if (r < 16 || r > UBT_MAX_RANK || r % 16 != 0) return UBT_ERR_SHAPE;
+  for (int i = 0; i < gamma; ++i)
+    if (!(isfinite(alpha[i]) && alpha[i] > 0.f && isfinite(lambda[i]) && lambda[i] > 0.f)) return UBT_ERR_VALUE;
+  if (feat_dt == UBT_BF16 && !(aligned16(phi_tab) && aligned16(psi_tab) && aligned16(gate)))
+    return UBT_ERR_UNSUPPORTED;
+  sc = ubt::Scales{};
+  for (int i = 0; i < gamma; ++i) {
+    sc.alpha[i] = alpha[i];
+    sc.lambda[i] = lambda[i];
+  }
+  return UBT_OK;
+}
+
+// Checks of ubt_build_tree's arguments (logq and dbg aside); fills the launch arguments.
+ubt_status_t check_tree(const int32_t* anchor, const int32_t* cand_ids, int B, int gamma, int K, int W, int budget,
+                        float zeta, int32_t* n_nodes, int32_t* token, int32_t* parent, int32_t* depth,
+                        int32_t* cand_rank, float* score, uint32_t* mask, ubt::TreeArgs& a) {
+  if (!anchor || !cand_ids || !n_nodes || !token || !parent || !depth || !cand_rank || !score) return UBT_ERR_NULL;
+  if (B < 1 || gamma < 1 || gamma > UBT_MAX_GAMMA || K < 1 || K > UBT_MAX_K) return UBT_ERR_SHAPE;
+  if (W < 1 || W > UBT_MAX_WIDTH || budget < 1 || budget > UBT_MAX_BUDGET) return UBT_ERR_SHAPE;
+  if (static_cast<int64_t>(W) * K > UBT_MAX_EXPANSION || static_cast<int64_t>(gamma) * W > UBT_MAX_EXPANSION)
+    return UBT_ERR_UNSUPPORTED;
+  if (!(isfinite(zeta) && zeta <= 0.f)) return UBT_ERR_VALUE;
+  a = ubt::TreeArgs{};
+  a.anchor = anchor;
+  a.cand_ids = cand_ids;
+  a.B = B;
+  a.gamma = gamma;
+  a.K = K;
+  a.W = W;
+  a.budget = budget;
+  a.zeta = zeta;
+  a.n_nodes = n_nodes;
+  a.token = token;
+  a.parent = parent;
+  a.depth = depth;
+  a.cand_rank = cand_rank;
+  a.score = score;
+  a.mask = mask;
+  return UBT_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -62,21 +112,11 @@ ubt_status_t ubt_bigram_scores(const void* phi_tab, const void* psi_tab, const v
                                int64_t V, int r, const int32_t* anchor, const int32_t* cand_ids,
                                const float* cand_logit, const float* alpha, const float* lambda, int B, int gamma,
                                int K, float* delta, float* logq, hipStream_t stream) {
-  if (!phi_tab || !psi_tab || !gate || !anchor || !cand_ids || !cand_logit || !alpha || !lambda || !logq)
-    return UBT_ERR_NULL;
-  if (!valid_dtype(feat_dt)) return UBT_ERR_VALUE;
-  if (B < 1 || gamma < 1 || gamma > UBT_MAX_GAMMA || K < 1 || K > UBT_MAX_K || V < K || V >= (int64_t(1) << 31))
-    return UBT_ERR_SHAPE;
-  if (r < 16 || r > UBT_MAX_RANK || r % 16 != 0) return UBT_ERR_SHAPE;
-  for (int i = 0; i < gamma; ++i)
-    if (!(isfinite(alpha[i]) && alpha[i] > 0.f && isfinite(lambda[i]) && lambda[i] > 0.f)) return UBT_ERR_VALUE;
-  if (feat_dt == UBT_BF16 && !(aligned16(phi_tab) && aligned16(psi_tab) && aligned16(gate)))
-    return UBT_ERR_UNSUPPORTED;
-  ubt::Scales sc{};
-  for (int i = 0; i < gamma; ++i) {
-    sc.alpha[i] = alpha[i];
-    sc.lambda[i] = lambda[i];
-  }
+  if (!logq) return UBT_ERR_NULL;
+  ubt::Scales sc;
+  const ubt_status_t st = check_selector(phi_tab, psi_tab, gate, feat_dt, V, r, anchor, cand_ids, cand_logit, alpha,
+                                         lambda, B, gamma, K, sc);
+  if (st != UBT_OK) return st;
   return hip_status(ubt::launch_bigram(phi_tab, psi_tab, gate, static_cast<int>(feat_dt), V, r, anchor, cand_ids,
                                        cand_logit, sc, B, gamma, K, delta, logq, stream));
 }
@@ -85,37 +125,52 @@ ubt_status_t ubt_build_tree(const int32_t* anchor, const int32_t* cand_ids, cons
                             int W, int budget, float zeta, int32_t* n_nodes, int32_t* token, int32_t* parent,
                             int32_t* depth, int32_t* cand_rank, float* score, uint32_t* mask,
                             const ubt_supertree_t* dbg, hipStream_t stream) {
-  if (!anchor || !cand_ids || !logq || !n_nodes || !token || !parent || !depth || !cand_rank || !score)
-    return UBT_ERR_NULL;
+  if (!logq) return UBT_ERR_NULL;
   if (dbg && !(dbg->f_count && dbg->f_parent_slot && dbg->f_cand && dbg->f_score)) return UBT_ERR_NULL;
-  if (B < 1 || gamma < 1 || gamma > UBT_MAX_GAMMA || K < 1 || K > UBT_MAX_K) return UBT_ERR_SHAPE;
-  if (W < 1 || W > UBT_MAX_WIDTH || budget < 1 || budget > UBT_MAX_BUDGET) return UBT_ERR_SHAPE;
-  if (static_cast<int64_t>(W) * K > UBT_MAX_EXPANSION || static_cast<int64_t>(gamma) * W > UBT_MAX_EXPANSION)
-    return UBT_ERR_UNSUPPORTED;
-  if (!(isfinite(zeta) && zeta <= 0.f)) return UBT_ERR_VALUE;
-  ubt::TreeArgs a{};
-  a.anchor = anchor;
-  a.cand_ids = cand_ids;
+  ubt::TreeArgs a;
+  const ubt_status_t st = check_tree(anchor, cand_ids, B, gamma, K, W, budget, zeta, n_nodes, token, parent, depth,
+                                     cand_rank, score, mask, a);
+  if (st != UBT_OK) return st;
   a.logq = logq;
-  a.B = B;
-  a.gamma = gamma;
-  a.K = K;
-  a.W = W;
-  a.budget = budget;
-  a.zeta = zeta;
-  a.n_nodes = n_nodes;
-  a.token = token;
-  a.parent = parent;
-  a.depth = depth;
-  a.cand_rank = cand_rank;
-  a.score = score;
-  a.mask = mask;
   if (dbg) {
     a.f_count = dbg->f_count;
     a.f_parent = dbg->f_parent_slot;
     a.f_cand = dbg->f_cand;
     a.f_score = dbg->f_score;
   }
+  return hip_status(ubt::launch_build_tree(a, stream));
+}
+
+ubt_status_t ubt_draft_tree(const void* phi_tab, const void* psi_tab, const void* gate, ubt_dtype_t feat_dt,
+                            int64_t V, int r, const int32_t* anchor, const int32_t* cand_ids, const float* cand_logit,
+                            const float* alpha, const float* lambda, int B, int gamma, int K, int W, int budget,
+                            float zeta, float* logq, int32_t* n_nodes, int32_t* token, int32_t* parent,
+                            int32_t* depth, int32_t* cand_rank, float* score, uint32_t* mask, hipStream_t stream) {
+  if (!logq) return UBT_ERR_NULL;
+  ubt::Scales sc;
+  ubt_status_t st = check_selector(phi_tab, psi_tab, gate, feat_dt, V, r, anchor, cand_ids, cand_logit, alpha, lambda,
+                                   B, gamma, K, sc);
+  if (st != UBT_OK) return st;
+  ubt::TreeArgs a;
+  st = check_tree(anchor, cand_ids, B, gamma, K, W, budget, zeta, n_nodes, token, parent, depth, cand_rank, score,
+                  mask, a);
+  if (st != UBT_OK) return st;
+  a.logq = logq;
+  if (ubt::draft_tree_fused(static_cast<int>(feat_dt), gamma, K, W)) {
+    ubt::SelectorArgs s;
+    s.phi = static_cast<const uint16_t*>(phi_tab);
+    s.psi = static_cast<const uint16_t*>(psi_tab);
+    s.gate = static_cast<const uint16_t*>(gate);
+    s.V = V;
+    s.r = r;
+    s.cand_logit = cand_logit;
+    s.logq = logq;
+    s.sc = sc;
+    return hip_status(ubt::launch_draft_tree(s, a, stream));
+  }
+  st = hip_status(ubt::launch_bigram(phi_tab, psi_tab, gate, static_cast<int>(feat_dt), V, r, anchor, cand_ids,
+                                     cand_logit, sc, B, gamma, K, nullptr, logq, stream));
+  if (st != UBT_OK) return st;
   return hip_status(ubt::launch_build_tree(a, stream));
 }
 

@@ -14,42 +14,11 @@
 // form every product g_k phi_k(a) psi_k(b) exactly and only the fp32 accumulation
 // rounds.  The row log-softmax runs on the accumulator tile: a row of the tile lives in
 // one aligned group of 16 lanes.  fp32 features use fp32 FMAs on the vector ALUs.
-#include "ubt_device.h"
+#include "bigram_tile.h"
 #include "ubt_launch.h"
 
 namespace ubt {
 namespace {
-
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-
-__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
-
-// Token ids come from device memory; out-of-range ids are clamped so a gather never
-// leaves the tables (the scores of such a pair are then unspecified).
-__device__ __forceinline__ int64_t clamp_id(int32_t id, int64_t V) { return id < 0 ? 0 : (id >= V ? V - 1 : id); }
-
-// Predecessor operand for one k-slice: hi and lo bf16 parts of g_k * phi_k(a).
-__device__ __forceinline__ void split_gated(u32x4 g, u32x4 p, u32x4& hi, u32x4& lo) {
-#pragma unroll
-  for (int w = 0; w < 4; ++w) {
-    uint32_t h2 = 0, l2 = 0;
-#pragma unroll
-    for (int half = 0; half < 2; ++half) {
-      const int s = 16 * half;
-      const float gv = __uint_as_float(((g[w] >> s) & 0xFFFFu) << 16);
-      const float pv = __uint_as_float(((p[w] >> s) & 0xFFFFu) << 16);
-      const float prod = gv * pv;                              // exact: 8-bit x 8-bit significands
-      const uint32_t hb = __float_as_uint(prod) & 0xFFFF0000u;  // leading 8 significant bits
-      const float rest = prod - __uint_as_float(hb);           // exact; at most 8 significant bits
-      h2 |= (hb >> 16) << s;
-      l2 |= (__float_as_uint(rest) >> 16) << s;
-    }
-    hi[w] = h2;
-    lo[w] = l2;
-  }
-}
 
 template <int KT>  // output tiles per side: K <= 16 * KT
 __global__ __launch_bounds__(kWave) void bigram_bf16_kernel(const uint16_t* __restrict__ phi,
@@ -60,90 +29,12 @@ __global__ __launch_bounds__(kWave) void bigram_bf16_kernel(const uint16_t* __re
                                                             const float* __restrict__ cand_logit, Scales sc,
                                                             int gamma, int K, float* __restrict__ delta,
                                                             float* __restrict__ logq) {
-  const int lane = threadIdx.x;
   const int64_t bi = blockIdx.x;  // b * gamma + i
   const int i = static_cast<int>(bi % gamma);
   const int64_t b = bi / gamma;
-  const int lr = lane & 15;  // operand row (A) / column (B) inside a tile
-  const int kg = lane >> 4;  // k-slice group: slots 8*kg .. 8*kg+7 of each 32-wide step
-
-  int64_t pred[KT], succ[KT];
-#pragma unroll
-  for (int t = 0; t < KT; ++t) {
-    const int a = 16 * t + lr;
-    pred[t] = (i == 0) ? (a == 0 ? clamp_id(anchor[b], V) : -1) : (a < K ? clamp_id(cand_ids[(bi - 1) * K + a], V) : -1);
-    const int c = 16 * t + lr;
-    succ[t] = c < K ? clamp_id(cand_ids[bi * K + c], V) : -1;
-  }
-
-  f32x4 acc[KT][KT];
-#pragma unroll
-  for (int mt = 0; mt < KT; ++mt)
-#pragma unroll
-    for (int nt = 0; nt < KT; ++nt) acc[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  const u32x4 zero = u32x4{0u, 0u, 0u, 0u};
-  const uint16_t* g_row = gate + bi * r;
-  for (int k0 = 8 * kg; k0 - 8 * kg < r; k0 += 32) {
-    const bool in = k0 < r;
-    const u32x4 g = in ? *reinterpret_cast<const u32x4*>(g_row + k0) : zero;
-    u32x4 ahi[KT], alo[KT], bq[KT];
-#pragma unroll
-    for (int t = 0; t < KT; ++t) {
-      const u32x4 p = (in && pred[t] >= 0) ? *reinterpret_cast<const u32x4*>(phi + pred[t] * r + k0) : zero;
-      split_gated(g, p, ahi[t], alo[t]);
-      bq[t] = (in && succ[t] >= 0) ? *reinterpret_cast<const u32x4*>(psi + succ[t] * r + k0) : zero;
-    }
-#pragma unroll
-    for (int mt = 0; mt < KT; ++mt)
-#pragma unroll
-      for (int nt = 0; nt < KT; ++nt) {
-        acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(ahi[mt]), as_bf16x8(bq[nt]), acc[mt][nt], 0, 0, 0);
-        acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(alo[mt]), as_bf16x8(bq[nt]), acc[mt][nt], 0, 0, 0);
-      }
-  }
-
-  // Epilogue.  acc[mt][nt][j] = delta(a, c) with a = 16 mt + 4 kg + j, c = 16 nt + lr.
-  const float al = sc.alpha[i], la = sc.lambda[i];
-  float au[KT];
-#pragma unroll
-  for (int nt = 0; nt < KT; ++nt) {
-    const int c = 16 * nt + lr;
-    au[nt] = c < K ? al * cand_logit[bi * K + c] : 0.f;
-  }
-  float* dslab = delta ? delta + bi * K * K : nullptr;
-  float* qslab = logq + bi * K * K;
-#pragma unroll
-  for (int mt = 0; mt < KT; ++mt)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int a = 16 * mt + 4 * kg + j;
-      float s[KT];
-      float m = neg_inf();
-#pragma unroll
-      for (int nt = 0; nt < KT; ++nt) {
-        const int c = 16 * nt + lr;
-        s[nt] = c < K ? fmaf(la, acc[mt][nt][j], au[nt]) : neg_inf();
-        m = fmaxf(m, s[nt]);
-      }
-      m = group16_max(m);
-      float e = 0.f;
-#pragma unroll
-      for (int nt = 0; nt < KT; ++nt) e += __builtin_amdgcn_exp2f((s[nt] - m) * kLog2e);
-      e = group16_sum(e);
-      const float norm = m + __builtin_amdgcn_logf(e) * kLn2;
-      const bool real = (i == 0) ? a == 0 : a < K;
-      if (a < K) {
-#pragma unroll
-        for (int nt = 0; nt < KT; ++nt) {
-          const int c = 16 * nt + lr;
-          if (c < K) {
-            if (dslab) dslab[a * K + c] = real ? acc[mt][nt][j] : 0.f;
-            qslab[a * K + c] = real ? fminf(s[nt] - norm, 0.f) : 0.f;
-          }
-        }
-      }
-    }
+  bigram_tile_bf16<KT>(phi, psi, gate + bi * r, V, r, i, K, anchor + b, i > 0 ? cand_ids + (bi - 1) * K : cand_ids, cand_ids + bi * K,
+                       cand_logit + bi * K, sc.alpha[i], sc.lambda[i], delta ? delta + bi * K * K : nullptr,
+                       logq + bi * K * K, nullptr, static_cast<int>(threadIdx.x));
 }
 
 __global__ __launch_bounds__(kWave) void bigram_f32_kernel(const float* __restrict__ phi, const float* __restrict__ psi,

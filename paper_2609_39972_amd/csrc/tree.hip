@@ -14,6 +14,7 @@
 // the supertree gives the pruned tree, whose emission order is the ranking itself.
 // Ties: score desc, then the extension index (parent position in F_{d-1}, then the
 // candidate rank); across depths score desc, depth asc, position in F_d asc.
+#include "bigram_tile.h"
 #include "ubt_device.h"
 #include "ubt_launch.h"
 
@@ -22,6 +23,7 @@ namespace {
 
 constexpr int kMaxSlabFloats = 12288;  // 48 KB of staged score slabs
 constexpr int kMaxNodes = 256;
+constexpr int kDraftWaves = 8;  // waves per workgroup of the one-launch selector + search
 
 struct TreeSmem {
   float* slab;        // [gamma][K][K] when staged
@@ -351,7 +353,7 @@ constexpr int kStageCap = kStageLive + kWave;  // + one dummy slot per lane
 constexpr int kMaskWords = 8;                  // ceil(256 / 32)
 
 struct FastLayout {
-  uint32_t slab, cids, xpose, stage, s_key, s_info, f_slot, anc, mk, total;
+  uint32_t slab, cids, xpose, stage, s_key, s_info, f_slot, anc, mk, ready, total;
 };
 
 __host__ __device__ inline FastLayout fast_layout(int gamma, int K, int W) {
@@ -371,6 +373,7 @@ __host__ __device__ inline FastLayout fast_layout(int gamma, int K, int W) {
   L.f_slot = take(static_cast<size_t>(gamma) * W * sizeof(int32_t));
   L.anc = take(kMaxNodes * sizeof(int32_t));
   L.mk = take(kMaxNodes * kMaskWords * sizeof(uint32_t));
+  L.ready = take(static_cast<size_t>(gamma) * sizeof(uint32_t));
   L.total = p;
   return L;
 }
@@ -506,6 +509,7 @@ struct FastSmem {
   int32_t* f_slot;
   int32_t* anc;
   uint32_t* mk;
+  uint32_t* ready;  // per position: its slab is in LDS (one-launch kernel only)
 };
 
 // Top_budget over the supertree: stages the selected entries (as compact_selected does).
@@ -523,43 +527,48 @@ __device__ __forceinline__ void prune_supertree(const FastSmem& sm, int GW, int 
   compact_selected<RS>(sm.stage, skey, ssel, n_sel, lane);
 }
 
-template <int KT, int R>
-__global__ __launch_bounds__(kWave) void build_tree_fast_kernel(TreeArgs a, uint64_t magic_w) {
-  extern __shared__ __align__(16) unsigned char smem_raw[];
+__device__ __forceinline__ FastSmem fast_smem(unsigned char* raw, const FastLayout& L) {
+  FastSmem sm;
+  sm.slab = reinterpret_cast<float*>(raw + L.slab);
+  sm.cids = reinterpret_cast<int32_t*>(raw + L.cids);
+  sm.xpose = reinterpret_cast<float*>(raw + L.xpose);
+  sm.stage = reinterpret_cast<uint2*>(raw + L.stage);
+  sm.s_key = reinterpret_cast<uint32_t*>(raw + L.s_key);
+  sm.s_info = reinterpret_cast<uint32_t*>(raw + L.s_info);
+  sm.f_slot = reinterpret_cast<int32_t*>(raw + L.f_slot);
+  sm.anc = reinterpret_cast<int32_t*>(raw + L.anc);
+  sm.mk = reinterpret_cast<uint32_t*>(raw + L.mk);
+  sm.ready = reinterpret_cast<uint32_t*>(raw + L.ready);
+  return sm;
+}
+
+// Publishes slab i to the workgroup: every lane's earlier LDS writes complete before the
+// flag is set.
+__device__ __forceinline__ void publish_slab(uint32_t* ready, int i) {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __hip_atomic_store(&ready[i], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
+// Waits until slab i has been published.  Its producer is another wave of the same
+// workgroup that runs unconditionally, so the flag is always set; the wait is bounded
+// all the same.
+__device__ __forceinline__ void wait_slab(uint32_t* ready, int i) {
+  for (int spin = 0; spin < (1 << 22); ++spin) {
+    const uint32_t f = __hip_atomic_load(&ready[i], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP);
+    if (__builtin_amdgcn_readfirstlane(f) != 0u) return;
+    __builtin_amdgcn_s_sleep(1);
+  }
+}
+
+// Algorithm 1 for sequence b, run by one wavefront once the sequence's candidate ids are
+// in LDS and, unless kWait, all its score slabs; with kWait the slab of position i is
+// awaited before depth i + 1 first reads it.
+template <int KT, int R, bool kWait>
+__device__ __forceinline__ void fast_search(const TreeArgs& a, const FastSmem& sm, int64_t b, int lane,
+                                            uint64_t magic_w) {
   constexpr int kLogK = KT == 4 ? 2 : (KT == 8 ? 3 : 4);
-  const int lane = threadIdx.x;
-  const int64_t b = blockIdx.x;
   const int gamma = a.gamma, W = a.W;
   const int GW = gamma * W;
-  const FastLayout L = fast_layout(gamma, KT, W);
-  FastSmem sm;
-  sm.slab = reinterpret_cast<float*>(smem_raw + L.slab);
-  sm.cids = reinterpret_cast<int32_t*>(smem_raw + L.cids);
-  sm.xpose = reinterpret_cast<float*>(smem_raw + L.xpose);
-  sm.stage = reinterpret_cast<uint2*>(smem_raw + L.stage);
-  sm.s_key = reinterpret_cast<uint32_t*>(smem_raw + L.s_key);
-  sm.s_info = reinterpret_cast<uint32_t*>(smem_raw + L.s_info);
-  sm.f_slot = reinterpret_cast<int32_t*>(smem_raw + L.f_slot);
-  sm.anc = reinterpret_cast<int32_t*>(smem_raw + L.anc);
-  sm.mk = reinterpret_cast<uint32_t*>(smem_raw + L.mk);
-
-  // ---- stage this sequence's score slabs and candidate ids --------------------------
-  {
-    const int ns = gamma * KT * KT;
-    const float* gslab = a.logq + b * ns;
-    if ((reinterpret_cast<uintptr_t>(gslab) & 15u) == 0) {
-      const float4* src = reinterpret_cast<const float4*>(gslab);
-      float4* dst = reinterpret_cast<float4*>(sm.slab);
-#pragma unroll 4
-      for (int e = lane; e < ns / 4; e += kWave) dst[e] = src[e];
-    } else {
-#pragma unroll 4
-      for (int e = lane; e < ns; e += kWave) sm.slab[e] = gslab[e];
-    }
-    const int32_t* gids = a.cand_ids + b * gamma * KT;
-    for (int e = lane; e < gamma * KT; e += kWave) sm.cids[e] = gids[e];
-  }
-  __syncthreads();
 
   // ---- depth-wise expansion ---------------------------------------------------------
   // Frontier entry on lane j < np: score key, position in F, and its slab row for the
@@ -567,6 +576,7 @@ __global__ __launch_bounds__(kWave) void build_tree_fast_kernel(TreeArgs a, uint
   uint32_t fkey = f32_key(0.f);
   int fpos = 0;
   float nq[KT];
+  if (kWait) wait_slab(sm.ready, 0);
   load_row<KT>(sm.slab, nq);  // depth 1 extends the root through row 0
   int np = 1, total = 0;
   const float zeta = a.zeta;
@@ -604,7 +614,10 @@ __global__ __launch_bounds__(kWave) void build_tree_fast_kernel(TreeArgs a, uint
     const int e = have ? static_cast<int>(~mx) : 0;
     const int p = e >> kLogK;
     const int c = e & (KT - 1);
-    if (d < gamma) load_row<KT>(sm.slab + (d * KT + c) * KT, nq);
+    if (d < gamma) {
+      if (kWait) wait_slab(sm.ready, d);
+      load_row<KT>(sm.slab + (d * KT + c) * KT, nq);
+    }
     const int rank = rank_in_stage(sm.stage, w_d, order_value(mx, my));
     const int fb = (d - 1) * W;
     if (have) {
@@ -763,6 +776,67 @@ __global__ __launch_bounds__(kWave) void build_tree_fast_kernel(TreeArgs a, uint
   }
 }
 
+template <int KT, int R>
+__global__ __launch_bounds__(kWave) void build_tree_fast_kernel(TreeArgs a, uint64_t magic_w) {
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  const int lane = threadIdx.x;
+  const int64_t b = blockIdx.x;
+  const int gamma = a.gamma;
+  const FastSmem sm = fast_smem(smem_raw, fast_layout(gamma, KT, a.W));
+  // Stage this sequence's score slabs and candidate ids.
+  const int ns = gamma * KT * KT;
+  const float* gslab = a.logq + b * ns;
+  if ((reinterpret_cast<uintptr_t>(gslab) & 15u) == 0) {
+    const float4* src = reinterpret_cast<const float4*>(gslab);
+    float4* dst = reinterpret_cast<float4*>(sm.slab);
+#pragma unroll 4
+    for (int e = lane; e < ns / 4; e += kWave) dst[e] = src[e];
+  } else {
+#pragma unroll 4
+    for (int e = lane; e < ns; e += kWave) sm.slab[e] = gslab[e];
+  }
+  const int32_t* gids = a.cand_ids + b * gamma * KT;
+  for (int e = lane; e < gamma * KT; e += kWave) sm.cids[e] = gids[e];
+  __syncthreads();
+  fast_search<KT, R, false>(a, sm, b, lane, magic_w);
+}
+
+// Selector scores and tree search in one launch, one workgroup per sequence.  Wave 0
+// computes the score slab of position 0 and starts searching; the other waves compute
+// positions 1, 2, ... (round-robin) and publish each slab as it lands in LDS, and the
+// search waits for a slab only when it first needs it.  Every slab also goes to global
+// memory (logq).
+template <int KT, int R>
+__global__ __launch_bounds__(kDraftWaves* kWave) void draft_tree_fast_kernel(TreeArgs a, SelectorArgs s,
+                                                                             uint64_t magic_w) {
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  const int w = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) / kWave);
+  const int lane = static_cast<int>(threadIdx.x) % kWave;
+  const int nw = static_cast<int>(blockDim.x) / kWave;  // >= 2 when gamma >= 2
+  const int64_t b = blockIdx.x;
+  const int gamma = a.gamma;
+  const FastSmem sm = fast_smem(smem_raw, fast_layout(gamma, KT, a.W));
+  const int32_t* gids = a.cand_ids + b * gamma * KT;
+  for (int e = static_cast<int>(threadIdx.x); e < gamma * KT; e += static_cast<int>(blockDim.x)) sm.cids[e] = gids[e];
+  for (int e = static_cast<int>(threadIdx.x); e < gamma; e += static_cast<int>(blockDim.x)) sm.ready[e] = 0u;
+  __syncthreads();
+  const int first = w;
+  const int stride = w == 0 ? gamma : nw - 1;
+  for (int i = first; i < gamma; i += stride) {
+    const int64_t bi = b * gamma + i;
+    float* slab = sm.slab + i * KT * KT;
+    bigram_tile_bf16<1>(s.phi, s.psi, s.gate + bi * s.r, s.V, s.r, i, KT, a.anchor + b,
+                        i > 0 ? sm.cids + (i - 1) * KT : sm.cids, sm.cids + i * KT, s.cand_logit + bi * KT,
+                        s.sc.alpha[i], s.sc.lambda[i], nullptr, slab, nullptr, lane);
+    publish_slab(sm.ready, i);
+    float* g = s.logq + bi * KT * KT;
+#pragma unroll
+    for (int e = lane; e < KT * KT; e += kWave) g[e] = slab[e];
+  }
+  if (w != 0) return;
+  fast_search<KT, R, true>(a, sm, b, lane, magic_w);
+}
+
 __global__ __launch_bounds__(256) void tree_mask_kernel(const int32_t* __restrict__ parent,
                                                         const int32_t* __restrict__ n_nodes, int N,
                                                         uint32_t* __restrict__ mask) {
@@ -860,6 +934,46 @@ hipError_t launch_build_tree(const TreeArgs& a, hipStream_t stream) {
   else
     UBT_TREE_LAUNCH(64);
 #undef UBT_TREE_LAUNCH
+  return hipGetLastError();
+}
+
+bool draft_tree_fused(int feat_dtype, int gamma, int K, int W) {
+  return feat_dtype == 1 && fast_tree_fits(gamma, K, W);
+}
+
+hipError_t launch_draft_tree(const SelectorArgs& s, const TreeArgs& a, hipStream_t stream) {
+  const uint64_t magic_w = (0x100000000ull + a.W - 1) / a.W;
+  const size_t smem = fast_layout(a.gamma, a.K, a.W).total;
+  const int wk = a.W * a.K;
+  const int nw = a.gamma < kDraftWaves ? a.gamma : kDraftWaves;
+  const dim3 grid(static_cast<unsigned>(a.B)), block(static_cast<unsigned>(nw * kWave));
+#define UBT_DRAFT_LAUNCH(KK, RR)                                                                             \
+  do {                                                                                                       \
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&draft_tree_fast_kernel<KK, RR>),                \
+                              hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(smem));           \
+    hipLaunchKernelGGL((draft_tree_fast_kernel<KK, RR>), grid, block, smem, stream, a, s, magic_w);           \
+  } while (0)
+#define UBT_DRAFT_ROWS(KK)      \
+  do {                          \
+    if (wk <= 64)               \
+      UBT_DRAFT_LAUNCH(KK, 1);  \
+    else if (wk <= 128)         \
+      UBT_DRAFT_LAUNCH(KK, 2);  \
+    else if (wk <= 256)         \
+      UBT_DRAFT_LAUNCH(KK, 4);  \
+    else if (wk <= 384)         \
+      UBT_DRAFT_LAUNCH(KK, 6);  \
+    else                        \
+      UBT_DRAFT_LAUNCH(KK, 8);  \
+  } while (0)
+  if (a.K == 4)
+    UBT_DRAFT_ROWS(4);
+  else if (a.K == 8)
+    UBT_DRAFT_ROWS(8);
+  else
+    UBT_DRAFT_ROWS(16);
+#undef UBT_DRAFT_ROWS
+#undef UBT_DRAFT_LAUNCH
   return hipGetLastError();
 }
 

@@ -47,4 +47,20 @@ hipError_t launch_build_tree(const TreeArgs& a, hipStream_t stream);
 hipError_t launch_tree_mask(const int32_t* parent, const int32_t* n_nodes, int B, int N, uint32_t* mask,
                             hipStream_t stream);
 
+// ---- selector scores + tree search in one launch --------------------------------------
+struct SelectorArgs {
+  const uint16_t* phi;  // bf16 tables and gate
+  const uint16_t* psi;
+  const uint16_t* gate;
+  int64_t V;
+  int r;
+  const float* cand_logit;
+  float* logq;  // also written, [B, gamma, K, K]
+  Scales sc;
+};
+// True if the one-launch kernel handles the shape (bf16 features and the register-
+// resident search: K in {4, 8, 16}, W <= 64, W*K <= 512, gamma*W <= 1024).
+bool draft_tree_fused(int feat_dtype, int gamma, int K, int W);
+hipError_t launch_draft_tree(const SelectorArgs& s, const TreeArgs& a, hipStream_t stream);
+
 }  // namespace ubt
