@@ -108,6 +108,31 @@ def test_build_tree_incomplete_debug_struct():
     assert _tree(dbg=ctypes.byref(s)) == 1
 
 
+def _draft(alpha=None, lam=None, **kw):
+    a_ = (ctypes.c_float * 64)(*([1.0] * 64)) if alpha is None else alpha
+    l_ = (ctypes.c_float * 64)(*([1.0] * 64)) if lam is None else lam
+    a = dict(phi=FAKE, psi=FAKE, gate=FAKE, dt=1, V=1000, r=64, anchor=FAKE, ids=FAKE, logit=FAKE, B=2, gamma=3,
+             K=8, W=4, budget=10, zeta=0.0, logq=FAKE, nn=FAKE, tok=FAKE, par=FAKE, dep=FAKE, cr=FAKE, sc=FAKE,
+             mask=None)
+    a.update(kw)
+    return ubt.lib().ubt_draft_tree(a["phi"], a["psi"], a["gate"], a["dt"], a["V"], a["r"], a["anchor"], a["ids"],
+                                    a["logit"], a_, l_, a["B"], a["gamma"], a["K"], a["W"], a["budget"], a["zeta"],
+                                    a["logq"], a["nn"], a["tok"], a["par"], a["dep"], a["cr"], a["sc"], a["mask"],
+                                    None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(phi=None), 1), (dict(logit=None), 1), (dict(logq=None), 1), (dict(nn=None), 1), (dict(sc=None), 1),
+    (dict(dt=9), 3), (dict(r=8), 2), (dict(K=65), 2), (dict(gamma=65), 2), (dict(V=5), 2), (dict(B=0), 2),
+    (dict(W=0), 2), (dict(budget=256), 2), (dict(W=65, K=64), 4), (dict(gamma=64, W=65, K=4), 4),
+    (dict(alpha=_arr([1.0, 0.0, 1.0])), 3), (dict(lam=_arr([1.0, 1.0, float("nan")])), 3),
+    (dict(zeta=0.5), 3), (dict(zeta=float("nan")), 3), (dict(gate=ctypes.c_void_p(0x10008)), 4),
+])
+def test_draft_tree_validation(kw, code):
+    """The one-call selector + search checks the union of the two calls' arguments."""
+    assert _draft(**kw) == code
+
+
 @pytest.mark.parametrize("args,code", [
     ((None, FAKE, 2, 65, FAKE), 1), ((FAKE, None, 2, 65, FAKE), 1), ((FAKE, FAKE, 2, 65, None), 1),
     ((FAKE, FAKE, 0, 65, FAKE), 2), ((FAKE, FAKE, 2, 0, FAKE), 2), ((FAKE, FAKE, 2, 257, FAKE), 2),
