@@ -353,7 +353,7 @@ constexpr int kStageCap = kStageLive + kWave;  // + one dummy slot per lane
 constexpr int kMaskWords = 8;                  // ceil(256 / 32)
 
 struct FastLayout {
-  uint32_t slab, cids, xpose, stage, s_key, s_info, f_slot, anc, mk, ready, total;
+  uint32_t slab, rmax, cids, xpose, stage, s_key, s_info, f_slot, anc, mk, ready, total;
 };
 
 __host__ __device__ inline FastLayout fast_layout(int gamma, int K, int W) {
@@ -365,6 +365,7 @@ __host__ __device__ inline FastLayout fast_layout(int gamma, int K, int W) {
     return at;
   };
   L.slab = take(static_cast<size_t>(gamma) * K * K * sizeof(float));
+  L.rmax = take(static_cast<size_t>(gamma) * K * sizeof(float));
   L.cids = take(static_cast<size_t>(gamma) * K * sizeof(int32_t));
   L.xpose = take(kFastMaxWK * sizeof(float));
   L.stage = take(kStageCap * sizeof(uint2));
@@ -384,40 +385,54 @@ __host__ __device__ inline bool fast_tree_fits(int gamma, int K, int W) {
 
 // Selects the `need` best live entries under (key desc, index asc), where entry (r, lane)
 // has index r*64 + lane and key 0 marks a dead entry (rows past the data hold key 0).
+// kmax and kmin, if given (kmin != 0), are the largest live key and a lower bound of the
+// need-th largest one; otherwise they are taken from the keys.
 template <int R>
-__device__ __forceinline__ void select_best(const uint32_t (&key)[R], int n_live, int need, uint64_t (&sel)[R]) {
+__device__ __forceinline__ void select_best(const uint32_t (&key)[R], int n_live, int need, uint64_t (&sel)[R],
+                                            uint32_t kmax = 0u, uint32_t kmin = 0u) {
   if (n_live <= need) {
 #pragma unroll
     for (int r = 0; r < R; ++r) sel[r] = ballot(key[r] != 0u);
     return;
   }
-  uint32_t hi = 0, lo = ~0u;
+  if (kmin == 0u) {
+    uint32_t hi = 0, lo = ~0u;
 #pragma unroll
-  for (int r = 0; r < R; ++r) {
-    hi = max(hi, key[r]);
-    lo = min(lo, key[r] != 0u ? key[r] : ~0u);
+    for (int r = 0; r < R; ++r) {
+      hi = max(hi, key[r]);
+      lo = min(lo, key[r] != 0u ? key[r] : ~0u);
+    }
+    kmax = wave_umax(hi);
+    kmin = wave_umin(lo);
   }
-  const uint32_t kmax = wave_umax(hi);
-  const uint32_t kmin = wave_umin(lo);
-  // Live keys share the bits above the highest bit where kmax and kmin differ.
+  // The need-th largest key lies in [kmin, kmax], so it shares the bits above the
+  // highest bit where the two differ.
   uint32_t t = kmax;
   if (kmax != kmin) {
     uint32_t m = 0x80000000u >> __clz(kmax ^ kmin);
     t = kmax & ~(m | (m - 1u));
-    for (; m != 0u; m >>= 1) {
+    // One exit: the loop ends at an exact split (the entries at or above cand) or after
+    // the last bit, with t the need-th largest key.
+    int cnt;
+    do {
       const uint32_t cand = t | m;
-      int cnt = 0;
+      cnt = 0;
 #pragma unroll
       for (int r = 0; r < R; ++r) {
         sel[r] = ballot(key[r] >= cand);
         cnt += popc(sel[r]);
       }
-      if (cnt == need) return;  // an exact split: the entries at or above cand
       t = cnt > need ? cand : t;
-    }
+      // m = cnt == need ? 0 : m >> 1, as one scalar compare and select, so that the loop
+      // test is a single compare of m.
+      uint32_t next = m >> 1;
+      asm volatile("s_cmp_lg_u32 %1, %2\n\ts_cselect_b32 %0, %0, 0" : "+s"(next) : "s"(cnt), "s"(need) : "scc");
+      m = next;
+    } while (m != 0u);
+    if (cnt == need) return;
   }
-  // t is the need-th largest key and more than `need` keys are >= t: the boundary is a
-  // tie.  Take every key above t and the tied entries of smallest index.
+  // t is the need-th largest key: take every key above t and the entries equal to t of
+  // smallest index.
   int left = need;
 #pragma unroll
   for (int r = 0; r < R; ++r) {
@@ -501,6 +516,7 @@ __device__ __forceinline__ void load_row(const float* row, float (&v)[KT]) {
 
 struct FastSmem {
   float* slab;
+  float* rmax;  // per slab row: its largest entry
   int32_t* cids;
   float* xpose;
   uint2* stage;
@@ -530,6 +546,7 @@ __device__ __forceinline__ void prune_supertree(const FastSmem& sm, int GW, int 
 __device__ __forceinline__ FastSmem fast_smem(unsigned char* raw, const FastLayout& L) {
   FastSmem sm;
   sm.slab = reinterpret_cast<float*>(raw + L.slab);
+  sm.rmax = reinterpret_cast<float*>(raw + L.rmax);
   sm.cids = reinterpret_cast<int32_t*>(raw + L.cids);
   sm.xpose = reinterpret_cast<float*>(raw + L.xpose);
   sm.stage = reinterpret_cast<uint2*>(raw + L.stage);
@@ -540,6 +557,19 @@ __device__ __forceinline__ FastSmem fast_smem(unsigned char* raw, const FastLayo
   sm.mk = reinterpret_cast<uint32_t*>(raw + L.mk);
   sm.ready = reinterpret_cast<uint32_t*>(raw + L.ready);
   return sm;
+}
+
+// rmax[e] = the largest entry of slab row e, for rows e0, e0 + stride, ... < e1.
+template <int KT>
+__device__ __forceinline__ void slab_row_max(const float* slab, float* rmax, int e0, int e1, int stride) {
+  for (int e = e0; e < e1; e += stride) {
+    float v[KT];
+    load_row<KT>(slab + e * KT, v);
+    float m = v[0];
+#pragma unroll
+    for (int c = 1; c < KT; ++c) m = fmaxf(m, v[c]);
+    rmax[e] = m;
+  }
 }
 
 // Publishes slab i to the workgroup: every lane's earlier LDS writes complete before the
@@ -560,17 +590,15 @@ __device__ __forceinline__ void wait_slab(uint32_t* ready, int i) {
   }
 }
 
-// Algorithm 1 for sequence b, run by one wavefront once the sequence's candidate ids are
-// in LDS and, unless kWait, all its score slabs; with kWait the slab of position i is
-// awaited before depth i + 1 first reads it.
+// Depth-wise expansion (Eq. ubtree-frontier): F_d = Top_W(E_d) for d = 1..gamma.  F_d is
+// ranked (score desc, parent position, candidate rank) as it is formed and stored in that
+// order to s_key / s_info (parent = its position in F_{d-1}), with the supertree outputs
+// if asked.  total = the number of supertree nodes.
 template <int KT, int R, bool kWait>
-__device__ __forceinline__ void fast_search(const TreeArgs& a, const FastSmem& sm, int64_t b, int lane,
-                                            uint64_t magic_w) {
+__device__ __forceinline__ void expand_depths(const TreeArgs& a, const FastSmem& sm, int64_t b, int lane,
+                                              int& total) {
   constexpr int kLogK = KT == 4 ? 2 : (KT == 8 ? 3 : 4);
   const int gamma = a.gamma, W = a.W;
-  const int GW = gamma * W;
-
-  // ---- depth-wise expansion ---------------------------------------------------------
   // Frontier entry on lane j < np: score key, position in F, and its slab row for the
   // next depth (prefetched as soon as the entry's candidate rank is known).
   uint32_t fkey = f32_key(0.f);
@@ -578,19 +606,28 @@ __device__ __forceinline__ void fast_search(const TreeArgs& a, const FastSmem& s
   float nq[KT];
   if (kWait) wait_slab(sm.ready, 0);
   load_row<KT>(sm.slab, nq);  // depth 1 extends the root through row 0
-  int np = 1, total = 0;
+  float rm = sm.rmax[0];
+  int np = 1;
+  total = 0;
   const float zeta = a.zeta;
   const bool with_zeta = zeta != 0.f;
   for (int d = 1; d <= gamma; ++d) {
+    // Each parent's best child comes from its row maximum (rounding is monotone, so it
+    // is exactly the largest of the children computed below).  With at least W parents,
+    // W extensions reach the smallest of these, a lower bound of the W-th best one.
+    uint32_t best_key = 0u;
     if (lane < np) {
       const float base = f32_key_value(fkey);
       float v[KT];
 #pragma unroll
       for (int c = 0; c < KT; ++c) v[c] = base + nq[c];
+      float best = base + rm;
       if (with_zeta) {
 #pragma unroll
         for (int c = 0; c < KT; ++c) v[c] += zeta;
+        best += zeta;
       }
+      best_key = f32_key(best);
       float4* dst = reinterpret_cast<float4*>(sm.xpose + fpos * KT);
 #pragma unroll
       for (int i = 0; i < KT / 4; ++i) dst[i] = make_float4(v[4 * i], v[4 * i + 1], v[4 * i + 2], v[4 * i + 3]);
@@ -606,7 +643,13 @@ __device__ __forceinline__ void fast_search(const TreeArgs& a, const FastSmem& s
     }
     const int w_d = n < W ? n : W;
     uint64_t sel[R];
-    select_best<R>(key, n, w_d, sel);
+    if (np >= W) {
+      const uint32_t kmax = wave_umax(best_key);
+      const uint32_t kbound = wave_umin(lane < np ? best_key : ~0u);
+      select_best<R>(key, n, w_d, sel, kmax, kbound);
+    } else {
+      select_best<R>(key, n, w_d, sel);
+    }
     compact_selected<R>(sm.stage, key, sel, w_d, lane);
     const uint2 st = sm.stage[lane];
     const bool have = lane < w_d;
@@ -617,6 +660,7 @@ __device__ __forceinline__ void fast_search(const TreeArgs& a, const FastSmem& s
     if (d < gamma) {
       if (kWait) wait_slab(sm.ready, d);
       load_row<KT>(sm.slab + (d * KT + c) * KT, nq);
+      rm = sm.rmax[d * KT + c];
     }
     const int rank = rank_in_stage(sm.stage, w_d, order_value(mx, my));
     const int fb = (d - 1) * W;
@@ -645,6 +689,19 @@ __device__ __forceinline__ void fast_search(const TreeArgs& a, const FastSmem& s
     total += w_d;
     __builtin_amdgcn_wave_barrier();
   }
+}
+
+// Algorithm 1 for sequence b, run by one wavefront once the sequence's candidate ids are
+// in LDS and, unless kWait, all its score slabs; with kWait the slab of position i is
+// awaited before depth i + 1 first reads it.
+template <int KT, int R, bool kWait>
+__device__ __forceinline__ void fast_search(const TreeArgs& a, const FastSmem& sm, int64_t b, int lane,
+                                            uint64_t magic_w) {
+  const int gamma = a.gamma, W = a.W;
+  const int GW = gamma * W;
+
+  int total = 0;
+  expand_depths<KT, R, kWait>(a, sm, b, lane, total);
 
   // ---- global pruning: Top_budget over the supertree --------------------------------
   const int n_sel = total < a.budget ? total : a.budget;
@@ -798,6 +855,8 @@ __global__ __launch_bounds__(kWave) void build_tree_fast_kernel(TreeArgs a, uint
   const int32_t* gids = a.cand_ids + b * gamma * KT;
   for (int e = lane; e < gamma * KT; e += kWave) sm.cids[e] = gids[e];
   __syncthreads();
+  slab_row_max<KT>(sm.slab, sm.rmax, lane, gamma * KT, kWave);
+  __syncthreads();
   fast_search<KT, R, false>(a, sm, b, lane, magic_w);
 }
 
@@ -828,6 +887,7 @@ __global__ __launch_bounds__(kDraftWaves* kWave) void draft_tree_fast_kernel(Tre
     bigram_tile_bf16<1>(s.phi, s.psi, s.gate + bi * s.r, s.V, s.r, i, KT, a.anchor + b,
                         i > 0 ? sm.cids + (i - 1) * KT : sm.cids, sm.cids + i * KT, s.cand_logit + bi * KT,
                         s.sc.alpha[i], s.sc.lambda[i], nullptr, slab, nullptr, lane);
+    slab_row_max<KT>(sm.slab, sm.rmax, i * KT + lane, lane < KT ? i * KT + KT : 0, kWave);
     publish_slab(sm.ready, i);
     float* g = s.logq + bi * KT * KT;
 #pragma unroll

@@ -65,6 +65,11 @@ def test_exact_ties(tie_frac, levels):
     _compare(2, 15, 16, 24, 128, seed=4, tie_frac=tie_frac, levels=levels)
     _compare(2, 16, 8, 64, 255, seed=5, tie_frac=tie_frac, levels=levels)
     _compare(2, 8, 20, 12, 64, seed=6, tie_frac=tie_frac, levels=levels)
+    # Supertrees of at most 256 entries, ranked after the expansion.
+    _compare(3, 12, 4, 16, 60, seed=7, tie_frac=tie_frac, levels=levels)
+    _compare(2, 6, 16, 20, 100, seed=8, tie_frac=tie_frac, levels=levels)
+    _compare(2, 20, 8, 12, 200, seed=9, tie_frac=tie_frac, levels=levels)
+    _compare(4, 15, 8, 12, 64, seed=10, tie_frac=tie_frac, levels=levels)
 
 
 @pytest.mark.parametrize("zeta", [-0.125, -1.0, -1000.0])
