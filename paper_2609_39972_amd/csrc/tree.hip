@@ -423,11 +423,7 @@ __device__ __forceinline__ void select_best(const uint32_t (&key)[R], int n_live
         cnt += popc(sel[r]);
       }
       t = cnt > need ? cand : t;
-      // m = cnt == need ? 0 : m >> 1, as one scalar compare and select, so that the loop
-      // test is a single compare of m.
-      uint32_t next = m >> 1;
-      asm volatile("s_cmp_lg_u32 %1, %2\n\ts_cselect_b32 %0, %0, 0" : "+s"(next) : "s"(cnt), "s"(need) : "scc");
-      m = next;
+      m = radix_next(m, cnt, need, 0u);
     } while (m != 0u);
     if (cnt == need) return;
   }

@@ -140,6 +140,20 @@ __device__ __forceinline__ void live_key_range(const uint32_t (&key)[R], const u
   kmin = wave_umin(lo);
 }
 
+// The next bit of a radix search over keys: m >> 1, or 0 (the search is over) when
+// need <= cnt <= need + span.  One scalar compare and select, so that the loop that
+// calls it ends on a single test of the returned value; cnt, need and span must be
+// wave-uniform.
+__device__ __forceinline__ uint32_t radix_next(uint32_t m, int cnt, int need, uint32_t span) {
+  uint32_t next = __builtin_amdgcn_readfirstlane(m >> 1), d;
+  asm volatile("s_sub_u32 %1, %2, %3\n\ts_cmp_gt_u32 %1, %4\n\ts_cselect_b32 %0, %0, 0"
+               : "+s"(next), "=&s"(d)
+               : "s"(__builtin_amdgcn_readfirstlane(cnt)), "s"(__builtin_amdgcn_readfirstlane(need)),
+                 "s"(__builtin_amdgcn_readfirstlane(span))
+               : "scc");
+  return next;
+}
+
 // Radix search for the need-th largest live key, for need < the number of live keys.
 // Live keys share the bits above the highest bit where the largest and the smallest of
 // them differ, so the search starts below that common prefix.  Returns true, with sel =
@@ -155,44 +169,19 @@ __device__ __forceinline__ bool radix_split(const uint32_t (&key)[R], const uint
   if (kmax == kmin) return false;
   uint32_t m = 0x80000000u >> __clz(kmax ^ kmin);
   t = kmax & ~(m | (m - 1u));
-  for (; m != 0u; m >>= 1) {
+  int cnt;
+  do {
     const uint32_t cand = t | m;
-    int cnt = 0;
+    cnt = 0;
 #pragma unroll
     for (int r = 0; r < R; ++r) {
       sel[r] = ballot(key[r] >= cand) & live[r];
       cnt += popc(sel[r]);
     }
-    if (cnt == need) return true;
     t = cnt > need ? cand : t;
-  }
-  return false;
-}
-
-// Largest t such that at least `need` of the live entries have key >= t, i.e. the
-// need-th largest live key (0 if fewer than `need` are live).  Entries are key[r] on
-// every lane, r < R; `live[r]` masks entries in or out.  Keys use at most `nbits` bits.
-template <int R>
-__device__ __forceinline__ uint32_t wave_kth_largest(const uint32_t (&key)[R], const uint64_t (&live)[R],
-                                                     int need, int nbits) {
-  (void)nbits;
-  int n_live = 0;
-#pragma unroll
-  for (int r = 0; r < R; ++r) n_live += popc(live[r]);
-  if (n_live < need) return 0u;
-  uint32_t kmax, kmin;
-  live_key_range<R>(key, live, kmax, kmin);
-  if (kmax == kmin) return kmax;
-  uint32_t m = 0x80000000u >> __clz(kmax ^ kmin);
-  uint32_t t = kmax & ~(m | (m - 1u));
-  for (; m != 0u; m >>= 1) {
-    const uint32_t cand = t | m;
-    int cnt = 0;
-#pragma unroll
-    for (int r = 0; r < R; ++r) cnt += popc(ballot(key[r] >= cand) & live[r]);
-    t = cnt >= need ? cand : t;
-  }
-  return t;
+    m = radix_next(m, cnt, need, 0u);
+  } while (m != 0u);
+  return cnt == need;
 }
 
 // A threshold t with at least `need` live keys >= t, refined only until at most `cap` of
@@ -210,16 +199,14 @@ __device__ __forceinline__ uint32_t wave_threshold(const uint32_t (&key)[R], con
   if (n_live <= cap || kmax == kmin) return kmin;
   uint32_t m = 0x80000000u >> __clz(kmax ^ kmin);
   uint32_t t = kmax & ~(m | (m - 1u));
-  for (; m != 0u; m >>= 1) {
+  do {
     const uint32_t cand = t | m;
     int cnt = 0;
 #pragma unroll
     for (int r = 0; r < R; ++r) cnt += popc(ballot(key[r] >= cand) & live[r]);
-    if (cnt >= need) {
-      t = cand;
-      if (cnt <= cap) break;
-    }
-  }
+    t = cnt >= need ? cand : t;
+    m = radix_next(m, cnt, need, static_cast<uint32_t>(cap - need));
+  } while (m != 0u);
   return t;
 }
 
