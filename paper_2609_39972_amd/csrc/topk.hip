@@ -4,30 +4,33 @@
 // Sets": C_i = the K tokens of largest q_i, ranked here on the logits (softmax is
 // increasing) with ties to the lower token id.
 //
-// One HBM pass, one workgroup per row.  The row is cut into sub-chunks of 64 lanes x 4
-// groups x 16 B (2048 bf16 or 1024 fp32 elements), dealt round-robin to the waves of
-// the workgroup; each wave streams its sub-chunks with the next two already in flight
-// (three register buffers, nontemporal 16-byte buffer loads addressed by a fixed lane
-// offset plus a wave-uniform scalar base).  Only the first sub-chunk is requested before
-// it arrives, so first sub-chunks never queue behind other waves' prefetches.  A lane
-// keeps a running (max, sum of exp(x - max)) whose max may trail the true one by a
-// bounded slack, so most sub-chunks need no rescale: one exp per element.
+// One HBM pass, one workgroup of 8 waves per row.  The row is cut into tiles of 64 lanes
+// x 4 groups x 16 B (2048 bf16 or 1024 fp32 elements), dealt round-robin to the waves;
+// each wave streams its tiles with the next one in flight (nontemporal 16-byte buffer
+// loads addressed by a fixed lane offset plus a wave-uniform scalar base).  A ragged last
+// tile rides in the same pipeline: loads past the row read zeros, which are masked to
+// -inf.  A lane keeps a running (max, sum of exp(x - max)) whose max may trail the true
+// one by a bounded slack, so most tiles need no rescale: one exp per element.  Waves
+// with more tiles left get a higher issue priority, so the two workgroups that share a
+// CU finish together instead of one starving the other.
 //
 // Top-K: a group can hold a top-K element only if its maximum reaches a threshold that
-// is known to be at most the row's K-th largest element.  After every wave has
-// streamed its first sub-chunk, the workgroup takes T = the K-th largest of all lane
-// maxima seen so far (at least K elements reach it); from then on only groups whose
-// maximum reaches T are buffered in LDS.  A wave whose buffer overflows re-scans its
-// sub-chunks exactly at the end.  Every wave then selects its top K from its buffer,
-// and the waves' (max, sum) and candidates meet in LDS, where one wave writes the row's
-// LSE and sorted top-K.
+// is known to be at most the row's K-th largest element.  After every wave has reduced
+// its first tile, the workgroup takes T = the K-th largest of the 64 column maxima of
+// the lane maxima (K distinct groups reach it), found by counting; from then on only
+// groups whose maximum reaches T are buffered in LDS.  At the end each wave stages its
+// live elements (key >= T), ranks them by counting and publishes its top K, sorted, with
+// its K-th key; wave 0 keeps the published candidates at or above the best K-th key
+// (a lower bound of the row's K-th), ranks them by counting and writes the row's LSE and
+// sorted top-K.  Radix selection is the fallback for more than 64 candidates, and a wave
+// whose buffer overflows re-scans its tiles exactly.
 #include "ubt_device.h"
 #include "ubt_launch.h"
 
 namespace ubt {
 namespace {
 
-constexpr int kSubGroups = 4;     // 16-byte groups per lane per sub-chunk
+constexpr int kSubGroups = 4;     // 16-byte groups per lane per tile
 constexpr int kWaves = 8;         // waves per workgroup
 constexpr int kCapGroups = 64;    // LDS candidate-group buffer per wave
 
@@ -40,7 +43,6 @@ template <>
 struct Traits<uint16_t> {  // bf16 bit patterns
   static constexpr int kPer = 8;
   static constexpr int kKeyBits = 16;
-  static constexpr uint32_t kNegInfBits = 0xFF80u;
   __device__ static float elem(const u32x4& v, int j) {
     const uint32_t w = v[j >> 1];
     return __uint_as_float((j & 1) ? (w & 0xFFFF0000u) : (w << 16));
@@ -60,7 +62,6 @@ template <>
 struct Traits<float> {
   static constexpr int kPer = 4;
   static constexpr int kKeyBits = 32;
-  static constexpr uint32_t kNegInfBits = 0xFF800000u;
   __device__ static float elem(const u32x4& v, int j) { return __uint_as_float(v[j]); }
   __device__ static uint32_t key_bits(uint32_t bits) { return f32_key(__uint_as_float(bits)); }
   __device__ static uint32_t key_value(float f) { return f32_key(f); }
@@ -77,14 +78,17 @@ struct WaveLds {
   u32x4 data[kCapGroups];     // buffered candidate groups
   uint32_t base[kCapGroups];  // row index of each group's first element
   uint2 stage[kWave];         // compaction staging (key, id)
+  uint64_t cand[kWave];       // live candidates as 64-bit order values
 };
 
 struct RowLds {
   WaveLds wave[kWaves];
-  uint2 part[kWaves * kWave];     // wave w's K candidates (key, id) at [w*K, w*K + K)
-  float2 ms[kWaves];              // each wave's (max, sum)
-  uint32_t lane_max[kWaves * kWave];  // the largest lane maxima of every wave's first sub-chunk
-  uint32_t n_lane_max;
+  uint64_t part64[kWaves * kWave];  // wave w's top candidates, sorted, at [w*K, w*K + npart[w])
+  int npart[kWaves];
+  uint32_t thr2;                     // max over the waves of their K-th candidate key
+  uint2 part[kWaves * kWave];        // (key, id) copy of part64 for the radix fallback
+  float2 ms[kWaves];                 // each wave's (max, sum)
+  uint32_t lane_max[kWaves * kWave]; // lane maxima (keys) of every wave's first tile
 };
 
 // A buffer resource covering one row: loads address it with a 32-bit offset in a scalar
@@ -95,22 +99,17 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t row_resource(const void* row, 
 
 constexpr int kNontemporal = 2;  // cache policy of the streaming loads (read once)
 
-// Loads a full sub-chunk [c0, c0 + SUB) of an aligned row.  With `live` false the loads
-// are still issued, at an offset past the buffer range: they read zeros without touching
-// memory, and keep the number of loads in flight the same on every path, so the waits for
-// the current sub-chunk never include the prefetched one.
-//
+// Loads the tile [c0, c0 + SUB) of an aligned row; bytes past the row read as zero.
 // The lane's byte offset goes in the vector offset (the same register for every load of
-// the pass) and the wave-uniform sub-chunk base in the scalar offset, so issuing a load
-// writes no vector register other than its destination.
+// the pass) and the wave-uniform tile base in the scalar offset, so issuing a load writes
+// no vector register other than its destination.
 template <typename T>
 __device__ __forceinline__ void load_full(u32x4 (&buf)[kSubGroups], __amdgpu_buffer_rsrc_t rsrc, int64_t c0,
-                                          uint32_t lane_off, bool live = true) {
+                                          uint32_t lane_off) {
   constexpr int EPG = Traits<T>::kPer;
-  const uint32_t base = live ? static_cast<uint32_t>(c0 * sizeof(T)) : 0xFFFF0000u;
-  // Issued in group order on every path (no reordering across the barriers): the waits
-  // for group g then count exactly the loads issued after it.  The group's offset goes
-  // into the scalar operand, so all loads share one vector offset register.
+  const uint32_t base = static_cast<uint32_t>(c0 * sizeof(T));
+  // Issued in group order (no reordering across the barriers): the wait for group g then
+  // counts exactly the loads issued after it.
 #pragma unroll
   for (int g = 0; g < kSubGroups; ++g) {
     buf[g] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
@@ -119,7 +118,7 @@ __device__ __forceinline__ void load_full(u32x4 (&buf)[kSubGroups], __amdgpu_buf
   }
 }
 
-// Loads sub-chunk elements [c0, c0 + SUB) of a row that may end inside it or be
+// Loads tile elements [c0, c0 + SUB) of a row that may end inside it or be
 // unaligned; elements >= V read as -inf.  A 16-byte load that would cross the end of the
 // row is replaced by element loads.
 template <typename T, bool kAligned>
@@ -140,6 +139,25 @@ __device__ __forceinline__ void load_checked(u32x4 (&buf)[kSubGroups], __amdgpu_
         if (r0 + j < lim) Traits<T>::set_elem(buf[g], j, Traits<T>::load_elem(rp + c0 + r0 + j));
     }
   }
+}
+
+// Sets the groups of a tile that lie at or past V to -inf (groups never straddle V when
+// V * sizeof(T) is a multiple of 16, the only case that loads a ragged tile whole).
+template <typename T>
+__device__ __forceinline__ void mask_tail(u32x4 (&buf)[kSubGroups], int64_t c0, int64_t V, int lane) {
+  constexpr int EPG = Traits<T>::kPer;
+#pragma unroll
+  for (int g = 0; g < kSubGroups; ++g)
+    if (c0 + (g * kWave + lane) * EPG >= V) Traits<T>::set_neg_inf(buf[g]);
+}
+
+// Wave priority from the number of tiles this wave still has to stream: waves that are
+// behind win the issue arbitration, so the waves sharing a CU finish together.
+__device__ __forceinline__ void set_prio(int rem) {
+  if (rem >= 6) __builtin_amdgcn_s_setprio(3);
+  else if (rem >= 4) __builtin_amdgcn_s_setprio(2);
+  else if (rem >= 2) __builtin_amdgcn_s_setprio(1);
+  else __builtin_amdgcn_s_setprio(0);
 }
 
 // Compacts the selected entries (at most 64) into lanes 0.. of (out_key, out_id).
@@ -244,6 +262,53 @@ __device__ __forceinline__ void merge_parts(const uint2* part, int total, int K,
   compact<R>(s, key, sub, sel, lane, cur_key, cur_id);
 }
 
+
+// 64-bit order value of a candidate: larger is better (key desc, then id asc).
+__device__ __forceinline__ uint64_t cand_order(uint32_t key, uint32_t id) {
+  return (static_cast<uint64_t>(key) << 32) | static_cast<uint32_t>(~id);
+}
+// Number of the n order values at v[0..n) (LDS, 16-byte aligned, 64 entries readable)
+// greater than `mine`.  Eight entries per round trip.
+__device__ __forceinline__ int count_above(const uint64_t* v, int n, uint64_t mine) {
+  int c = 0;
+  for (int j0 = 0; j0 < n; j0 += 8) {
+    ulonglong2 p[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) p[q] = *reinterpret_cast<const ulonglong2*>(v + j0 + 2 * q);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) c += (j0 + 2 * q < n && p[q].x > mine) + (j0 + 2 * q + 1 < n && p[q].y > mine);
+  }
+  return c;
+}
+// Stages the buffered elements with key >= thr to s.cand (in buffer order); returns how
+// many there are (only the first 64 are staged).
+template <typename T>
+__device__ __forceinline__ int stage_live(WaveLds& s, int nbuf, int64_t V, uint32_t thr, int lane) {
+  constexpr int EPG = Traits<T>::kPer;
+  const int total = nbuf * EPG;
+  int n = 0;
+  for (int e0 = 0; e0 < total; e0 += kWave) {
+    const int e = e0 + lane;
+    uint32_t k = 0, id = 0;
+    if (e < total) {
+      const int g = e / EPG, j = e % EPG;
+      const uint32_t word = reinterpret_cast<const uint32_t*>(&s.data[g])[j * 4 / EPG];
+      const uint32_t bits = EPG == 8 ? (word >> (16 * (j & 1))) & 0xFFFFu : word;
+      const int64_t gid = static_cast<int64_t>(s.base[g]) + j;
+      if (gid < V) {
+        k = Traits<T>::key_bits(bits);
+        id = static_cast<uint32_t>(gid);
+        if (k < thr) k = 0;
+      }
+    }
+    const uint64_t m = ballot(k != 0);
+    const int pos = n + static_cast<int>(lanes_below(m));
+    if (k != 0 && pos < kWave) s.cand[pos] = cand_order(k, id);
+    n += popc(m);
+  }
+  return n;
+}
+
 // Smallest key among the K candidates held in lanes 0..K-1.
 __device__ __forceinline__ uint32_t kth_key(uint32_t cur_key, int K, int lane) {
   uint32_t mn = lane < K ? cur_key : 0xFFFFFFFFu;
@@ -260,10 +325,10 @@ struct WaveState {
   bool overflow;  // a group that passed could not be buffered
 };
 
-// Max and exp-sum of one sub-chunk, folded into the lane's running (lm, ls): ls is the
+// Max and exp-sum of one tile, folded into the lane's running (lm, ls): ls is the
 // sum of exp(x - lm) over the lane's elements so far, where lm may trail the lane's true
 // maximum by up to kSlack (terms stay below e^kSlack, far from fp32 overflow).  lm is
-// raised, with one rescale of ls, only when a sub-chunk would break that bound.
+// raised, with one rescale of ls, only when a tile would break that bound.
 constexpr float kSlack = 32.f;
 template <typename T>
 __device__ __forceinline__ float reduce_sub(const u32x4 (&buf)[kSubGroups], float (&gmax)[kSubGroups], float& lm,
@@ -304,7 +369,7 @@ __device__ __forceinline__ float reduce_sub(const u32x4 (&buf)[kSubGroups], floa
   return sub_max;
 }
 
-// Group maxima of one sub-chunk (re-scan path).
+// Group maxima of one tile (re-scan path).
 template <typename T>
 __device__ __forceinline__ void group_max_sub(const u32x4 (&buf)[kSubGroups], float (&gmax)[kSubGroups]) {
   constexpr int EPG = Traits<T>::kPer;
@@ -317,7 +382,7 @@ __device__ __forceinline__ void group_max_sub(const u32x4 (&buf)[kSubGroups], fl
   }
 }
 
-// True if any lane of the wave has a group of a full sub-chunk whose maximum reaches thr.
+// True if any lane of the wave has a group of a full tile whose maximum reaches thr.
 template <typename T>
 __device__ __forceinline__ bool any_pass_full(const float (&gmax)[kSubGroups], uint32_t thr) {
   const float thr_v = thr == 0 ? neg_inf() : Traits<T>::from_key(thr);
@@ -371,7 +436,7 @@ __device__ __forceinline__ uint32_t buffer_groups(const u32x4 (&buf)[kSubGroups]
 }
 
 // Exact fallback for a wave whose buffer overflowed (e.g. rows with long runs of equal
-// values): re-reads its sub-chunks and keeps a running top-K, merging the buffer each
+// values): re-reads its tiles and keeps a running top-K, merging the buffer each
 // time it fills and tightening the threshold once K candidates are held (later groups
 // carry larger ids, so they must beat the K-th candidate strictly).
 template <typename T, bool kAligned>
@@ -426,7 +491,7 @@ __global__ __launch_bounds__(kWave* kWaves, 4) void topk_row_kernel(const T* __r
   constexpr int64_t SUB = static_cast<int64_t>(kSubGroups) * kWave * EPG;
   __shared__ RowLds lds;
   const int nw = blockDim.x / kWave;
-  // Wave-uniform, and known to be: the sub-chunk indices and offsets derived from it
+  // Wave-uniform, and known to be: the tile indices and offsets derived from it
   // then live in scalar registers.
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const int lane = threadIdx.x % kWave;
@@ -438,64 +503,53 @@ __global__ __launch_bounds__(kWave* kWaves, 4) void topk_row_kernel(const T* __r
   const uint32_t lane_off = static_cast<uint32_t>(lane * EPG * sizeof(T));
   WaveLds& s = lds.wave[w];
 
-  if (threadIdx.x == 0) lds.n_lane_max = 0;
   WaveState st{neg_inf(), 0.f, 0u, 0, false};
-  u32x4 bufA[kSubGroups], bufB[kSubGroups], bufC[kSubGroups];
+  u32x4 bufA[kSubGroups], bufB[kSubGroups];
   float gmax[kSubGroups];
-  // Full sub-chunks stream through the fast path (aligned rows only); the ragged last
-  // sub-chunk, or every sub-chunk of an unaligned row, goes through checked loads.
-  const int64_t nfull = kAligned ? V / SUB : 0;
+  // Tiles [0, nfull) stream through the pipeline (aligned rows only, with the ragged last
+  // tile when V * sizeof(T) is a multiple of 16); the others go through checked loads.
+  const int64_t nfull0 = kAligned ? V / SUB : 0;
+  const int64_t nfull = kAligned && (V * static_cast<int64_t>(sizeof(T))) % 16 == 0 ? nsub : nfull0;
+  const int64_t last_c0 = (nfull > nfull0) ? (nsub - 1) * SUB : -1;
   int64_t sc = w;
 
-  // First full sub-chunk of every wave, then one workgroup-wide threshold.
-  // Only the first sub-chunk is requested up front: every wave of the launch needs its
-  // first sub-chunk before its workgroup can agree on a threshold, so those requests
-  // must not queue behind other waves' prefetches.  The next two follow as soon as it
-  // has arrived.
-  load_full<T>(bufA, rsrc, sc * SUB, lane_off, sc < nfull);
-  {
+  // First tile of every wave, then one workgroup-wide threshold.  Only the first tile is
+  // requested up front: every wave of the launch needs it before its workgroup can agree
+  // on a threshold, so those requests must not queue behind other waves' prefetches.
+  // The second follows as soon as it has arrived.
+  if (sc < nfull) {
+    load_full<T>(bufA, rsrc, sc * SUB, lane_off);
     uint32_t x = bufA[kSubGroups - 1][0];
-    asm volatile("" : "+v"(x));  // the first sub-chunk has arrived
+    asm volatile("" : "+v"(x));  // the first tile has arrived
     __builtin_amdgcn_sched_barrier(0);
   }
-  load_full<T>(bufB, rsrc, (sc + nw) * SUB, lane_off, sc + nw < nfull);
-  load_full<T>(bufC, rsrc, (sc + 2 * nw) * SUB, lane_off, sc + 2 * nw < nfull);
-  __syncthreads();  // n_lane_max is cleared
+  if (sc + nw < nfull) load_full<T>(bufB, rsrc, (sc + nw) * SUB, lane_off);
   {
     uint32_t lkey = 0;
+    if (sc * SUB == last_c0) mask_tail<T>(bufA, sc * SUB, V, lane);
     if (sc < nfull) lkey = Traits<T>::key_value(reduce_sub<T>(bufA, gmax, st.lm, st.ls));
-    // This wave's K largest lane maxima (more with ties) join the workgroup's union.
-    const uint32_t lk[1] = {lkey};
-    const uint64_t all[1] = {~0ull};
-    const uint32_t tw = wave_threshold<1>(lk, all, K, K);
-    const bool mine = lkey != 0 && lkey >= tw;
-    const uint64_t m = ballot(mine);
-    uint32_t base = 0;
-    if (lane == 0 && m) base = atomicAdd(&lds.n_lane_max, static_cast<uint32_t>(popc(m)));
-    base = __builtin_amdgcn_readfirstlane(base);
-    if (mine) lds.lane_max[base + lanes_below(m)] = lkey;
+    lds.lane_max[w * kWave + lane] = lkey;
+    if (threadIdx.x == 0) lds.thr2 = 0;
   }
   __syncthreads();
   {
-    // T = the K-th largest lane maximum of the workgroup: a lower bound of the row's
-    // K-th largest element, so every top-K element sits in a group reaching it.
-    const int n = static_cast<int>(lds.n_lane_max);
-    if (n <= 2 * kWave) {
-      const uint32_t v0 = lds.lane_max[lane], v1 = lds.lane_max[kWave + lane];
-      const uint32_t k2[2] = {lane < n ? v0 : 0u, kWave + lane < n ? v1 : 0u};
-      const uint64_t l2[2] = {ballot(lane < n), ballot(kWave + lane < n)};
-      st.thr = wave_threshold<2>(k2, l2, K, K);
-    } else {
-      // Many ties among the lane maxima: count straight from LDS.
-      uint32_t t = 0;
-      for (int bit = Traits<T>::kKeyBits - 1; bit >= 0; --bit) {
-        const uint32_t cand = t | (1u << bit);
-        int cnt = 0;
-        for (int e0 = 0; e0 < n; e0 += kWave) cnt += popc(ballot(e0 + lane < n && lds.lane_max[e0 + lane] >= cand));
-        if (cnt >= K) t = cand;
-      }
-      st.thr = t;
+    // T = the K-th largest of the 64 column maxima (lane l's largest lane maximum over the
+    // waves): K distinct groups reach it, so it is a lower bound of the row's K-th largest
+    // element.  Each lane counts the column maxima above its own.
+    uint32_t cm = 0;
+    for (int j = 0; j < nw; ++j) cm = max(cm, lds.lane_max[j * kWave + lane]);
+    uint32_t* sv = reinterpret_cast<uint32_t*>(s.stage);
+    sv[lane] = cm;
+    __builtin_amdgcn_wave_barrier();
+    int cnt = 0;
+#pragma unroll
+    for (int j = 0; j < kWave; j += 4) {
+      const uint4 v = *reinterpret_cast<const uint4*>(&sv[j]);
+      cnt += (v.x > cm) + (v.y > cm) + (v.z > cm) + (v.w > cm);
     }
+    __builtin_amdgcn_wave_barrier();
+    const int n_live = popc(ballot(cm != 0));
+    st.thr = n_live < K ? 0u : wave_umin(cm != 0 && cnt < K ? cm : ~0u);
   }
   if (sc < nfull) {
     const uint32_t p = passing_groups<T>(gmax, sc * SUB, V, st.thr, false, lane);
@@ -503,34 +557,40 @@ __global__ __launch_bounds__(kWave* kWaves, 4) void topk_row_kernel(const T* __r
   }
   sc += nw;
 
-  // Remaining full sub-chunks, the next two always in flight.
-  while (sc < nfull) {
-    load_full<T>(bufA, rsrc, (sc + 2 * nw) * SUB, lane_off, sc + 2 * nw < nfull);
-    reduce_sub<T>(bufB, gmax, st.lm, st.ls);
+  // Reduces tile c0 and buffers its groups that reach the threshold.
+  auto consume = [&](u32x4 (&buf)[kSubGroups], int64_t c0) {
+    if (c0 == last_c0) mask_tail<T>(buf, c0, V, lane);
+    reduce_sub<T>(buf, gmax, st.lm, st.ls);
     if (!st.overflow && any_pass_full<T>(gmax, st.thr)) {
-      const uint32_t p = passing_groups<T>(gmax, sc * SUB, V, st.thr, false, lane);
-      if (ballot(buffer_groups<T>(bufB, p, sc * SUB, lane, s, st.nbuf) != 0)) st.overflow = true;
+      const uint32_t p = passing_groups<T>(gmax, c0, V, st.thr, false, lane);
+      if (ballot(buffer_groups<T>(buf, p, c0, lane, s, st.nbuf) != 0)) st.overflow = true;
     }
-    sc += nw;
-    if (sc >= nfull) break;
-    load_full<T>(bufB, rsrc, (sc + 2 * nw) * SUB, lane_off, sc + 2 * nw < nfull);
-    reduce_sub<T>(bufC, gmax, st.lm, st.ls);
-    if (!st.overflow && any_pass_full<T>(gmax, st.thr)) {
-      const uint32_t p = passing_groups<T>(gmax, sc * SUB, V, st.thr, false, lane);
-      if (ballot(buffer_groups<T>(bufC, p, sc * SUB, lane, s, st.nbuf) != 0)) st.overflow = true;
+  };
+  // The remaining tiles, the next one always in flight; the last tile issues no load.
+  if (sc < nfull) {
+    int left = static_cast<int>((nfull - 1 - sc) / nw);  // tiles after the current one
+    for (;;) {
+      if (left == 0) {
+        consume(bufB, sc * SUB);
+        break;
+      }
+      set_prio(left--);
+      load_full<T>(bufA, rsrc, (sc + nw) * SUB, lane_off);
+      consume(bufB, sc * SUB);
+      sc += nw;
+      if (left == 0) {
+        consume(bufA, sc * SUB);
+        break;
+      }
+      set_prio(left--);
+      load_full<T>(bufB, rsrc, (sc + nw) * SUB, lane_off);
+      consume(bufA, sc * SUB);
+      sc += nw;
     }
-    sc += nw;
-    if (sc >= nfull) break;
-    load_full<T>(bufC, rsrc, (sc + 2 * nw) * SUB, lane_off, sc + 2 * nw < nfull);
-    reduce_sub<T>(bufA, gmax, st.lm, st.ls);
-    if (!st.overflow && any_pass_full<T>(gmax, st.thr)) {
-      const uint32_t p = passing_groups<T>(gmax, sc * SUB, V, st.thr, false, lane);
-      if (ballot(buffer_groups<T>(bufA, p, sc * SUB, lane, s, st.nbuf) != 0)) st.overflow = true;
-    }
-    sc += nw;
   }
 
-  // Ragged or unaligned sub-chunks: this wave's share of [nfull, nsub).
+  __builtin_amdgcn_s_setprio(3);
+  // Ragged or unaligned tiles: this wave's share of [nfull, nsub).
   for (int64_t sr = nfull + ((w - nfull % nw) + nw) % nw; sr < nsub; sr += nw) {
     load_checked<T, kAligned>(bufA, rsrc, rp, sr * SUB, V, lane);
     reduce_sub<T>(bufA, gmax, st.lm, st.ls);
@@ -540,31 +600,45 @@ __global__ __launch_bounds__(kWave* kWaves, 4) void topk_row_kernel(const T* __r
     }
   }
 
-  // This wave's top-K: one selection over the buffered groups, or the exact re-scan.
-  uint32_t cur_key = 0, cur_id = 0;
-  if (!st.overflow) {
-    if (st.nbuf > 0) {
+  // This wave's live candidates (key >= the threshold) in s.cand: staged straight from
+  // the buffer, or, when there are more than 64 of them or the buffer overflowed, the top
+  // K picked by the radix selection.
+  int n = 0;
+  if (!st.overflow) n = st.nbuf > 0 ? stage_live<T>(s, st.nbuf, V, st.thr, lane) : 0;
+  if (st.overflow || n > kWave) {
+    uint32_t ck = 0, ci = 0;
+    if (!st.overflow) {
       __builtin_amdgcn_wave_barrier();
       const uint2 c = flush<T, true>(s, st.nbuf, V, st.thr, false, K, lane, 0u, 0u);
-      cur_key = c.x;
-      cur_id = c.y;
+      ck = c.x;
+      ci = c.y;
+    } else {
+      const uint2 c = rescan<T, kAligned>(rsrc, rp, w, nsub, nw, V, st.thr, K, lane, s);
+      ck = c.x;
+      ci = c.y;
     }
-  } else {
-    const uint2 c = rescan<T, kAligned>(rsrc, rp, w, nsub, nw, V, st.thr, K, lane, s);
-    cur_key = c.x;
-    cur_id = c.y;
+    const uint64_t m = ballot(ck != 0);
+    __builtin_amdgcn_wave_barrier();
+    if (ck != 0) s.cand[lanes_below(m)] = cand_order(ck, ci);
+    n = popc(m);
+  }
+  __builtin_amdgcn_wave_barrier();
+  {
+    // Rank of each candidate among the wave's: the first K in rank order are the wave's
+    // top K, written sorted; the K-th one's key bounds the row's K-th from below.
+    const uint64_t mine = lane < n ? s.cand[lane] : 0ull;
+    const int r = lane < n ? count_above(s.cand, n, mine) : kWave;
+    if (r < K) lds.part64[w * K + r] = mine;
+    if (n >= K && r == K - 1) atomicMax(&lds.thr2, static_cast<uint32_t>(mine >> 32));
+    if (lane == 0) lds.npart[w] = n < K ? n : K;
   }
 
-  // The wave's (max, sum) and candidates.
   const float wm = wave_max(st.lm);
   const float wsum = wave_sum((st.lm == neg_inf()) ? 0.f : st.ls * fast_exp2((st.lm - wm) * kLog2e));
-  if (lane < K) lds.part[w * K + lane] = make_uint2(cur_key, cur_id);
   if (lane == 0) lds.ms[w] = make_float2(wm, wsum);
   __syncthreads();
   if (w != 0) return;
 
-  // Wave 0 merges the row.  The waves' (max, sum) pairs are read by every lane (LDS
-  // broadcast) and combined without crossing lanes.
   float2 ms[kWaves];
 #pragma unroll
   for (int j = 0; j < kWaves; ++j) ms[j] = lds.ms[j];
@@ -577,26 +651,58 @@ __global__ __launch_bounds__(kWave* kWaves, 4) void topk_row_kernel(const T* __r
     if (j < nw && ms[j].x != neg_inf()) e += ms[j].y * fast_exp2((ms[j].x - m) * kLog2e);
   const float l = (m == neg_inf()) ? neg_inf() : m + fast_log2(e) * kLn2;
 
-  const int total = nw * K;  // <= kWaves * kWave
-  if (total <= kWave)
-    merge_parts<T, 1>(lds.part, total, K, lane, s, cur_key, cur_id);
-  else if (total <= 2 * kWave)
-    merge_parts<T, 2>(lds.part, total, K, lane, s, cur_key, cur_id);
-  else if (total <= 4 * kWave)
-    merge_parts<T, 4>(lds.part, total, K, lane, s, cur_key, cur_id);
-  else
-    merge_parts<T, 8>(lds.part, total, K, lane, s, cur_key, cur_id);
-  // Position of each selected entry in the (value desc, id asc) order.
-  int rank = 0;
-  for (int j = 0; j < K; ++j) {
-    const uint32_t kj = __builtin_amdgcn_readlane(cur_key, j);
-    const uint32_t ij = __builtin_amdgcn_readlane(cur_id, j);
-    rank += (kj > cur_key) || (kj == cur_key && ij < cur_id);
+  // The waves' candidates at or above the best K-th key (a lower bound of the row's K-th
+  // largest), gathered into s.cand; more than 64 of them fall back to the radix merge.
+  const uint32_t t3 = lds.thr2;
+  const int slots = nw * K;
+  int nf = 0;
+  for (int e0 = 0; e0 < slots; e0 += kWave) {
+    const int e = e0 + lane;
+    uint64_t v = 0;
+    if (e < slots) {
+      const int ww = e / K, j = e - ww * K;
+      if (j < lds.npart[ww]) v = lds.part64[e];
+      if (static_cast<uint32_t>(v >> 32) < t3) v = 0;
+    }
+    const uint64_t msk = ballot(v != 0);
+    const int pos = nf + static_cast<int>(lanes_below(msk));
+    if (v != 0 && pos < kWave) s.cand[pos] = v;
+    nf += popc(msk);
   }
-  if (lane < K) {
-    const int64_t o = row * K + rank;
-    const float v = Traits<T>::from_key(cur_key);
-    cand_ids[o] = static_cast<int32_t>(cur_id);
+  __builtin_amdgcn_wave_barrier();
+  uint64_t mine = 0;
+  int r = kWave;
+  if (nf <= kWave) {
+    mine = lane < nf ? s.cand[lane] : 0ull;
+    r = lane < nf ? count_above(s.cand, nf, mine) : kWave;
+  } else {
+    // Rare (heavy ties): radix selection over all the waves' candidates.
+    for (int e = lane; e < slots; e += kWave) {
+      const int ww = e / K, j = e - ww * K;
+      const uint64_t v = j < lds.npart[ww] ? lds.part64[e] : 0ull;
+      lds.part[e] = make_uint2(static_cast<uint32_t>(v >> 32), ~static_cast<uint32_t>(v));
+    }
+    __builtin_amdgcn_wave_barrier();
+    uint32_t ck = 0, ci = 0;
+    if (slots <= 2 * kWave)
+      merge_parts<T, 2>(lds.part, slots, K, lane, s, ck, ci);
+    else if (slots <= 4 * kWave)
+      merge_parts<T, 4>(lds.part, slots, K, lane, s, ck, ci);
+    else
+      merge_parts<T, 8>(lds.part, slots, K, lane, s, ck, ci);
+    const uint64_t msk = ballot(ck != 0);
+    __builtin_amdgcn_wave_barrier();
+    if (ck != 0) s.cand[lanes_below(msk)] = cand_order(ck, ci);
+    const int nk = popc(msk);
+    __builtin_amdgcn_wave_barrier();
+    mine = lane < nk ? s.cand[lane] : 0ull;
+    r = lane < nk ? count_above(s.cand, nk, mine) : kWave;
+  }
+  if (r < K) {
+    const int64_t o = row * K + r;
+    const uint32_t key = static_cast<uint32_t>(mine >> 32);
+    const float v = Traits<T>::from_key(key);
+    cand_ids[o] = static_cast<int32_t>(~static_cast<uint32_t>(mine));
     cand_logit[o] = v;
     if (cand_logprob) cand_logprob[o] = v - l;
   }

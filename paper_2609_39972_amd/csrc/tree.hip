@@ -344,7 +344,6 @@ __global__ __launch_bounds__(kWave) void build_tree_kernel(TreeArgs a, int stage
 //    of them with broadcast reads, so F_d needs no sort and no reordering of registers.
 //  * the supertree keys of all depths are loaded once into registers for Top_budget;
 //    the ancestor mask is built by pointer jumping (ceil(log2(gamma+1)) rounds).
-constexpr int kFastMaxK = 16;
 constexpr int kFastMaxWK = 512;
 constexpr int kFastMaxGW = 1024;
 constexpr int kFastMaxW = 64;
