@@ -38,7 +38,7 @@ def log(msg: str) -> None:
 
 def sweep_source_hash() -> str:
     h = hashlib.sha256()
-    for f in ("topk.hip", "ubt_device.h"):
+    for f in ("topk.hip", "sweep.h", "ubt_device.h"):
         with open(os.path.join(ROOT, "paper_2609_39972_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
