@@ -1,0 +1,519 @@
+// Register-resident tree search (Appendix A, Algorithm 1) for the common shapes, shared
+// by the search kernels and the one-launch draft step: depth-wise expansion (Eq.
+// ubtree-frontier), global pruning (Eq. ubtree-pruning) and the ancestor mask.
+#pragma once
+
+#include "ubt_device.h"
+#include "ubt_launch.h"
+
+namespace ubt {
+namespace {
+
+constexpr int kMaxNodes = 256;
+
+// e / K for 0 <= e < 2^16 and 1 <= K <= 64, with magic = ceil(2^32 / K).
+__device__ __forceinline__ int div_k(int e, uint64_t magic) {
+  return static_cast<int>((static_cast<uint64_t>(static_cast<uint32_t>(e)) * magic) >> 32);
+}
+// ---- register-resident search for the common shapes ---------------------------------
+//
+// Used when K is 4, 8 or 16, W <= 64, W*K <= 512 and gamma*W <= 1024.  Same results as
+// the kernel above.  One wave runs alone per sequence, so a wave issues roughly one
+// instruction per four cycles and every dependent LDS round trip is exposed: the layout
+// is chosen to keep both counts low per depth.
+//  * F_{d-1} is held one entry per lane (score key, position).  Each parent lane has its
+//    slab row q_d[c_p][.] prefetched into registers and writes its K children to a
+//    transpose buffer at index p*K + c, read back 64 entries per row.
+//  * Top_W is a ballot radix selection over the bits below the common prefix of the live
+//    keys (from a DPP max/min), stopping at the first bit that splits exactly W entries
+//    off; a tie exactly at the boundary is resolved by index with mbcnt.
+//  * the W survivors are compacted to LDS and each lane ranks its own entry against all
+//    of them with broadcast reads, so F_d needs no sort and no reordering of registers.
+//  * the supertree keys of all depths are loaded once into registers for Top_budget;
+//    the ancestor mask is built by pointer jumping (ceil(log2(gamma+1)) rounds).
+constexpr int kFastMaxWK = 512;
+constexpr int kFastMaxGW = 1024;
+constexpr int kFastMaxW = 64;
+constexpr int kStageLive = 272;                // up to 255 selected entries + 16 zero entries
+constexpr int kStageCap = kStageLive + kWave;  // + one dummy slot per lane
+constexpr int kMaskWords = 8;                  // ceil(256 / 32)
+
+struct FastLayout {
+  uint32_t slab, rmax, cids, xpose, stage, s_key, s_info, f_slot, anc, mk, ready, total;
+};
+
+__host__ __device__ inline FastLayout fast_layout(int gamma, int K, int W) {
+  FastLayout L{};
+  uint32_t p = 0;
+  auto take = [&p](size_t bytes) {
+    const uint32_t at = p;
+    p += static_cast<uint32_t>((bytes + 15) & ~static_cast<size_t>(15));
+    return at;
+  };
+  L.slab = take(static_cast<size_t>(gamma) * K * K * sizeof(float));
+  L.rmax = take(static_cast<size_t>(gamma) * K * sizeof(float));
+  L.cids = take(static_cast<size_t>(gamma) * K * sizeof(int32_t));
+  L.xpose = take(kFastMaxWK * sizeof(float));
+  L.stage = take(kStageCap * sizeof(uint2));
+  L.s_key = take(static_cast<size_t>(gamma) * W * sizeof(uint32_t));
+  L.s_info = take(static_cast<size_t>(gamma) * W * sizeof(uint32_t));
+  L.f_slot = take(static_cast<size_t>(gamma) * W * sizeof(int32_t));
+  L.anc = take(kMaxNodes * sizeof(int32_t));
+  L.mk = take(kMaxNodes * kMaskWords * sizeof(uint32_t));
+  L.ready = take(static_cast<size_t>(gamma) * sizeof(uint32_t));
+  L.total = p;
+  return L;
+}
+
+__host__ __device__ inline bool fast_tree_fits(int gamma, int K, int W) {
+  return (K == 4 || K == 8 || K == 16) && W <= kFastMaxW && W * K <= kFastMaxWK && gamma * W <= kFastMaxGW;
+}
+
+// Selects the `need` best live entries under (key desc, index asc), where entry (r, lane)
+// has index r*64 + lane and key 0 marks a dead entry (rows past the data hold key 0).
+// kmax and kmin, if given (kmin != 0), are the largest live key and a lower bound of the
+// need-th largest one; otherwise they are taken from the keys.
+template <int R>
+__device__ __forceinline__ void select_best(const uint32_t (&key)[R], int n_live, int need, uint64_t (&sel)[R],
+                                            uint32_t kmax = 0u, uint32_t kmin = 0u) {
+  if (n_live <= need) {
+#pragma unroll
+    for (int r = 0; r < R; ++r) sel[r] = ballot(key[r] != 0u);
+    return;
+  }
+  if (kmin == 0u) {
+    uint32_t hi = 0, lo = ~0u;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      hi = max(hi, key[r]);
+      lo = min(lo, key[r] != 0u ? key[r] : ~0u);
+    }
+    kmax = wave_umax(hi);
+    kmin = wave_umin(lo);
+  }
+  // The need-th largest key lies in [kmin, kmax], so it shares the bits above the
+  // highest bit where the two differ.
+  uint32_t t = kmax;
+  if (kmax != kmin) {
+    uint32_t m = 0x80000000u >> __clz(kmax ^ kmin);
+    t = kmax & ~(m | (m - 1u));
+    // One exit: the loop ends at an exact split (the entries at or above cand) or after
+    // the last bit, with t the need-th largest key.
+    int cnt;
+    do {
+      const uint32_t cand = t | m;
+      cnt = 0;
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        sel[r] = ballot(key[r] >= cand);
+        cnt += popc(sel[r]);
+      }
+      t = cnt > need ? cand : t;
+      m = radix_next(m, cnt, need, 0u);
+    } while (m != 0u);
+    if (cnt == need) return;
+  }
+  // t is the need-th largest key: take every key above t and the entries equal to t of
+  // smallest index.
+  int left = need;
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    sel[r] = ballot(key[r] > t);
+    left -= popc(sel[r]);
+  }
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const uint64_t eq = ballot(key[r] == t);
+    const int c = popc(eq);
+    if (left >= c) {
+      sel[r] |= eq;
+      left -= c;
+    } else if (left > 0) {
+      sel[r] |= ballot(lane_in(eq) && static_cast<int>(lanes_below(eq)) < left);
+      left = 0;
+    }
+  }
+}
+
+// Writes the selected entries to stage[0..n) in index order as (x = ~index, y = key), so
+// that the 64-bit value y:x orders entries by (key desc, index asc), then 16 zero
+// entries.  Lanes with nothing to write store to their own dummy slot (no branches).
+template <int R>
+__device__ __forceinline__ void compact_selected(uint2* stage, const uint32_t (&key)[R], const uint64_t (&sel)[R],
+                                                 int n, int lane) {
+  const int dummy = kStageLive + lane;
+  int pos = 0;
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int at = lane_in(sel[r]) ? pos + static_cast<int>(lanes_below(sel[r])) : dummy;
+    stage[at] = make_uint2(~static_cast<uint32_t>(r * kWave + lane), key[r]);
+    pos += popc(sel[r]);
+  }
+  stage[lane < 16 ? n + lane : dummy] = make_uint2(0u, 0u);
+  __builtin_amdgcn_wave_barrier();
+}
+
+__device__ __forceinline__ uint64_t order_value(uint32_t x, uint32_t y) {
+  return (static_cast<uint64_t>(y) << 32) | x;
+}
+
+// Number of the n staged entries that come before `mine`.  Entries n..n+15 are zero, so
+// whole chunks of 16 entries are compared; the next chunk is loaded before the current
+// one is compared.
+__device__ __forceinline__ int rank_in_stage(const uint2* stage, int n, uint64_t mine) {
+  const uint4* s4 = reinterpret_cast<const uint4*>(stage);
+  const int chunks = (n + 15) >> 4;
+  uint4 cur[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) cur[i] = s4[i];
+  int rank = 0;
+  for (int ch = 0; ch < chunks; ++ch) {
+    uint4 nxt[8];
+    if (ch + 1 < chunks) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) nxt[i] = s4[(ch + 1) * 8 + i];
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      rank += order_value(cur[i].x, cur[i].y) > mine ? 1 : 0;
+      rank += order_value(cur[i].z, cur[i].w) > mine ? 1 : 0;
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) cur[i] = nxt[i];
+  }
+  return rank;
+}
+
+template <int KT>
+__device__ __forceinline__ void load_row(const float* row, float (&v)[KT]) {
+#pragma unroll
+  for (int i = 0; i < KT / 4; ++i) {
+    const float4 t = reinterpret_cast<const float4*>(row)[i];
+    v[4 * i] = t.x;
+    v[4 * i + 1] = t.y;
+    v[4 * i + 2] = t.z;
+    v[4 * i + 3] = t.w;
+  }
+}
+
+struct FastSmem {
+  float* slab;
+  float* rmax;  // per slab row: its largest entry
+  int32_t* cids;
+  float* xpose;
+  uint2* stage;
+  uint32_t* s_key;
+  uint32_t* s_info;
+  int32_t* f_slot;
+  int32_t* anc;
+  uint32_t* mk;
+  uint32_t* ready;  // per position: its slab is in LDS (one-launch kernel only)
+};
+
+// Top_budget over the supertree: stages the selected entries (as compact_selected does).
+template <int RS>
+__device__ __forceinline__ void prune_supertree(const FastSmem& sm, int GW, int total, int n_sel, int lane) {
+  uint32_t skey[RS];
+#pragma unroll
+  for (int r = 0; r < RS; ++r) {
+    const int f = r * kWave + lane;
+    const uint32_t k = sm.s_key[f < GW ? f : GW - 1];
+    skey[r] = f < GW ? k : 0u;
+  }
+  uint64_t ssel[RS];
+  select_best<RS>(skey, total, n_sel, ssel);
+  compact_selected<RS>(sm.stage, skey, ssel, n_sel, lane);
+}
+
+__device__ __forceinline__ FastSmem fast_smem(unsigned char* raw, const FastLayout& L) {
+  FastSmem sm;
+  sm.slab = reinterpret_cast<float*>(raw + L.slab);
+  sm.rmax = reinterpret_cast<float*>(raw + L.rmax);
+  sm.cids = reinterpret_cast<int32_t*>(raw + L.cids);
+  sm.xpose = reinterpret_cast<float*>(raw + L.xpose);
+  sm.stage = reinterpret_cast<uint2*>(raw + L.stage);
+  sm.s_key = reinterpret_cast<uint32_t*>(raw + L.s_key);
+  sm.s_info = reinterpret_cast<uint32_t*>(raw + L.s_info);
+  sm.f_slot = reinterpret_cast<int32_t*>(raw + L.f_slot);
+  sm.anc = reinterpret_cast<int32_t*>(raw + L.anc);
+  sm.mk = reinterpret_cast<uint32_t*>(raw + L.mk);
+  sm.ready = reinterpret_cast<uint32_t*>(raw + L.ready);
+  return sm;
+}
+
+// rmax[e] = the largest entry of slab row e, for rows e0, e0 + stride, ... < e1.
+template <int KT>
+__device__ __forceinline__ void slab_row_max(const float* slab, float* rmax, int e0, int e1, int stride) {
+  for (int e = e0; e < e1; e += stride) {
+    float v[KT];
+    load_row<KT>(slab + e * KT, v);
+    float m = v[0];
+#pragma unroll
+    for (int c = 1; c < KT; ++c) m = fmaxf(m, v[c]);
+    rmax[e] = m;
+  }
+}
+
+// Publishes slab i to the workgroup: every lane's earlier LDS writes complete before the
+// flag is set.
+__device__ __forceinline__ void publish_slab(uint32_t* ready, int i) {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __hip_atomic_store(&ready[i], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
+// Waits until slab i has been published.  Its producer is another wave of the same
+// workgroup that runs unconditionally, so the flag is always set; the wait is bounded
+// all the same.
+__device__ __forceinline__ void wait_slab(uint32_t* ready, int i) {
+  for (int spin = 0; spin < (1 << 22); ++spin) {
+    const uint32_t f = __hip_atomic_load(&ready[i], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP);
+    if (__builtin_amdgcn_readfirstlane(f) != 0u) return;
+    __builtin_amdgcn_s_sleep(1);
+  }
+}
+
+// Depth-wise expansion (Eq. ubtree-frontier): F_d = Top_W(E_d) for d = 1..gamma.  F_d is
+// ranked (score desc, parent position, candidate rank) as it is formed and stored in that
+// order to s_key / s_info (parent = its position in F_{d-1}), with the supertree outputs
+// if asked.  total = the number of supertree nodes.
+template <int KT, int R, bool kWait>
+__device__ __forceinline__ void expand_depths(const TreeArgs& a, const FastSmem& sm, int64_t b, int lane,
+                                              int& total) {
+  constexpr int kLogK = KT == 4 ? 2 : (KT == 8 ? 3 : 4);
+  const int gamma = a.gamma, W = a.W;
+  // Frontier entry on lane j < np: score key, position in F, and its slab row for the
+  // next depth (prefetched as soon as the entry's candidate rank is known).
+  uint32_t fkey = f32_key(0.f);
+  int fpos = 0;
+  float nq[KT];
+  if (kWait) wait_slab(sm.ready, 0);
+  load_row<KT>(sm.slab, nq);  // depth 1 extends the root through row 0
+  float rm = sm.rmax[0];
+  int np = 1;
+  total = 0;
+  const float zeta = a.zeta;
+  const bool with_zeta = zeta != 0.f;
+  for (int d = 1; d <= gamma; ++d) {
+    // Each parent's best child comes from its row maximum (rounding is monotone, so it
+    // is exactly the largest of the children computed below).  With at least W parents,
+    // W extensions reach the smallest of these, a lower bound of the W-th best one.
+    uint32_t best_key = 0u;
+    if (lane < np) {
+      const float base = f32_key_value(fkey);
+      float v[KT];
+#pragma unroll
+      for (int c = 0; c < KT; ++c) v[c] = base + nq[c];
+      float best = base + rm;
+      if (with_zeta) {
+#pragma unroll
+        for (int c = 0; c < KT; ++c) v[c] += zeta;
+        best += zeta;
+      }
+      best_key = f32_key(best);
+      float4* dst = reinterpret_cast<float4*>(sm.xpose + fpos * KT);
+#pragma unroll
+      for (int i = 0; i < KT / 4; ++i) dst[i] = make_float4(v[4 * i], v[4 * i + 1], v[4 * i + 2], v[4 * i + 3]);
+    }
+    __builtin_amdgcn_wave_barrier();
+    const int n = np * KT;
+    uint32_t key[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const int e = r * kWave + lane;
+      const float x = sm.xpose[e];
+      key[r] = e < n ? f32_key(x) : 0u;
+    }
+    const int w_d = n < W ? n : W;
+    uint64_t sel[R];
+    if (np >= W) {
+      const uint32_t kmax = wave_umax(best_key);
+      const uint32_t kbound = wave_umin(lane < np ? best_key : ~0u);
+      select_best<R>(key, n, w_d, sel, kmax, kbound);
+    } else {
+      select_best<R>(key, n, w_d, sel);
+    }
+    compact_selected<R>(sm.stage, key, sel, w_d, lane);
+    const uint2 st = sm.stage[lane];
+    const bool have = lane < w_d;
+    const uint32_t mx = have ? st.x : 0u, my = have ? st.y : 0u;
+    const int e = have ? static_cast<int>(~mx) : 0;
+    const int p = e >> kLogK;
+    const int c = e & (KT - 1);
+    if (d < gamma) {
+      if (kWait) wait_slab(sm.ready, d);
+      load_row<KT>(sm.slab + (d * KT + c) * KT, nq);
+      rm = sm.rmax[d * KT + c];
+    }
+    const int rank = rank_in_stage(sm.stage, w_d, order_value(mx, my));
+    const int fb = (d - 1) * W;
+    if (have) {
+      sm.s_key[fb + rank] = my;
+      sm.s_info[fb + rank] = static_cast<uint32_t>(p) | (static_cast<uint32_t>(c) << 16);
+    } else if (lane < W) {
+      sm.s_key[fb + lane] = 0u;
+    }
+    if (a.f_count) {
+      if (lane == 0) a.f_count[b * gamma + d - 1] = w_d;
+      const int64_t o = (b * gamma + d - 1) * W;
+      if (have) {
+        a.f_parent[o + rank] = p;
+        a.f_cand[o + rank] = c;
+        a.f_score[o + rank] = f32_key_value(my);
+      } else if (lane < W) {
+        a.f_parent[o + lane] = -1;
+        a.f_cand[o + lane] = -1;
+        a.f_score[o + lane] = neg_inf();
+      }
+    }
+    fkey = my;
+    fpos = rank;
+    np = w_d;
+    total += w_d;
+    __builtin_amdgcn_wave_barrier();
+  }
+}
+
+// Algorithm 1 for sequence b, run by one wavefront once the sequence's candidate ids are
+// in LDS and, unless kWait, all its score slabs; with kWait the slab of position i is
+// awaited before depth i + 1 first reads it.
+template <int KT, int R, bool kWait>
+__device__ __forceinline__ void fast_search(const TreeArgs& a, const FastSmem& sm, int64_t b, int lane,
+                                            uint64_t magic_w) {
+  const int gamma = a.gamma, W = a.W;
+  const int GW = gamma * W;
+
+  int total = 0;
+  expand_depths<KT, R, kWait>(a, sm, b, lane, total);
+
+  // ---- global pruning: Top_budget over the supertree --------------------------------
+  const int n_sel = total < a.budget ? total : a.budget;
+  if (GW <= 4 * kWave)
+    prune_supertree<4>(sm, GW, total, n_sel, lane);
+  else if (GW <= 8 * kWave)
+    prune_supertree<8>(sm, GW, total, n_sel, lane);
+  else
+    prune_supertree<16>(sm, GW, total, n_sel, lane);
+  // Emission order = rank under (score desc, depth asc, position asc); slot = 1 + rank.
+  const int nrows = (n_sel + kWave - 1) / kWave;  // <= 4
+  uint2 ent[4];
+  int slot[4];
+#pragma unroll
+  for (int rb = 0; rb < 4; ++rb) {
+    const int i = rb * kWave + lane;
+    const uint2 st = sm.stage[i];
+    ent[rb] = i < n_sel ? st : make_uint2(0u, 0u);
+    slot[rb] = 0;
+    if (rb < nrows) {
+      slot[rb] = 1 + rank_in_stage(sm.stage, n_sel, order_value(ent[rb].x, ent[rb].y));
+      if (i < n_sel) sm.f_slot[~ent[rb].x] = slot[rb];
+    }
+  }
+  __builtin_amdgcn_wave_barrier();
+
+  const int N = a.budget + 1;
+  const int words = (N + 31) / 32;
+  const int n_nodes = 1 + n_sel;
+  int32_t* tok = a.token + b * N;
+  int32_t* par = a.parent + b * N;
+  int32_t* dep = a.depth + b * N;
+  int32_t* crk = a.cand_rank + b * N;
+  float* scr = a.score + b * N;
+  if (lane == 0) {
+    a.n_nodes[b] = n_nodes;
+    tok[0] = a.anchor[b];
+    par[0] = -1;
+    dep[0] = 0;
+    crk[0] = -1;
+    scr[0] = 0.f;
+    sm.anc[0] = -1;
+  }
+#pragma unroll
+  for (int rb = 0; rb < 4; ++rb) {
+    if (rb < nrows && rb * kWave + lane < n_sel) {
+      const int f = static_cast<int>(~ent[rb].x);
+      const int d = div_k(f, magic_w) + 1;
+      const uint32_t info = sm.s_info[f];
+      const int p = static_cast<int>(info & 0xFFFFu);
+      const int c = static_cast<int>(info >> 16);
+      const int ps = d == 1 ? 0 : sm.f_slot[(d - 2) * W + p];
+      const int s = slot[rb];
+      tok[s] = sm.cids[(d - 1) * KT + c];
+      par[s] = ps;
+      dep[s] = d;
+      crk[s] = c;
+      scr[s] = f32_key_value(ent[rb].y);
+      sm.anc[s] = ps;
+    }
+  }
+  for (int n = n_nodes + lane; n < N; n += kWave) {
+    tok[n] = -1;
+    par[n] = -1;
+    dep[n] = -1;
+    crk[n] = -1;
+    scr[n] = neg_inf();
+  }
+  __builtin_amdgcn_wave_barrier();
+
+  // ---- ancestor mask by pointer jumping ------------------------------------------------
+  // After round k, m covers the node and its 2^k - 1 nearest ancestors and `up` points
+  // 2^k steps up; a chain has at most gamma + 1 nodes.
+  if (a.mask) {
+    const int mrows = (N + kWave - 1) / kWave;  // <= 4
+    uint32_t m[4][kMaskWords];
+    int up[4];
+#pragma unroll
+    for (int rb = 0; rb < 4; ++rb) {
+      const int n = rb * kWave + lane;
+      const bool live = rb < mrows && n < n_nodes;
+      const int an = sm.anc[n < n_nodes ? n : 0];
+      up[rb] = live ? an : -1;
+#pragma unroll
+      for (int w = 0; w < kMaskWords; ++w) m[rb][w] = (live && (n >> 5) == w) ? (1u << (n & 31)) : 0u;
+    }
+    int rounds = 0;
+    while ((1 << rounds) < gamma + 1) ++rounds;
+    for (int it = 0; it < rounds; ++it) {
+#pragma unroll
+      for (int rb = 0; rb < 4; ++rb) {
+        const int n = rb * kWave + lane;
+        if (rb < mrows && n < n_nodes) {
+          uint4* dst = reinterpret_cast<uint4*>(sm.mk + n * kMaskWords);
+          dst[0] = make_uint4(m[rb][0], m[rb][1], m[rb][2], m[rb][3]);
+          dst[1] = make_uint4(m[rb][4], m[rb][5], m[rb][6], m[rb][7]);
+          sm.anc[n] = up[rb];
+        }
+      }
+      __builtin_amdgcn_wave_barrier();
+#pragma unroll
+      for (int rb = 0; rb < 4; ++rb) {
+        if (rb < mrows && up[rb] >= 0) {
+          const uint4* src = reinterpret_cast<const uint4*>(sm.mk + up[rb] * kMaskWords);
+          const uint4 lo = src[0], hi = src[1];
+          m[rb][0] |= lo.x;
+          m[rb][1] |= lo.y;
+          m[rb][2] |= lo.z;
+          m[rb][3] |= lo.w;
+          m[rb][4] |= hi.x;
+          m[rb][5] |= hi.y;
+          m[rb][6] |= hi.z;
+          m[rb][7] |= hi.w;
+          up[rb] = sm.anc[up[rb]];
+        }
+      }
+      __builtin_amdgcn_wave_barrier();
+    }
+    uint32_t* mrow = a.mask + b * static_cast<int64_t>(N) * words;
+#pragma unroll
+    for (int rb = 0; rb < 4; ++rb) {
+      const int n = rb * kWave + lane;
+      if (rb < mrows && n < N) {
+#pragma unroll
+        for (int w = 0; w < kMaskWords; ++w)
+          if (w < words) mrow[n * words + w] = m[rb][w];
+      }
+    }
+  }
+}
+
+}  // namespace
+}  // namespace ubt
