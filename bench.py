@@ -1,16 +1,18 @@
 """Benchmark of one UBTree draft step on one MI355X.
 
-A step is the whole hot path on one batch of synthetic proposer outputs:
-ubt_topk (softmax statistics + top-K over the vocabulary), then ubt_draft_tree, which
-does ubt_bigram_scores (selector scores + normalisation) and ubt_build_tree (beam
-search, pruning, tree and ancestor mask) in one launch (``--separate``: the two calls).  Steps rotate over a pool of distinct logit buffers whose total size
+A step is the whole hot path on one batch of synthetic proposer outputs: softmax
+statistics and top-K over the vocabulary, selector scores and normalisation, beam
+search, pruning, tree and ancestor mask.  By default it is ubt_topk then
+ubt_draft_tree (selector and search in one launch); ``--mode step`` runs the whole step
+as one ubt_draft_step call (one kernel launch), ``--mode separate`` the three calls
+ubt_topk, ubt_bigram_scores and ubt_build_tree.  Steps rotate over a pool of distinct logit buffers whose total size
 exceeds the 256 MB last-level cache, so every step reads its logits from HBM.  Inputs
 are resident in HBM before the timed region; the steps are captured once into a HIP
 graph and replayed.
 
-Prints one JSON line: trees/s (value), ms per step, the sweep kernel's achieved HBM
-bandwidth against the 8 TB/s peak (roofline), and the fp64 oracle timed on the host
-cores (cpu_baseline).
+Prints one JSON line: trees/s (value), ms per step, the step kernel's achieved HBM
+bandwidth against the 8 TB/s peak (roofline; the sweep alone is reported beside it), and
+the fp64 oracle timed on the host cores (cpu_baseline).
 """
 from __future__ import annotations
 
@@ -29,30 +31,32 @@ METRIC = "draft trees/sec and µs/step at B=32, V=151936; achieved HBM GB/s vs p
 HBM_PEAK_GBPS = 8000.0
 POOL_BYTES = 512 << 20  # pool size that defeats the 256 MB Infinity Cache
 SWEEP_KERNEL = "topk_row_kernel"
-TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "topk_sweep_zipf-v151936-b32_counters.md")
+STEP_KERNEL = "draft_step_kernel"
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "draft_step_zipf-v151936-b32_counters.md")
+STEP_SOURCES = ("step.hip", "sweep.h", "search.h", "bigram_tile.h", "ubt_device.h")
 
 
 def log(msg: str) -> None:
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def sweep_source_hash() -> str:
+def source_hash(files=STEP_SOURCES) -> str:
     h = hashlib.sha256()
-    for f in ("topk.hip", "sweep.h", "ubt_device.h"):
+    for f in files:
         with open(os.path.join(ROOT, "paper_2609_39972_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
 
 
 def measured_traffic() -> dict | None:
-    """HBM bytes per sweep launch from the committed counter summary, if it was taken on
-    the current sweep source."""
+    """HBM bytes per step-kernel launch from the committed counter summary, if it was
+    taken on the current source of that kernel."""
     if not os.path.exists(TRAFFIC_PROFILE):
         return None
     txt = open(TRAFFIC_PROFILE).read()
     m_hash = re.search(r"source hash:\s*`?([0-9a-f]{16})", txt)
     m_bytes = re.search(r"hbm bytes per launch:\s*([0-9.eE+]+)", txt)
-    if not (m_hash and m_bytes) or m_hash.group(1) != sweep_source_hash():
+    if not (m_hash and m_bytes) or m_hash.group(1) != source_hash():
         return None
     return {"bytes": float(m_bytes.group(1))}
 
@@ -82,8 +86,9 @@ def main() -> int:
     ap.add_argument("--workload", type=int, default=3, help="synthetic workload id (3 = B=32, V=151936 headline)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="minimum oracle time for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--separate", action="store_true",
-                    help="run the selector and the search as two calls instead of ubt_draft_tree")
+    ap.add_argument("--mode", choices=("step", "tree", "separate"), default="tree",
+                    help="step: one ubt_draft_step call; tree: ubt_topk + ubt_draft_tree; separate: ubt_topk + "
+                         "ubt_bigram_scores + ubt_build_tree")
     ap.add_argument("--sweep-launches", type=int, default=200, help="launches per kernel in the per-kernel timing")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run a plain device copy of known size (counter calibration) and exit")
@@ -132,7 +137,8 @@ def main() -> int:
             host0 = dict(d, phi=phi_np, psi=psi_np)
         step = ubt.DraftStep(w.B, w.gamma, w.V, w.K, w.W, w.budget, phi, psi, to_dev(d["gate"]),
                              torch.from_numpy(d["anchor"]).to(dev), d["alpha"], d["lam"], w.zeta,
-                             fused=not args.separate)
+                             fused=args.mode != "separate", one_call=args.mode == "step",
+                             logit_dtype=torch.bfloat16 if w.dtype == "bf16" else torch.float32)
         bufs.append((to_dev_logits(d["logits"]), step))
     torch.cuda.synchronize()
     log(f"inputs resident in HBM ({time.perf_counter() - t0:.1f} s)")
@@ -210,9 +216,23 @@ def main() -> int:
                                               bufs[j % pool][1].lam, w.W, w.budget, w.zeta,
                                               bufs[j % pool][1].sel["logq"], bufs[j % pool][1].tree), n)
     sweep_bytes = w.logit_bytes
-    achieved = sweep_bytes / (sweep_us * 1e-6) / 1e9
-    log(f"sweep {sweep_us:.2f} us ({achieved:.0f} GB/s), selector {bigram_us:.2f} us, tree {tree_us:.2f} us, "
+    sweep_gbps = sweep_bytes / (sweep_us * 1e-6) / 1e9
+    log(f"sweep {sweep_us:.2f} us ({sweep_gbps:.0f} GB/s), selector {bigram_us:.2f} us, tree {tree_us:.2f} us, "
         f"selector + tree in one launch {draft_us:.2f} us")
+    # The whole step as one launch (ubt_draft_step); its algorithmic bytes are the logits
+    # plus the selector's gathers and writes and the tree outputs.
+    step_us = timed(lambda j: bufs[j % pool][1].run(bufs[j % pool][0]), n) if args.mode == "step" else None
+    es = 2 if w.feat_dtype == "bf16" else 4
+    sel_bytes = (w.B * ((w.gamma - 1) * w.K + 1) * w.r * es        # phi rows of the predecessors
+                 + w.B * w.gamma * w.K * w.r * es                  # psi rows of the candidates
+                 + w.B * w.gamma * w.r * es                        # gate rows
+                 + w.B * w.gamma * w.K * w.K * 4)                  # logq
+    cand_bytes = w.B * w.gamma * (w.K * 12 + 4)                   # ids, logits, log-probs, lse
+    words = -(-w.N // 32)
+    tree_bytes = w.B * w.N * (5 * 4 + 4 * words) + w.B * 4        # tree arrays, mask, n_nodes
+    step_bytes = sweep_bytes + sel_bytes + cand_bytes + tree_bytes
+    if step_us is not None:
+        log(f"one-launch step {step_us:.2f} us ({step_bytes / (step_us * 1e-6) / 1e9:.0f} GB/s)")
 
     traffic = measured_traffic()
     cpu = None
@@ -239,15 +259,28 @@ def main() -> int:
         "config": {"workload": w.name, "B": w.B, "L": w.L, "gamma": w.gamma, "V": w.V, "K": w.K, "r": w.r,
                    "budget": w.budget, "W": w.W, "logits": f"{w.dtype} {w.logits}", "features": w.feat_dtype,
                    "pool_buffers": pool, "graph": f"{pool} steps per HIP graph, replayed {replays} times"},
-        "kernels_us": {"topk_sweep": round(sweep_us, 3), "bigram": round(bigram_us, 3), "build_tree": round(tree_us, 3),
-                       "draft_tree": round(draft_us, 3)},
-        "step_calls": "ubt_bigram_scores + ubt_build_tree" if args.separate else "ubt_draft_tree",
-        "roofline": {"bound": "hbm", "kernel": SWEEP_KERNEL, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
-                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
-                     "traffic": None if traffic is None else traffic["bytes"],
-                     "algorithmic_bytes_per_launch": sweep_bytes, "source_hash": sweep_source_hash()},
+        "kernels_us": {"draft_step": None if step_us is None else round(step_us, 3),
+                       "topk_sweep": round(sweep_us, 3), "bigram": round(bigram_us, 3),
+                       "build_tree": round(tree_us, 3), "draft_tree": round(draft_us, 3)},
+        "step_calls": {"step": "ubt_draft_step", "tree": "ubt_topk + ubt_draft_tree",
+                       "separate": "ubt_topk + ubt_bigram_scores + ubt_build_tree"}[args.mode],
+        "sweep_alone": {"kernel": SWEEP_KERNEL, "us": round(sweep_us, 3), "GB/s": round(sweep_gbps, 1),
+                        "frac": round(sweep_gbps / HBM_PEAK_GBPS, 4), "bytes": sweep_bytes},
         "cpu_baseline": cpu,
     }
+    if step_us is not None:
+        achieved = step_bytes / (step_us * 1e-6) / 1e9
+        res["roofline"] = {"bound": "hbm", "kernel": STEP_KERNEL, "achieved": round(achieved, 1),
+                           "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                           "traffic": None if traffic is None else traffic["bytes"],
+                           "algorithmic_bytes_per_launch": step_bytes, "source_hash": source_hash()}
+    else:
+        res["roofline"] = {"bound": "hbm", "kernel": SWEEP_KERNEL, "achieved": round(sweep_gbps, 1),
+                           "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(sweep_gbps / HBM_PEAK_GBPS, 4),
+                           "traffic": None, "algorithmic_bytes_per_launch": sweep_bytes}
+    res = {k: res[k] for k in ("metric", "value", "unit", "n_gpus", "steps", "warmup", "ms_per_step", "us_per_step",
+                               "higher_is_better", "scaling", "vs_baseline", "dtype", "data", "config", "kernels_us",
+                               "step_calls", "roofline", "sweep_alone", "cpu_baseline")}
     print(json.dumps(res), flush=True)
     return 0
 

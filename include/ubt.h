@@ -59,7 +59,7 @@ typedef enum ubt_status {
   UBT_ERR_SHAPE = 2,       /* a size, stride or limit is violated */
   UBT_ERR_VALUE = 3,       /* a scalar argument is out of range (zeta > 0, alpha <= 0, ...) */
   UBT_ERR_UNSUPPORTED = 4, /* a valid combination this build does not handle */
-  UBT_ERR_WORKSPACE = 5,   /* reserved */
+  UBT_ERR_WORKSPACE = 5,   /* a required workspace is missing, too small or misaligned */
   UBT_ERR_HIP = 6          /* a HIP launch failed; see ubt_last_hip_error() */
 } ubt_status_t;
 
@@ -184,6 +184,45 @@ ubt_status_t ubt_draft_tree(const void* phi_tab, const void* psi_tab, const void
                             float zeta, float* logq, int32_t* n_nodes, int32_t* token,
                             int32_t* parent, int32_t* depth, int32_t* cand_rank, float* score,
                             uint32_t* mask, hipStream_t stream);
+
+/* ------------------------------------------------------------------------------------
+ * ubt_draft_step -- one whole draft step: ubt_topk, then ubt_draft_tree, in one call.
+ * Method / Unigram Proposer, Eq. (ubtree-unigram) and "Candidate Sets"; Method /
+ * Parallel Computation, Eq. (ubtree-edge-matrix); Depth Calibration, Eq.
+ * (ubtree-depth); Appendix A / Path Scores, Eq. (ubtree-path); Appendix A, Algorithm 1
+ * with Eqs. (ubtree-frontier) and (ubtree-pruning); Verification via Tree-attention.
+ *
+ * The arguments are those of the two calls with the same meaning, layout and checks
+ * (cand_ids, cand_logit and logq are required outputs here).  cand_ids, cand_logit,
+ * logq and every tree output are bit-identical to those of ubt_topk followed by
+ * ubt_draft_tree; lse and cand_logprob agree to fp32 rounding (the sums run in another
+ * order).
+ *
+ * When the rows are 16-byte aligned and V * sizeof(element) is a multiple of 16, the
+ * features are bf16, B <= 64, and the search shape is one ubt_draft_tree handles in one
+ * launch, the whole step is ONE kernel launch: the sweep streams the rows in draft-depth
+ * order and each sequence's search runs while later depths are still being read.  That
+ * launch needs `workspace`: device memory of at least
+ * ubt_draft_step_workspace_bytes(B, gamma, V, K, dt) bytes, 256-byte aligned, owned by
+ * the caller and ZERO-FILLED before its first use.  Each launch resets the counters it
+ * keeps there, so one workspace serves any number of consecutive calls on one stream;
+ * calls that may overlap need separate workspaces.  The first 4 bytes (uint32) become
+ * nonzero if a wait inside the launch timed out (outputs are then unspecified and the
+ * workspace must be zero-filled again); this never happens in normal operation.  A missing,
+ * short or misaligned workspace returns UBT_ERR_WORKSPACE.  Other shapes run the two
+ * calls' kernels in order on `stream` and ignore the workspace.
+ * ------------------------------------------------------------------------------------ */
+size_t ubt_draft_step_workspace_bytes(int B, int gamma, int64_t V, int K, ubt_dtype_t dt);
+
+ubt_status_t ubt_draft_step(const void* logits, ubt_dtype_t dt, int B, int gamma, int64_t V,
+                            int64_t stride_b, int64_t stride_i, int K, const void* phi_tab,
+                            const void* psi_tab, const void* gate, ubt_dtype_t feat_dt, int r,
+                            const int32_t* anchor, const float* alpha, const float* lambda, int W,
+                            int budget, float zeta, int32_t* cand_ids, float* cand_logit,
+                            float* cand_logprob, float* lse, float* logq, int32_t* n_nodes,
+                            int32_t* token, int32_t* parent, int32_t* depth, int32_t* cand_rank,
+                            float* score, uint32_t* mask, void* workspace, size_t workspace_bytes,
+                            hipStream_t stream);
 
 /* ------------------------------------------------------------------------------------
  * ubt_tree_mask -- the ancestor ("tree attention") mask of a tree given by parent

@@ -13,10 +13,12 @@ Calls, in pipeline order (the paper's section and equation names in brackets):
   [Eq. dflash2-selector, ubtree-depth, ubtree-edge-matrix, ubtree-path];
 * :func:`build_tree` -- beam search with global pruning and the ancestor mask
   [Appendix A, Algorithm 1];
-* :func:`tree_mask` -- the ancestor mask of any parent-pointer tree.
+* :func:`tree_mask` -- the ancestor mask of any parent-pointer tree;
+* :func:`draft_step` -- the whole step in one call (one kernel launch for the common
+  shapes; it needs a zero-filled workspace from :func:`draft_step_workspace`).
 
-:class:`DraftStep` preallocates everything for one workload shape and runs the three
-calls back to back on one stream (graph-capturable).
+:class:`DraftStep` preallocates everything for one workload shape and runs the step on
+one stream (graph-capturable).
 """
 from __future__ import annotations
 
@@ -34,7 +36,8 @@ STATUS = {0: "UBT_OK", 1: "UBT_ERR_NULL", 2: "UBT_ERR_SHAPE", 3: "UBT_ERR_VALUE"
 
 # Every symbol include/ubt.h declares.
 EXPORTS = ("ubt_status_str", "ubt_abi_version", "ubt_last_hip_error", "ubt_topk",
-           "ubt_bigram_scores", "ubt_build_tree", "ubt_draft_tree", "ubt_tree_mask")
+           "ubt_bigram_scores", "ubt_build_tree", "ubt_draft_tree", "ubt_draft_step_workspace_bytes",
+           "ubt_draft_step", "ubt_tree_mask")
 
 _p = ctypes.c_void_p
 _i32 = ctypes.c_int
@@ -72,7 +75,13 @@ def lib() -> ctypes.CDLL:
         L.ubt_draft_tree.argtypes = [_p, _p, _p, _i32, _i64, _i32, _p, _p, _p, _p, _p, _i32, _i32, _i32, _i32, _i32,
                                      _f32, _p, _p, _p, _p, _p, _p, _p, _p, _p]
         L.ubt_tree_mask.argtypes = [_p, _p, _i32, _i32, _p, _p]
-        for f in (L.ubt_topk, L.ubt_bigram_scores, L.ubt_build_tree, L.ubt_draft_tree, L.ubt_tree_mask):
+        L.ubt_draft_step_workspace_bytes.argtypes = [_i32, _i32, _i64, _i32, _i32]
+        L.ubt_draft_step_workspace_bytes.restype = ctypes.c_size_t
+        L.ubt_draft_step.argtypes = [_p, _i32, _i32, _i32, _i64, _i64, _i64, _i32, _p, _p, _p, _i32, _i32, _p, _p,
+                                     _p, _i32, _i32, _f32, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p,
+                                     ctypes.c_size_t, _p]
+        for f in (L.ubt_topk, L.ubt_bigram_scores, L.ubt_build_tree, L.ubt_draft_tree, L.ubt_tree_mask,
+                  L.ubt_draft_step):
             f.restype = _i32
         _lib = L
     return _lib
@@ -244,17 +253,70 @@ def tree_mask(parent: torch.Tensor, n_nodes: torch.Tensor, out: torch.Tensor | N
     return out
 
 
+def draft_step_workspace(B: int, gamma: int, V: int, K: int, dtype=torch.bfloat16, device="cuda") -> torch.Tensor:
+    """A zero-filled workspace for :func:`draft_step` (uint8, 256-byte aligned).  Each
+    call resets the counters it uses, so one workspace serves consecutive calls on one
+    stream."""
+    code = UBT_BF16 if dtype == torch.bfloat16 else UBT_F32
+    n = lib().ubt_draft_step_workspace_bytes(B, gamma, V, K, code)
+    if n == 0:
+        raise ValueError("invalid shape for ubt_draft_step")
+    ws = torch.zeros(n, dtype=torch.uint8, device=device)
+    if ws.data_ptr() % 256:
+        raise RuntimeError("workspace is not 256-byte aligned")
+    return ws
+
+
+def draft_step(logits: torch.Tensor, phi: torch.Tensor, psi: torch.Tensor, gate: torch.Tensor, anchor: torch.Tensor,
+               alpha, lam, K: int, W: int, budget: int, zeta: float = 0.0, workspace: torch.Tensor | None = None,
+               cand: dict | None = None, logq: torch.Tensor | None = None, out: dict | None = None,
+               with_mask: bool = True, stream=None) -> dict:
+    """The whole draft step (``topk`` then ``draft_tree``) in one library call; returns the
+    candidates, ``logq`` and the tree outputs."""
+    _need_gpu(logits, phi, psi, gate, anchor)
+    if logits.dim() != 3 or logits.stride(2) != 1:
+        raise ValueError("logits must be [B, gamma, V] with unit stride along V")
+    for n, t in (("phi", phi), ("psi", psi), ("gate", gate), ("anchor", anchor)):
+        _contig(t, n)
+    B, gamma, V = logits.shape
+    r = phi.shape[1]
+    dev = logits.device
+    f32 = dict(dtype=torch.float32, device=dev)
+    if cand is None:
+        cand = dict(cand_ids=torch.empty(B, gamma, K, dtype=torch.int32, device=dev),
+                    cand_logit=torch.empty(B, gamma, K, **f32), cand_logprob=torch.empty(B, gamma, K, **f32),
+                    lse=torch.empty(B, gamma, **f32))
+    if logq is None:
+        logq = torch.empty(B, gamma, K, K, **f32)
+    if out is None:
+        out = tree_outputs(B, gamma, W, budget, dev, with_mask)
+    if workspace is None:
+        workspace = draft_step_workspace(B, gamma, V, K, logits.dtype, dev)
+    a, l = _host_f32(alpha, gamma), _host_f32(lam, gamma)
+    st = lib().ubt_draft_step(_ptr(logits), _dtype_code(logits), B, gamma, V, logits.stride(0), logits.stride(1), K,
+                              _ptr(phi), _ptr(psi), _ptr(gate), _dtype_code(phi), r, _ptr(anchor), a, l, W, budget,
+                              float(zeta), _ptr(cand["cand_ids"]), _ptr(cand["cand_logit"]),
+                              _ptr(cand.get("cand_logprob")), _ptr(cand.get("lse")), _ptr(logq),
+                              _ptr(out["n_nodes"]), _ptr(out["token"]), _ptr(out["parent"]), _ptr(out["depth"]),
+                              _ptr(out["cand_rank"]), _ptr(out["score"]), _ptr(out.get("mask")), _ptr(workspace),
+                              workspace.numel(), _stream(stream))
+    _check("ubt_draft_step", st)
+    return {**cand, "logq": logq, **out}
+
+
 class DraftStep:
     """One draft step (top-K -> selector -> tree + mask) with every buffer preallocated.
 
     ``run(logits)`` issues the library calls on the current stream and allocates nothing,
-    so it can be captured into a HIP graph.  By default the selector and the search go
-    through ``ubt_draft_tree`` (one call); ``fused=False``, ``with_delta`` or ``debug``
-    use the separate ``ubt_bigram_scores`` and ``ubt_build_tree`` calls."""
+    so it can be captured into a HIP graph.  By default it is ``ubt_topk``, then the
+    selector and the search through ``ubt_draft_tree``; ``one_call=True`` makes the whole
+    step one ``ubt_draft_step`` call; ``fused=False``, ``with_delta`` or ``debug`` use the
+    separate ``ubt_topk``, ``ubt_bigram_scores`` and ``ubt_build_tree`` calls."""
 
     def __init__(self, B: int, gamma: int, V: int, K: int, W: int, budget: int, phi: torch.Tensor,
                  psi: torch.Tensor, gate: torch.Tensor, anchor: torch.Tensor, alpha, lam, zeta: float = 0.0,
-                 with_delta: bool = False, debug: bool = False, fused: bool = True):
+                 with_delta: bool = False, debug: bool = False, fused: bool = True, one_call: bool = False,
+                 logit_dtype=torch.bfloat16):
         dev = phi.device
         self.shape = (B, gamma, V, K, W, budget)
         self.phi, self.psi, self.gate, self.anchor = phi, psi, gate, anchor
@@ -268,8 +330,15 @@ class DraftStep:
                         logq=torch.empty(B, gamma, K, K, **f32))
         self.tree = tree_outputs(B, gamma, W, budget, dev, True, debug)
         self.fused = fused and not with_delta and not debug
+        self.one_call = one_call and self.fused
+        self.workspace = draft_step_workspace(B, gamma, V, K, logit_dtype, dev) if self.one_call else None
+        self.logit_dtype_code = UBT_BF16 if logit_dtype == torch.bfloat16 else UBT_F32
 
     def run(self, logits: torch.Tensor, stream=None) -> dict:
+        if self.one_call:
+            draft_step(logits, self.phi, self.psi, self.gate, self.anchor, self.alpha, self.lam, self.K, self.W,
+                       self.budget, self.zeta, self.workspace, self.cand, self.sel["logq"], self.tree, stream=stream)
+            return {**self.cand, **self.sel, **self.tree}
         topk(logits, self.K, self.cand, stream=stream)
         if self.fused:
             draft_tree(self.phi, self.psi, self.gate, self.anchor, self.cand["cand_ids"], self.cand["cand_logit"],

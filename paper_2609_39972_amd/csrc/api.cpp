@@ -174,6 +174,61 @@ ubt_status_t ubt_draft_tree(const void* phi_tab, const void* psi_tab, const void
   return hip_status(ubt::launch_build_tree(a, stream));
 }
 
+size_t ubt_draft_step_workspace_bytes(int B, int gamma, int64_t V, int K, ubt_dtype_t dt) {
+  if (B < 1 || gamma < 1 || gamma > UBT_MAX_GAMMA || K < 1 || K > UBT_MAX_K || V < K || V >= (int64_t(1) << 31) ||
+      !valid_dtype(dt))
+    return 0;
+  return ubt::step_plan(B, gamma, V, K, static_cast<int>(dt)).bytes;
+}
+
+ubt_status_t ubt_draft_step(const void* logits, ubt_dtype_t dt, int B, int gamma, int64_t V, int64_t stride_b,
+                            int64_t stride_i, int K, const void* phi_tab, const void* psi_tab, const void* gate,
+                            ubt_dtype_t feat_dt, int r, const int32_t* anchor, const float* alpha,
+                            const float* lambda, int W, int budget, float zeta, int32_t* cand_ids, float* cand_logit,
+                            float* cand_logprob, float* lse, float* logq, int32_t* n_nodes, int32_t* token,
+                            int32_t* parent, int32_t* depth, int32_t* cand_rank, float* score, uint32_t* mask,
+                            void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (!logits || !cand_ids || !cand_logit || !logq) return UBT_ERR_NULL;
+  if (!valid_dtype(dt)) return UBT_ERR_VALUE;
+  if (B < 1 || gamma < 1 || gamma > UBT_MAX_GAMMA || K < 1 || K > UBT_MAX_K || V < K || V >= (int64_t(1) << 31))
+    return UBT_ERR_SHAPE;
+  if (stride_i < V || stride_b < static_cast<int64_t>(gamma) * stride_i) return UBT_ERR_SHAPE;
+  if (V * (dt == UBT_BF16 ? 2 : 4) >= (int64_t(1) << 32)) return UBT_ERR_SHAPE;
+  ubt::Scales sc;
+  ubt_status_t st = check_selector(phi_tab, psi_tab, gate, feat_dt, V, r, anchor, cand_ids, cand_logit, alpha, lambda,
+                                   B, gamma, K, sc);
+  if (st != UBT_OK) return st;
+  ubt::TreeArgs a;
+  st = check_tree(anchor, cand_ids, B, gamma, K, W, budget, zeta, n_nodes, token, parent, depth, cand_rank, score,
+                  mask, a);
+  if (st != UBT_OK) return st;
+  a.logq = logq;
+  const int64_t es = dt == UBT_BF16 ? 2 : 4;
+  const bool aligned = aligned16(logits) && (stride_b * es) % 16 == 0 && (stride_i * es) % 16 == 0;
+  if (!ubt::draft_step_fused(static_cast<int>(dt), aligned, B, gamma, V, K, static_cast<int>(feat_dt), W)) {
+    st = hip_status(ubt::launch_topk(logits, static_cast<int>(dt), aligned, B, gamma, V, stride_b, stride_i, K,
+                                     cand_ids, cand_logit, cand_logprob, lse, stream));
+    if (st != UBT_OK) return st;
+    return ubt_draft_tree(phi_tab, psi_tab, gate, feat_dt, V, r, anchor, cand_ids, cand_logit, alpha, lambda, B,
+                          gamma, K, W, budget, zeta, logq, n_nodes, token, parent, depth, cand_rank, score, mask,
+                          stream);
+  }
+  if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0 ||
+      workspace_bytes < ubt::step_plan(B, gamma, V, K, static_cast<int>(dt)).bytes)
+    return UBT_ERR_WORKSPACE;
+  ubt::SelectorArgs s;
+  s.phi = static_cast<const uint16_t*>(phi_tab);
+  s.psi = static_cast<const uint16_t*>(psi_tab);
+  s.gate = static_cast<const uint16_t*>(gate);
+  s.V = V;
+  s.r = r;
+  s.cand_logit = cand_logit;
+  s.logq = logq;
+  s.sc = sc;
+  return hip_status(ubt::launch_draft_step(logits, static_cast<int>(dt), B, gamma, V, stride_b, stride_i, K, cand_ids,
+                                           cand_logit, cand_logprob, lse, s, a, workspace, stream));
+}
+
 ubt_status_t ubt_tree_mask(const int32_t* parent, const int32_t* n_nodes, int B, int N, uint32_t* mask,
                            hipStream_t stream) {
   if (!parent || !n_nodes || !mask) return UBT_ERR_NULL;

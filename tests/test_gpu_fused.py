@@ -28,7 +28,7 @@ def _both(w: synth.Workload, W: int, buf: int = 0) -> tuple[dict, dict]:
             dev_i32(d["anchor"]), d["alpha"], d["lam"], w.zeta)
     logits = dev_values(d["logits"])
     sep = ubt.DraftStep(*args, fused=False)
-    fus = ubt.DraftStep(*args, fused=True)
+    fus = ubt.DraftStep(*args, fused=True, one_call=False)
     assert fus.fused and not sep.fused
     a = to_np(sep.run(logits))
     torch.cuda.synchronize()

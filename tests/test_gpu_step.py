@@ -1,0 +1,235 @@
+"""GPU tests of ubt_draft_step, the whole step in one call (one kernel launch for the
+common shapes).  Its candidates, logq and trees must be bit-identical to ubt_topk
+followed by the separate selector and search calls (whose parity with the oracle the
+pipeline tests establish); its LSE and log-probs are summed in another order and must
+agree with the oracle within the fp32 score tolerance.  Also: the workspace counters are
+reset and its error word clear after every call, repeated calls on one workspace
+give identical bits, graph replays match eager calls, and the shapes that stress the
+one-launch kernel (ties across many tiles, rows whose top elements sit outside the
+sample tiles, few tiles per row, fp32 logits, one position, 64 sequences) and the
+two-launch fallback."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+import oracle
+import parity
+import synth
+
+pytestmark = pytest.mark.gpu
+
+EXACT_KEYS = ("cand_ids", "cand_logit", "logq", "n_nodes", "token", "parent", "depth", "cand_rank", "score", "mask")
+
+
+def _args(w: synth.Workload, d: dict, W: int):
+    from gpu_util import dev_i32, dev_values
+
+    return (w.B, w.gamma, w.V, w.K, W, w.budget, dev_values(d["phi"]), dev_values(d["psi"]), dev_values(d["gate"]),
+            dev_i32(d["anchor"]), d["alpha"], d["lam"], w.zeta)
+
+
+def _logits_tensor(w: synth.Workload, d: dict):
+    from gpu_util import dev_values
+
+    return dev_values(d["logits"])
+
+
+def _run_both(w: synth.Workload, d: dict, W: int) -> tuple[dict, dict, object]:
+    import torch
+
+    import paper_2609_39972_amd as ubt
+    from gpu_util import to_np
+
+    args = _args(w, d, W)
+    logits = _logits_tensor(w, d)
+    dtype = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    sep = ubt.DraftStep(*args, fused=False)
+    one = ubt.DraftStep(*args, one_call=True, logit_dtype=dtype)
+    a = to_np(sep.run(logits))
+    torch.cuda.synchronize()
+    b = to_np(one.run(logits))
+    torch.cuda.synchronize()
+    return a, b, one
+
+
+def _check_workspace(step) -> None:
+    """The error word is clear and every row's counters (tiles done and threshold: the
+    first 8 bytes of each row block) are back to zero."""
+    B, gamma, V, K = step.shape[:4]
+    ws = step.workspace.cpu().numpy()
+    assert int(ws[:4].view(np.uint32)[0]) == 0, "a wait inside the launch timed out"
+    tile = 2048 if step.logit_dtype_code == 1 else 1024
+    nt = -(-V // tile)
+    row_bytes = -(-(16 + nt * 16 + nt * K * 8 + nt * 16 * 16 + nt * 16 * 4) // 256) * 256
+    rows = B * gamma
+    assert ws.size >= 256 + rows * row_bytes
+    blocks = ws[256:256 + rows * row_bytes].reshape(rows, row_bytes)
+    assert not blocks[:, :8].any(), "row counters were not reset"
+
+
+def _same(a: dict, b: dict, logit_dtype: str) -> None:
+    for k in EXACT_KEYS:
+        assert a[k].dtype == b[k].dtype
+        if a[k].dtype == np.float32:
+            assert np.array_equal(a[k].view(np.uint32), b[k].view(np.uint32)), f"{k} differs"
+        else:
+            assert np.array_equal(a[k], b[k]), f"{k} differs"
+    # LSE and log-probs: fp32 sums in another order.
+    for k in ("lse", "cand_logprob"):
+        ref = a[k].astype(np.float64)
+        assert np.all(np.abs(b[k] - ref) <= 1e-5 * np.maximum(1.0, np.abs(ref))), f"{k} differs beyond 1e-5"
+
+
+def _check(w: synth.Workload, W: int, d: dict | None = None, buf: int = 0, vs_oracle: bool = True) -> None:
+    from gpu_util import say
+
+    say(f"draft_step workload {w.cfg} buf={buf} W={W}: {w.describe()}")
+    if d is None:
+        d = synth.inputs(w, buf)
+    a, b, one = _run_both(w, d, W)
+    _same(a, b, w.dtype)
+    if one.workspace is not None:
+        _check_workspace(one)
+    if vs_oracle:
+        parity.check_topk(b, oracle.topk(d["logits"], w.K))
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+def test_step_workload(cfg):
+    w = synth.WORKLOADS[cfg]
+    _check(w, w.W)
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4])
+def test_step_best_first_width(cfg):
+    w = synth.WORKLOADS[cfg]
+    _check(w, w.budget, vs_oracle=False)
+
+
+def test_step_repeat_and_pool():
+    """One workspace, consecutive calls over different logit buffers and back: bitwise
+    identical results for the same input, and the workspace clean after each."""
+    import torch
+
+    import paper_2609_39972_amd as ubt
+    from gpu_util import say, to_np
+
+    w = synth.WORKLOADS[3]
+    say("draft_step repeat: workload 3, buffers 0, 1, 0")
+    d0, d1 = synth.inputs(w, 0), synth.inputs(w, 1)
+    one = ubt.DraftStep(*_args(w, d0, w.W), one_call=True)
+    r0 = to_np(one.run(_logits_tensor(w, d0)))
+    torch.cuda.synchronize()
+    _check_workspace(one)
+    r1 = to_np(one.run(_logits_tensor(w, d1)))
+    torch.cuda.synchronize()
+    _check_workspace(one)
+    r2 = to_np(one.run(_logits_tensor(w, d0)))
+    torch.cuda.synchronize()
+    _check_workspace(one)
+    for k in r0:
+        assert np.array_equal(r0[k], r2[k]), f"{k} differs between identical calls"
+    assert not np.array_equal(r0["cand_ids"], r1["cand_ids"])
+    parity.check_topk(r1, oracle.topk(d1["logits"], w.K))
+
+
+def test_step_graph_replay():
+    """The step captured in a HIP graph: every replay, with eager work in between,
+    matches the eager call."""
+    import torch
+
+    import paper_2609_39972_amd as ubt
+    from gpu_util import say, to_np
+
+    w = synth.WORKLOADS[3]
+    say("draft_step graph replay: workload 3")
+    d = synth.inputs(w, 0)
+    logits = _logits_tensor(w, d)
+    one = ubt.DraftStep(*_args(w, d, w.W), one_call=True)
+    ref = to_np(one.run(logits))
+    torch.cuda.synchronize()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(s):
+        one.run(logits)  # warm-up on the capture stream
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g, stream=s):
+            out = one.run(logits)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        for v in out.values():
+            if v is not None:
+                v.fill_(0)
+        g.replay()
+        torch.cuda.synchronize()
+        got = to_np(out)
+        for k in ref:
+            assert np.array_equal(ref[k], got[k]), f"{k} differs after a graph replay"
+        _check_workspace(one)
+        one.run(logits)  # eager call between replays
+        torch.cuda.synchronize()
+
+
+def _custom(cfg: int, **kw) -> synth.Workload:
+    base = dict(V=20000, dtype="bf16", feat_dtype="bf16", logits="normal", logit_std=2.0, K=8, r=32, budget=24, W=6)
+    base.update(kw)
+    return synth.custom(cfg, **base)
+
+
+@pytest.mark.parametrize("kw", [
+    dict(B=3, L=4),                                   # few rows: stream tiles run before their samples
+    dict(B=1, L=2, K=16, W=8, budget=40),             # one position
+    dict(B=2, L=9, V=5000, K=4, W=3, budget=12),      # 3 tiles per row: every tile a sample
+    dict(B=2, L=9, V=16384 + 8, K=8),                 # a ragged last tile of 8 elements
+    dict(B=64, L=3, V=3000, K=4, W=4, budget=16),     # 64 searchers
+    dict(B=2, L=6, V=30000, dtype="f32", feat_dtype="bf16", K=8),  # fp32 logits
+    dict(B=2, L=6, V=10000, K=16, W=32, budget=60),   # W * K = 512
+    dict(B=2, L=6, V=10000, K=5, W=4, budget=20),     # K outside {4, 8, 16}: two launches
+    dict(B=2, L=6, V=10001, K=8, W=4, budget=20),     # V * 2 bytes not a multiple of 16: two launches
+])
+def test_step_shapes(kw):
+    w = _custom(300, **kw)
+    _check(w, w.W)
+
+
+def test_step_ties_everywhere():
+    """Constant rows and rows with long runs of equal top values: tiles hold more groups
+    at the threshold than their records keep, and the merge reads them again; ids must
+    come out lowest first."""
+    w = _custom(301, B=2, L=5, V=40000)
+    d = synth.inputs(w, 0)
+    lg = d["logits"].copy()
+    lg[0, 0, :] = lg[0, 0, 0]                      # constant row
+    lg[0, 1, :] = lg[0, 1, :].min()                # floor everywhere ...
+    lg[0, 1, 25000:25000 + 3000] = lg[0, 1, 5]     # ... and a run of 3000 equal values late in the row
+    lg[1, 2, ::7] = lg[1, 2, 3]                    # every 7th element equal
+    d["logits"] = lg
+    _check(w, w.W, d=d)
+
+
+def test_step_top_outside_samples():
+    """Rows whose largest values all sit far from the first (sample) tiles."""
+    w = _custom(302, B=2, L=5, V=60000, K=16, W=8, budget=40)
+    d = synth.inputs(w, 0)
+    lg = d["logits"].copy()
+    rng = np.random.default_rng(7)
+    for b in range(w.B):
+        for i in range(w.gamma):
+            idx = rng.choice(np.arange(40000, 60000), size=40, replace=False)
+            lg[b, i, idx] = synth.store(np.full(40, 12.0) + rng.normal(0, 0.5, 40), w.dtype)
+    d["logits"] = lg
+    _check(w, w.W, d=d)
+
+
+def test_step_neg_inf():
+    """Rows that are mostly -inf (bf16 0xFF80), with a few finite values in late tiles."""
+    w = _custom(303, B=2, L=4, V=30000, K=8)
+    d = synth.inputs(w, 0)
+    lg = d["logits"].copy()
+    lg[0, 0, :] = 0xFF80
+    lg[0, 0, 29990:] = synth.store(np.linspace(-1, 1, 10), "bf16")
+    lg[1, 1, 100:] = 0xFF80
+    d["logits"] = lg
+    _check(w, w.W, d=d)
