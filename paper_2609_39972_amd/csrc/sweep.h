@@ -83,15 +83,18 @@ struct WaveLds {
   uint64_t cand[kWave];       // live candidates as 64-bit order values
 };
 
-struct RowLds {
-  WaveLds wave[kWaves];
-  uint64_t part64[kWaves * kWave];  // wave w's top candidates, sorted, at [w*K, w*K + npart[w])
-  int npart[kWaves];
+// Shared memory of one row's workgroup of up to MW waves.
+template <int MW>
+struct RowLdsT {
+  WaveLds wave[MW];
+  uint64_t part64[MW * kWave];  // wave w's top candidates, sorted, at [w*K, w*K + npart[w])
+  int npart[MW];
   uint32_t thr2;                     // max over the waves of their K-th candidate key
-  uint2 part[kWaves * kWave];        // (key, id) copy of part64 for the radix fallback
-  float2 ms[kWaves];                 // each wave's (max, sum)
-  uint32_t lane_max[kWaves * kWave]; // lane maxima (keys) of every wave's first tile
+  uint2 part[MW * kWave];        // (key, id) copy of part64 for the radix fallback
+  float2 ms[MW];                 // each wave's (max, sum)
+  uint32_t lane_max[MW * kWave]; // lane maxima (keys) of every wave's first tile
 };
+using RowLds = RowLdsT<kWaves>;
 
 // A buffer resource covering one row: loads address it with a 32-bit offset in a scalar
 // descriptor instead of a 64-bit address per lane, and offsets past the row read zero.
@@ -501,10 +504,10 @@ struct RowOut {
   }
 };
 
-// The row at rp (V elements) of global row index `row`; the workgroup has up to kWaves
-// waves and `lds` is its shared memory.  Writes cand_*[row * K, row * K + K) and lse[row].
-template <typename T, bool kAligned>
-__device__ __forceinline__ void sweep_row(RowLds& lds, const T* __restrict__ rp, int64_t V, int K, int64_t row,
+// The row at rp (V elements) of global row index `row`; the workgroup has up to MW waves
+// and `lds` is its shared memory.  Writes cand_*[row * K, row * K + K) and lse[row].
+template <typename T, bool kAligned, int MW = kWaves>
+__device__ __forceinline__ void sweep_row(RowLdsT<MW>& lds, const T* __restrict__ rp, int64_t V, int K, int64_t row,
                                           const RowOut& out) {
   constexpr int EPG = Traits<T>::kPer;
   constexpr int64_t SUB = static_cast<int64_t>(kSubGroups) * kWave * EPG;
@@ -654,15 +657,15 @@ __device__ __forceinline__ void sweep_row(RowLds& lds, const T* __restrict__ rp,
   __syncthreads();
   if (w != 0) return;
 
-  float2 ms[kWaves];
+  float2 ms[MW];
 #pragma unroll
-  for (int j = 0; j < kWaves; ++j) ms[j] = lds.ms[j];
+  for (int j = 0; j < MW; ++j) ms[j] = lds.ms[j];
   float m = neg_inf();
 #pragma unroll
-  for (int j = 0; j < kWaves; ++j) m = j < nw ? fmaxf(m, ms[j].x) : m;
+  for (int j = 0; j < MW; ++j) m = j < nw ? fmaxf(m, ms[j].x) : m;
   float e = 0.f;
 #pragma unroll
-  for (int j = 0; j < kWaves; ++j)
+  for (int j = 0; j < MW; ++j)
     if (j < nw && ms[j].x != neg_inf()) e += ms[j].y * fast_exp2((ms[j].x - m) * kLog2e);
   const float l = (m == neg_inf()) ? neg_inf() : m + fast_log2(e) * kLn2;
 

@@ -63,18 +63,13 @@ struct SelectorArgs {
 bool draft_tree_fused(int feat_dtype, int gamma, int K, int W);
 hipError_t launch_draft_tree(const SelectorArgs& s, const TreeArgs& a, hipStream_t stream);
 
-// ---- the whole step in one launch -----------------------------------------------------
-constexpr int kSampleTiles = 8;         // sample tiles per row (the first ones)
-constexpr int kMaxStepTiles = 512;      // tiles per row
+// ---- the whole step: head rows, then tail rows beside the searchers -----------------
 constexpr int kMaxStepSequences = 64;   // searcher workgroups
-struct StepPlan {
-  int nt, S;
-  size_t off_ent, off_grp, off_gpos, row_bytes, bytes;  // per-row block layout; total bytes
-};
-StepPlan step_plan(int B, int gamma, int64_t V, int K, int dtype);
-// True if one launch handles the shape: aligned rows whose byte length is a multiple of
-// 16, bf16 features, the register-resident search, B <= kMaxStepSequences and at most
-// kMaxStepTiles tiles per row.
+// Workspace bytes of launch_draft_step: an error word and one flag per row.
+size_t step_workspace_bytes(int B, int gamma);
+// True if the two-launch step handles the shape: aligned rows, bf16 features, the
+// register-resident search, B <= kMaxStepSequences, and enough compute units that the
+// searchers and the tail rows fit side by side.
 bool draft_step_fused(int dtype, bool aligned, int B, int gamma, int64_t V, int K, int feat_dtype, int W);
 hipError_t launch_draft_step(const void* logits, int dtype, int B, int gamma, int64_t V, int64_t stride_b,
                              int64_t stride_i, int K, int32_t* cand_ids, float* cand_logit, float* cand_logprob,
