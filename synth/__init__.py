@@ -85,6 +85,11 @@ WORKLOADS = {
                 dtype="bf16", feat_dtype="bf16", logits="normal", logit_std=0.7, steps=1000),
     5: Workload(5, "zipf-v151936-b256", B=256, L=32, V=151936, K=16, r=256, budget=128, W=24,
                 dtype="bf16", feat_dtype="bf16", logits="zipf", steps=200),
+    # The paper's own configuration (Appendix, Table "UBTree configuration": 15 future
+    # positions plus the anchor, K = 64, W = 12, budget 64, selector rank 256, zeta = 0)
+    # on the headline batch of 32 sequences.
+    6: Workload(6, "paper-k64-v151936-b32", B=32, L=16, V=151936, K=64, r=256, budget=64, W=12,
+                dtype="bf16", feat_dtype="bf16", logits="zipf", steps=1000),
 }
 
 

@@ -46,13 +46,13 @@ def _same(a: dict, b: dict) -> None:
             assert np.array_equal(a[k], b[k]), f"{k} differs"
 
 
-@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5, 6])
 def test_fused_workload(cfg):
     w = synth.WORKLOADS[cfg]
     _same(*_both(w, w.W))
 
 
-@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5, 6])
 def test_fused_best_first_width(cfg):
     w = synth.WORKLOADS[cfg]
     _same(*_both(w, w.budget))

@@ -1,5 +1,5 @@
 """End-to-end GPU parity of one draft step (top-K -> selector -> tree + mask) against
-the oracle, on the five workloads at full size and at the exact best-first width."""
+the oracle, on the six workloads at full size and at the exact best-first width."""
 from __future__ import annotations
 
 import numpy as np
@@ -35,13 +35,13 @@ def test_workload1_exact():
     _check_workload(synth.WORKLOADS[1], synth.WORKLOADS[1].W)
 
 
-@pytest.mark.parametrize("cfg", [2, 3, 4, 5])
+@pytest.mark.parametrize("cfg", [2, 3, 4, 5, 6])
 def test_workload_full_size(cfg):
     w = synth.WORKLOADS[cfg]
     _check_workload(w, w.W)
 
 
-@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5, 6])
 def test_workload_best_first_width(cfg):
     w = synth.WORKLOADS[cfg]
     _check_workload(w, w.budget)

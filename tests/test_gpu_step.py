@@ -89,7 +89,7 @@ def _check(w: synth.Workload, W: int, d: dict | None = None, buf: int = 0, vs_or
         parity.check_topk(b, oracle.topk(d["logits"], w.K))
 
 
-@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5, 6])
 def test_step_workload(cfg):
     w = synth.WORKLOADS[cfg]
     _check(w, w.W)
