@@ -11,6 +11,12 @@
  *   ubt_build_tree     per sequence: beam search + global pruning -> tree and mask
  *   ubt_tree_mask      (optional) the ancestor mask of any parent-pointer tree
  *
+ * and the tree is then verified by the target model:
+ *
+ *   ubt_tree_attention every node attends to the committed context and its ancestors
+ *   ubt_verify_accept  the accepted path and the bonus token
+ *   ubt_commit_kv      the accepted path's keys and values appended to the cache
+ *
  * ubt_draft_tree does ubt_bigram_scores + ubt_build_tree in one call (one launch for
  * the common shapes).
  *
@@ -241,6 +247,83 @@ ubt_status_t ubt_draft_step(const void* logits, ubt_dtype_t dt, int B, int gamma
  * ------------------------------------------------------------------------------------ */
 ubt_status_t ubt_tree_mask(const int32_t* parent, const int32_t* n_nodes, int B, int N,
                            uint32_t* mask, hipStream_t stream);
+
+/* ====================================================================================
+ * Verification of a draft tree (the consumer of the tree and its mask).
+ * Appendix A / Verification via Tree-attention; Background, "Tree Drafting".
+ * ==================================================================================== */
+
+/* ------------------------------------------------------------------------------------
+ * ubt_tree_attention -- attention of every tree node over the committed context and its
+ * own ancestors.  Appendix A / Verification via Tree-attention: the whole tree is
+ * verified in one target forward pass, each node evaluated under its own
+ * autoregressive prefix (the committed tokens, then the root-to-node path).
+ *
+ * For node n < n_nodes[b] and query head h (key/value head h / (H / H_kv)):
+ *   out[b, n, h] = sum_j softmax_j(scale * q[b, n, h] . k_j) v_j
+ * over j = the cache positions 0..prefix_len[b]-1 and the tree nodes m < n_nodes[b]
+ * whose bit m is set in mask row n (its ancestors and itself, as ubt_build_tree and
+ * ubt_tree_mask write it).  lse[b, n, h] = the natural log of the softmax denominator
+ * plus its maximum.  Rows n >= n_nodes[b] are written as 0 (lse -inf).
+ *
+ * q           : bf16 [B, N, H, D], 16-byte aligned.
+ * k_cache,
+ * v_cache     : bf16 [B, P_max, H_kv, D], 16-byte aligned (may be NULL if P_max == 0).
+ * prefix_len  : int32 [B], values clamped to [0, P_max].
+ * k_tree,
+ * v_tree      : bf16 [B, N, H_kv, D], the keys and values of the tree nodes (root at
+ *               slot 0), 16-byte aligned.
+ * mask        : uint32 [B, N, ceil(N/32)], LSB-first.
+ * n_nodes     : int32 [B], values clamped to [0, N].
+ * N           : 1 <= N <= UBT_MAX_BUDGET + 1; H % H_kv == 0; D in {64, 128}
+ *               (UBT_ERR_UNSUPPORTED otherwise); scale > 0 and finite.
+ * out         : [B, N, H, D] of out_dt (bf16 rounds to nearest even, or f32),
+ *               16-byte aligned.
+ * lse         : optional float [B, N, H].
+ * Products run on bf16 MFMA with fp32 accumulation; the probabilities are rounded to
+ * bf16 before the value product.
+ * ------------------------------------------------------------------------------------ */
+ubt_status_t ubt_tree_attention(const void* q, const void* k_cache, const void* v_cache,
+                                const int32_t* prefix_len, int64_t P_max, const void* k_tree,
+                                const void* v_tree, const uint32_t* mask, const int32_t* n_nodes,
+                                int B, int N, int H, int H_kv, int D, float scale, void* out,
+                                ubt_dtype_t out_dt, float* lse, hipStream_t stream);
+
+/* ------------------------------------------------------------------------------------
+ * ubt_verify_accept -- the acceptance walk.  Appendix A / Verification via
+ * Tree-attention: from the root, follow the child whose token equals the target model's
+ * sample at the current node, until no child matches; that sample is the bonus token.
+ *
+ * token, parent : int32 [B, N], a tree as ubt_build_tree writes it (parent[n] < n).
+ * n_nodes       : int32 [B], clamped to [1, N].
+ * target        : int32 [B, N]: target[b, n] is the target's sample after node n's prefix.
+ * accept_len    : int32 [B], the number of accepted non-root nodes.
+ * accept_nodes  : int32 [B, N]: node 0, then the accepted nodes in path order, then -1.
+ * bonus         : int32 [B].
+ * Only nodes after the current one are searched, and among several matching children
+ * the lowest index is taken, so any input ends the walk within N steps.
+ * ------------------------------------------------------------------------------------ */
+ubt_status_t ubt_verify_accept(const int32_t* token, const int32_t* parent,
+                               const int32_t* n_nodes, const int32_t* target, int B, int N,
+                               int32_t* accept_len, int32_t* accept_nodes, int32_t* bonus,
+                               hipStream_t stream);
+
+/* ------------------------------------------------------------------------------------
+ * ubt_commit_kv -- carries the key/value rows of the accepted path into the cache.
+ * Appendix A / Verification via Tree-attention: the cache along the accepted path moves
+ * on to the next round; other branches are discarded.
+ *
+ * Copies the rows of nodes accept_nodes[b, 0..accept_len[b]] (the root and the accepted
+ * nodes; H_kv * D bf16 each) of k_tree / v_tree [B, N, H_kv, D] to positions
+ * prefix_len[b], prefix_len[b] + 1, ... of k_cache / v_cache [B, P_max, H_kv, D], then
+ * sets prefix_len[b] += accept_len[b] + 1.  Rows that would land at or past P_max are
+ * dropped and prefix_len stops at P_max.  D in {64, 128}; every bf16 array 16-byte
+ * aligned.  Calls on one prefix_len array must not overlap.
+ * ------------------------------------------------------------------------------------ */
+ubt_status_t ubt_commit_kv(const void* k_tree, const void* v_tree, const int32_t* accept_nodes,
+                           const int32_t* accept_len, int32_t* prefix_len, void* k_cache,
+                           void* v_cache, int B, int N, int H_kv, int D, int64_t P_max,
+                           hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -38,7 +38,7 @@ STATUS = {0: "UBT_OK", 1: "UBT_ERR_NULL", 2: "UBT_ERR_SHAPE", 3: "UBT_ERR_VALUE"
 # Every symbol include/ubt.h declares.
 EXPORTS = ("ubt_status_str", "ubt_abi_version", "ubt_last_hip_error", "ubt_topk",
            "ubt_bigram_scores", "ubt_build_tree", "ubt_draft_tree", "ubt_draft_step_workspace_bytes",
-           "ubt_draft_step", "ubt_tree_mask")
+           "ubt_draft_step", "ubt_tree_mask", "ubt_tree_attention", "ubt_verify_accept", "ubt_commit_kv")
 
 _p = ctypes.c_void_p
 _i32 = ctypes.c_int
@@ -81,8 +81,12 @@ def lib() -> ctypes.CDLL:
         L.ubt_draft_step.argtypes = [_p, _i32, _i32, _i32, _i64, _i64, _i64, _i32, _p, _p, _p, _i32, _i32, _p, _p,
                                      _p, _i32, _i32, _f32, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p,
                                      ctypes.c_size_t, _p]
+        L.ubt_tree_attention.argtypes = [_p, _p, _p, _p, _i64, _p, _p, _p, _p, _i32, _i32, _i32, _i32, _i32, _f32,
+                                         _p, _i32, _p, _p]
+        L.ubt_verify_accept.argtypes = [_p, _p, _p, _p, _i32, _i32, _p, _p, _p, _p]
+        L.ubt_commit_kv.argtypes = [_p, _p, _p, _p, _p, _p, _p, _i32, _i32, _i32, _i32, _i64, _p]
         for f in (L.ubt_topk, L.ubt_bigram_scores, L.ubt_build_tree, L.ubt_draft_tree, L.ubt_tree_mask,
-                  L.ubt_draft_step):
+                  L.ubt_draft_step, L.ubt_tree_attention, L.ubt_verify_accept, L.ubt_commit_kv):
             f.restype = _i32
         _lib = L
     return _lib
@@ -303,6 +307,63 @@ def draft_step(logits: torch.Tensor, phi: torch.Tensor, psi: torch.Tensor, gate:
                               workspace.numel(), _stream(stream))
     _check("ubt_draft_step", st)
     return {**cand, "logq": logq, **out}
+
+
+def tree_attention(q: torch.Tensor, k_cache: torch.Tensor | None, v_cache: torch.Tensor | None,
+                   prefix_len: torch.Tensor, k_tree: torch.Tensor, v_tree: torch.Tensor, mask: torch.Tensor,
+                   n_nodes: torch.Tensor, scale: float | None = None, out: torch.Tensor | None = None,
+                   lse: torch.Tensor | None = None, out_dtype=torch.bfloat16, stream=None):
+    """``ubt_tree_attention``: every tree node attends to the committed context and to
+    its ancestors.  q ``[B, N, H, D]`` bf16; caches ``[B, P_max, H_kv, D]`` bf16 (or None
+    with no context); k_tree / v_tree ``[B, N, H_kv, D]`` bf16; mask ``[B, N, words]``
+    int32 (uint32 bits); prefix_len, n_nodes int32 ``[B]``.  Returns (out, lse)."""
+    _need_gpu(q, k_cache, v_cache, prefix_len, k_tree, v_tree, mask, n_nodes)
+    B, N, H, D = q.shape
+    Hkv = k_tree.shape[2]
+    Pmax = 0 if k_cache is None else k_cache.shape[1]
+    for name, t in (("q", q), ("k_tree", k_tree), ("v_tree", v_tree), ("k_cache", k_cache), ("v_cache", v_cache)):
+        if t is not None:
+            _contig(t, name)
+            if t.dtype != torch.bfloat16:
+                raise TypeError(f"{name} must be bfloat16")
+    if scale is None:
+        scale = D ** -0.5
+    if out is None:
+        out = torch.empty(B, N, H, D, dtype=out_dtype, device=q.device)
+    if lse is None:
+        lse = torch.empty(B, N, H, dtype=torch.float32, device=q.device)
+    st = lib().ubt_tree_attention(_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(prefix_len), Pmax, _ptr(k_tree),
+                                  _ptr(v_tree), _ptr(mask), _ptr(n_nodes), B, N, H, Hkv, D, float(scale), _ptr(out),
+                                  _dtype_code(out), _ptr(lse), _stream(stream))
+    _check("ubt_tree_attention", st)
+    return out, lse
+
+
+def verify_accept(token: torch.Tensor, parent: torch.Tensor, n_nodes: torch.Tensor, target: torch.Tensor,
+                  out: dict | None = None, stream=None) -> dict:
+    """``ubt_verify_accept``: the accepted path and the bonus token of each tree."""
+    _need_gpu(token, parent, n_nodes, target)
+    B, N = token.shape
+    if out is None:
+        i32 = dict(dtype=torch.int32, device=token.device)
+        out = dict(accept_len=torch.empty(B, **i32), accept_nodes=torch.empty(B, N, **i32),
+                   bonus=torch.empty(B, **i32))
+    st = lib().ubt_verify_accept(_ptr(token), _ptr(parent), _ptr(n_nodes), _ptr(target), B, N,
+                                 _ptr(out["accept_len"]), _ptr(out["accept_nodes"]), _ptr(out["bonus"]),
+                                 _stream(stream))
+    _check("ubt_verify_accept", st)
+    return out
+
+
+def commit_kv(k_tree: torch.Tensor, v_tree: torch.Tensor, accept_nodes: torch.Tensor, accept_len: torch.Tensor,
+              prefix_len: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor, stream=None) -> None:
+    """``ubt_commit_kv``: appends the accepted path's key/value rows to the caches and
+    advances ``prefix_len`` (in place)."""
+    _need_gpu(k_tree, v_tree, accept_nodes, accept_len, prefix_len, k_cache, v_cache)
+    B, N, Hkv, D = k_tree.shape
+    st = lib().ubt_commit_kv(_ptr(k_tree), _ptr(v_tree), _ptr(accept_nodes), _ptr(accept_len), _ptr(prefix_len),
+                             _ptr(k_cache), _ptr(v_cache), B, N, Hkv, D, k_cache.shape[1], _stream(stream))
+    _check("ubt_commit_kv", st)
 
 
 class DraftStep:

@@ -238,4 +238,65 @@ ubt_status_t ubt_tree_mask(const int32_t* parent, const int32_t* n_nodes, int B,
   return hip_status(ubt::launch_tree_mask(parent, n_nodes, B, N, mask, stream));
 }
 
+ubt_status_t ubt_tree_attention(const void* q, const void* k_cache, const void* v_cache, const int32_t* prefix_len,
+                                int64_t P_max, const void* k_tree, const void* v_tree, const uint32_t* mask,
+                                const int32_t* n_nodes, int B, int N, int H, int H_kv, int D, float scale, void* out,
+                                ubt_dtype_t out_dt, float* lse, hipStream_t stream) {
+  if (!q || !prefix_len || !k_tree || !v_tree || !mask || !n_nodes || !out) return UBT_ERR_NULL;
+  if (P_max > 0 && (!k_cache || !v_cache)) return UBT_ERR_NULL;
+  if (B < 1 || N < 1 || N > UBT_MAX_BUDGET + 1 || H < 1 || H_kv < 1 || H % H_kv != 0 || P_max < 0 ||
+      P_max >= (int64_t(1) << 31))
+    return UBT_ERR_SHAPE;
+  if (D != 64 && D != 128) return UBT_ERR_UNSUPPORTED;
+  if (!valid_dtype(out_dt)) return UBT_ERR_VALUE;
+  if (!(isfinite(scale) && scale > 0.f)) return UBT_ERR_VALUE;
+  const int64_t rows = static_cast<int64_t>(N) * (H / H_kv);
+  if (static_cast<int64_t>(B) * H_kv * ((rows + 63) / 64) >= (int64_t(1) << 31)) return UBT_ERR_SHAPE;
+  if (!aligned16(q) || !aligned16(k_tree) || !aligned16(v_tree) || !aligned16(out) ||
+      (P_max > 0 && (!aligned16(k_cache) || !aligned16(v_cache))))
+    return UBT_ERR_UNSUPPORTED;
+  ubt::TreeAttnArgs a{};
+  a.q = q;
+  a.k_cache = k_cache;
+  a.v_cache = v_cache;
+  a.prefix_len = prefix_len;
+  a.k_tree = k_tree;
+  a.v_tree = v_tree;
+  a.mask = mask;
+  a.n_nodes = n_nodes;
+  a.B = B;
+  a.N = N;
+  a.H = H;
+  a.Hkv = H_kv;
+  a.D = D;
+  a.Pmax = P_max;
+  a.scale = scale;
+  a.out = out;
+  a.out_f32 = out_dt == UBT_F32 ? 1 : 0;
+  a.lse = lse;
+  return hip_status(ubt::launch_tree_attention(a, stream));
+}
+
+ubt_status_t ubt_verify_accept(const int32_t* token, const int32_t* parent, const int32_t* n_nodes,
+                               const int32_t* target, int B, int N, int32_t* accept_len, int32_t* accept_nodes,
+                               int32_t* bonus, hipStream_t stream) {
+  if (!token || !parent || !n_nodes || !target || !accept_len || !accept_nodes || !bonus) return UBT_ERR_NULL;
+  if (B < 1 || N < 1 || N > UBT_MAX_BUDGET + 1) return UBT_ERR_SHAPE;
+  return hip_status(
+      ubt::launch_verify_accept(token, parent, n_nodes, target, B, N, accept_len, accept_nodes, bonus, stream));
+}
+
+ubt_status_t ubt_commit_kv(const void* k_tree, const void* v_tree, const int32_t* accept_nodes,
+                           const int32_t* accept_len, int32_t* prefix_len, void* k_cache, void* v_cache, int B, int N,
+                           int H_kv, int D, int64_t P_max, hipStream_t stream) {
+  if (!k_tree || !v_tree || !accept_nodes || !accept_len || !prefix_len || !k_cache || !v_cache) return UBT_ERR_NULL;
+  if (B < 1 || N < 1 || N > UBT_MAX_BUDGET + 1 || H_kv < 1 || P_max < 1 || P_max >= (int64_t(1) << 31))
+    return UBT_ERR_SHAPE;
+  if (D != 64 && D != 128) return UBT_ERR_UNSUPPORTED;
+  if (!aligned16(k_tree) || !aligned16(v_tree) || !aligned16(k_cache) || !aligned16(v_cache))
+    return UBT_ERR_UNSUPPORTED;
+  return hip_status(ubt::launch_commit_kv(k_tree, v_tree, accept_nodes, accept_len, prefix_len, k_cache, v_cache, B,
+                                          N, H_kv, D, P_max, stream));
+}
+
 }  // extern "C"

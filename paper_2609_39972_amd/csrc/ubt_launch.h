@@ -76,4 +76,29 @@ hipError_t launch_draft_step(const void* logits, int dtype, int B, int gamma, in
                              float* lse, const SelectorArgs& s, const TreeArgs& a, void* workspace,
                              hipStream_t stream);
 
+// ---- verification: tree attention, acceptance walk, KV commit -------------------------
+struct TreeAttnArgs {
+  const void* q;        // bf16 [B, N, H, D]
+  const void* k_cache;  // bf16 [B, Pmax, Hkv, D]
+  const void* v_cache;
+  const int32_t* prefix_len;  // [B]
+  const void* k_tree;   // bf16 [B, N, Hkv, D]
+  const void* v_tree;
+  const uint32_t* mask;  // [B, N, ceil(N / 32)]
+  const int32_t* n_nodes;
+  int B, N, H, Hkv, D;
+  int64_t Pmax;
+  float scale;
+  void* out;  // [B, N, H, D], bf16 or f32
+  int out_f32;
+  float* lse;  // optional [B, N, H]
+};
+hipError_t launch_tree_attention(const TreeAttnArgs& a, hipStream_t stream);
+hipError_t launch_verify_accept(const int32_t* token, const int32_t* parent, const int32_t* n_nodes,
+                                const int32_t* target, int B, int N, int32_t* accept_len, int32_t* accept_nodes,
+                                int32_t* bonus, hipStream_t stream);
+hipError_t launch_commit_kv(const void* k_tree, const void* v_tree, const int32_t* accept_nodes,
+                            const int32_t* accept_len, int32_t* prefix_len, void* k_cache, void* v_cache, int B, int N,
+                            int Hkv, int D, int64_t Pmax, hipStream_t stream);
+
 }  // namespace ubt

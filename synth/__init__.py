@@ -219,3 +219,40 @@ def dyadic_logq(B: int, gamma: int, K: int, seed: int = 0, step: float = 2.0 ** 
 def candidate_ids(B: int, gamma: int, K: int, V: int, seed: int = 0) -> np.ndarray:
     """Arbitrary candidate token ids ``int32[B, gamma, K]`` (tree tests that start from logq)."""
     return _rng(901, seed, B, gamma, K).integers(0, V, size=(B, gamma, K)).astype(np.int32)
+
+
+# ---- verification inputs ----------------------------------------------------------------
+F_VQ, F_VKC, F_VVC, F_VKT, F_VVT, F_VTARGET = range(20, 26)
+
+
+def verify_inputs(seed: int, B: int, N: int, H: int, Hkv: int, D: int, Pmax: int) -> dict:
+    """Synthetic operands of tree verification as bf16 bit patterns (uint16): queries of
+    the tree nodes ``q [B, N, H, D]``, cached keys/values ``[B, Pmax, Hkv, D]`` and the
+    tree nodes' keys/values ``[B, N, Hkv, D]``, all i.i.d. N(0, 1) (so that q.k / sqrt(D)
+    is of unit scale, as after the target's normalisation layers)."""
+    def draw(field, shape):
+        return round_bf16_bits(_rng(seed, field).normal(0.0, 1.0, size=shape))
+
+    return dict(q=draw(F_VQ, (B, N, H, D)), k_cache=draw(F_VKC, (B, Pmax, Hkv, D)),
+                v_cache=draw(F_VVC, (B, Pmax, Hkv, D)), k_tree=draw(F_VKT, (B, N, Hkv, D)),
+                v_tree=draw(F_VVT, (B, N, Hkv, D)))
+
+
+def verify_targets(seed: int, token: np.ndarray, parent: np.ndarray, n_nodes: np.ndarray, V: int,
+                   follow: float = 0.7) -> np.ndarray:
+    """Target samples ``[B, N]`` for the acceptance walk: from the root, with probability
+    ``follow`` per step the sample equals the token of a uniformly drawn child (so the walk
+    goes on), otherwise a uniform token; nodes off that walk get uniform tokens."""
+    rng = _rng(seed, F_VTARGET)
+    B, N = token.shape
+    tgt = rng.integers(0, V, size=(B, N)).astype(np.int32)
+    for b in range(B):
+        cur = 0
+        while True:
+            kids = [c for c in range(cur + 1, int(n_nodes[b])) if parent[b, c] == cur]
+            if not kids or rng.random() >= follow:
+                break
+            c = kids[int(rng.integers(0, len(kids)))]
+            tgt[b, cur] = token[b, c]
+            cur = c
+    return tgt

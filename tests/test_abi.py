@@ -146,3 +146,50 @@ def test_binding_refuses_host_tensors():
 
     with pytest.raises(ValueError):
         ubt.topk(torch.zeros(1, 1, 16, dtype=torch.bfloat16), 4)
+
+
+def _attn(**kw):
+    a = dict(q=FAKE, kc=FAKE, vc=FAKE, plen=FAKE, Pmax=128, kt=FAKE, vt=FAKE, mask=FAKE, nn=FAKE, B=2, N=65, H=32,
+             Hkv=8, D=128, scale=0.088, out=FAKE, odt=1, lse=None)
+    a.update(kw)
+    return ubt.lib().ubt_tree_attention(a["q"], a["kc"], a["vc"], a["plen"], a["Pmax"], a["kt"], a["vt"], a["mask"],
+                                        a["nn"], a["B"], a["N"], a["H"], a["Hkv"], a["D"], a["scale"], a["out"],
+                                        a["odt"], a["lse"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(q=None), 1), (dict(kt=None), 1), (dict(vt=None), 1), (dict(mask=None), 1), (dict(nn=None), 1),
+    (dict(out=None), 1), (dict(plen=None), 1), (dict(kc=None), 1), (dict(vc=None), 1),
+    (dict(B=0), 2), (dict(N=0), 2), (dict(N=257), 2), (dict(H=0), 2), (dict(Hkv=0), 2), (dict(H=30), 2),
+    (dict(Pmax=-1), 2), (dict(Pmax=2 ** 31), 2),
+    (dict(D=96), 4), (dict(D=256), 4), (dict(q=ctypes.c_void_p(0x10008)), 4), (dict(kc=ctypes.c_void_p(0x10004)), 4),
+    (dict(odt=7), 3), (dict(scale=0.0), 3), (dict(scale=float("inf")), 3), (dict(scale=-1.0), 3),
+])
+def test_tree_attention_validation(kw, code):
+    assert _attn(**kw) == code
+
+
+def test_tree_attention_without_context_needs_no_cache():
+    """P_max = 0 takes NULL caches; the call then fails only on what is still wrong."""
+    assert _attn(Pmax=0, kc=None, vc=None, N=0) == 2
+
+
+@pytest.mark.parametrize("args,code", [
+    ((None, FAKE, FAKE, FAKE, 2, 65, FAKE, FAKE, FAKE), 1), ((FAKE, FAKE, FAKE, None, 2, 65, FAKE, FAKE, FAKE), 1),
+    ((FAKE, FAKE, FAKE, FAKE, 2, 65, FAKE, FAKE, None), 1),
+    ((FAKE, FAKE, FAKE, FAKE, 0, 65, FAKE, FAKE, FAKE), 2), ((FAKE, FAKE, FAKE, FAKE, 2, 257, FAKE, FAKE, FAKE), 2),
+])
+def test_verify_accept_validation(args, code):
+    assert ubt.lib().ubt_verify_accept(*args, None) == code
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(kt=None), 1), (dict(kc=None), 1), (dict(plen=None), 1), (dict(nodes=None), 1),
+    (dict(B=0), 2), (dict(N=300), 2), (dict(Hkv=0), 2), (dict(Pmax=0), 2), (dict(D=32), 4),
+    (dict(kc=ctypes.c_void_p(0x10002)), 4),
+])
+def test_commit_kv_validation(kw, code):
+    a = dict(kt=FAKE, vt=FAKE, nodes=FAKE, alen=FAKE, plen=FAKE, kc=FAKE, vc=FAKE, B=2, N=65, Hkv=8, D=128, Pmax=64)
+    a.update(kw)
+    assert ubt.lib().ubt_commit_kv(a["kt"], a["vt"], a["nodes"], a["alen"], a["plen"], a["kc"], a["vc"], a["B"],
+                                   a["N"], a["Hkv"], a["D"], a["Pmax"], None) == code
