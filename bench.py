@@ -77,6 +77,133 @@ def cpu_baseline(w, d, min_seconds: float) -> dict:
                       f"pool buffer 0, fp64 C++ oracle, {threads} threads, {el:.1f} s"}
 
 
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+VERIFY_SHAPE = dict(B=32, N=65, H=32, Hkv=8, D=128, P=4096)  # budget 64; Qwen3-8B attention heads
+
+
+def bench_verify(args, dev) -> int:
+    """Tree verification on one batch of draft trees: ubt_tree_attention over a 4096-token
+    context (the dominant kernel), ubt_verify_accept and ubt_commit_kv.  The trees and
+    masks come from the headline draft step; queries, keys and values are synthetic."""
+    import numpy as np
+    import torch
+
+    import paper_2609_39972_amd as ubt
+    import synth
+
+    S = VERIFY_SHAPE
+    B, N, H, Hkv, D, P = S["B"], S["N"], S["H"], S["Hkv"], S["D"], S["P"]
+    w = synth.WORKLOADS[3]
+    assert w.B == B and w.N == N
+    di = synth.inputs(w, 0)
+    bits = lambda a: ubt.bf16_tensor_from_bits(a, dev)
+    step = ubt.DraftStep(w.B, w.gamma, w.V, w.K, w.W, w.budget, bits(di["phi"]), bits(di["psi"]), bits(di["gate"]),
+                         torch.from_numpy(di["anchor"]).to(dev), di["alpha"], di["lam"], w.zeta)
+    tree = step.run(bits(di["logits"]))
+    torch.cuda.synchronize()
+    d = synth.verify_inputs(1, B, N, H, Hkv, D, P + N)  # cache room for the committed path
+    q, kc, vc, kt, vt = (bits(d[k]) for k in ("q", "k_cache", "v_cache", "k_tree", "v_tree"))
+    plen0 = torch.full((B,), P, dtype=torch.int32, device=dev)
+    out = torch.empty(B, N, H, D, dtype=torch.bfloat16, device=dev)
+    lse = torch.empty(B, N, H, dtype=torch.float32, device=dev)
+    tok, par, nn, mask = tree["token"], tree["parent"], tree["n_nodes"], tree["mask"]
+    target = torch.from_numpy(synth.verify_targets(5, tok.cpu().numpy(), par.cpu().numpy(), nn.cpu().numpy(), w.V,
+                                                   0.8)).to(dev)
+    acc = ubt.verify_accept(tok, par, nn, target)
+    plen = plen0.clone()
+    stream = torch.cuda.Stream(device=dev)
+
+    def timed(fn, n=50, replays=4):
+        with torch.cuda.stream(stream):
+            fn()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=stream):
+            for _ in range(n):
+                fn()
+        torch.cuda.synchronize()
+        with torch.cuda.stream(stream):
+            g.replay()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        with torch.cuda.stream(stream):
+            a.record(stream)
+            for _ in range(replays):
+                g.replay()
+            b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) * 1e3 / (n * replays)
+
+    n_att = max(8, args.steps // 20)
+    att_us = timed(lambda: ubt.tree_attention(q, kc, vc, plen0, kt, vt, mask, nn, out=out, lse=lse, stream=stream),
+                   n=n_att)
+    acc_us = timed(lambda: ubt.verify_accept(tok, par, nn, target, out=acc, stream=stream))
+
+    def commit():
+        plen.copy_(plen0)
+        ubt.commit_kv(kt, vt, acc["accept_nodes"], acc["accept_len"], plen, kc, vc, stream=stream)
+    commit_us = timed(commit)
+
+    # Algorithmic work of one attention launch: each (node, head) reads the context and
+    # its ancestors once: 2 * D multiply-adds per key for q.k and as many for p.v.
+    m = mask.cpu().numpy().view(np.uint32)
+    vis = np.unpackbits(m.view(np.uint8), axis=-1, bitorder="little")[..., :N].sum(axis=-1)  # [B, N]
+    nn_h = nn.cpu().numpy()
+    keys = sum(int(P * nn_h[b] + vis[b, :nn_h[b]].sum()) for b in range(B))
+    flops = 4.0 * D * H * keys
+    kv_bytes = B * (P + N) * Hkv * D * 2 * 2
+    io_bytes = B * N * H * D * 2 * 2 + B * N * H * 4 + m.nbytes
+    att_bytes = kv_bytes + io_bytes
+    tflops = flops / (att_us * 1e-6) / 1e12
+    gbps = att_bytes / (att_us * 1e-6) / 1e9
+    t_hbm = att_bytes / (HBM_PEAK_GBPS * 1e9)
+    t_mfma = flops / (MFMA_BF16_PEAK_TFLOPS * 1e12)
+    bound = "hbm" if t_hbm >= t_mfma else "mfma"
+    log(f"tree attention {att_us:.2f} us: {gbps:.0f} GB/s, {tflops:.1f} TFLOP/s (HBM floor {t_hbm * 1e6:.1f} us, "
+        f"MFMA floor {t_mfma * 1e6:.1f} us); accept {acc_us:.2f} us; commit {commit_us:.2f} us")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle.verify as ov
+
+        host = {k: d[k] for k in d}
+        t0, reps = time.perf_counter(), 0
+        seqs = [0]
+        while True:
+            ov.tree_attention_fast(host["q"], host["k_cache"], host["v_cache"], np.full(B, P, np.int32),
+                                   host["k_tree"], host["v_tree"], m, nn_h, D ** -0.5, seqs=seqs)
+            reps += 1
+            if time.perf_counter() - t0 >= min(args.cpu_seconds, 10.0):
+                break
+        el = time.perf_counter() - t0
+        per_seq = el / reps
+        cpu = {"value": round(1.0 / (per_seq * B), 3), "unit": "verifications/s", "cores": os.cpu_count(),
+               "kind": "oracle",
+               "sample": f"{reps} x sequence 0 of {B} (all heads, 4096-token context), fp64 numpy oracle, "
+                         f"{el:.1f} s; value = 1 / (time per sequence * B)"}
+
+    res = {
+        "metric": "tree verification attention us/call at B=32, budget 64, Qwen3-8B heads, 4096-token context",
+        "value": round(1e6 / att_us, 1), "unit": "verifications/s", "n_gpus": 1, "steps": n_att * 4,
+        "warmup": 1, "ms_per_step": round(att_us / 1e3, 6), "us_per_step": round(att_us, 3),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "verify-qwen3-8b-heads-b32-n65-p4096", **S},
+        "kernels_us": {"tree_attention": round(att_us, 3), "verify_accept": round(acc_us, 3),
+                       "commit_kv": round(commit_us, 3)},
+        "roofline": {"bound": bound, "kernel": "tree_attention_kernel",
+                     "achieved": round(gbps, 1) if bound == "hbm" else round(tflops, 1),
+                     "peak": HBM_PEAK_GBPS if bound == "hbm" else MFMA_BF16_PEAK_TFLOPS,
+                     "unit": "GB/s" if bound == "hbm" else "TFLOP/s",
+                     "frac": round(gbps / HBM_PEAK_GBPS if bound == "hbm" else tflops / MFMA_BF16_PEAK_TFLOPS, 4),
+                     "traffic": None, "algorithmic_bytes_per_launch": att_bytes, "algorithmic_flops": flops,
+                     "other": {"TFLOP/s": round(tflops, 1), "mfma_frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4),
+                               "GB/s": round(gbps, 1), "hbm_frac": round(gbps / HBM_PEAK_GBPS, 4)}},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(res), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -85,9 +212,9 @@ def main() -> int:
     ap.add_argument("--workload", type=int, default=3, help="synthetic workload id (3 = B=32, V=151936 headline)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="minimum oracle time for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--mode", choices=("step", "tree", "separate"), default="tree",
+    ap.add_argument("--mode", choices=("step", "tree", "separate", "verify"), default="tree",
                     help="step: one ubt_draft_step call; tree: ubt_topk + ubt_draft_tree; separate: ubt_topk + "
-                         "ubt_bigram_scores + ubt_build_tree")
+                         "ubt_bigram_scores + ubt_build_tree; verify: tree verification (its own JSON line)")
     ap.add_argument("--sweep-launches", type=int, default=200, help="launches per kernel in the per-kernel timing")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run a plain device copy of known size (counter calibration) and exit")
@@ -116,6 +243,8 @@ def main() -> int:
         torch.cuda.synchronize()
         print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "launches": 5}))
         return 0
+    if args.mode == "verify":
+        return bench_verify(args, dev)
 
     w = synth.WORKLOADS[args.workload]
     pool = max(1, -(-POOL_BYTES // w.logit_bytes))

@@ -7,18 +7,23 @@
 // sample is the bonus token; the key/value rows along the accepted path are carried
 // into the cache and the other branches are dropped.  Background, "Tree Drafting".
 //
-// Tree attention: one workgroup of 4 waves per (sequence, key/value head, 64 query
-// rows).  The query rows of a key/value head are (node, head-in-group) pairs, node-major,
-// so grouped heads share every key/value block.  Keys stream in blocks of 32 through
-// LDS, double-buffered, the next block's global loads in flight while the current one is
-// used.  K is stored as it is; V is stored transposed (d-major), so both products read
-// MFMA operands with plain LDS loads:
-//   S^T = K Q^T     (v_mfma_f32_16x16x32_bf16, A = a K tile, B = the wave's 16 queries)
+// Tree attention: one workgroup of 8 waves per (sequence, key/value head, group of up to
+// 384 query rows).  The query rows of a key/value head are (node, head-in-group) pairs,
+// node-major, so grouped heads share every key/value block, and the whole tree of a head
+// fits one group at the usual shapes (65 nodes x 4 heads = 260 rows): keys and values
+// are then read from HBM once.  Each wave holds up to 3 tiles of 16 query rows, so every
+// operand fragment read from LDS feeds up to 3 MFMAs.  Keys stream in blocks of 32
+// through LDS, double-buffered, the next block's global loads in flight while the
+// current one is used.  K is stored as it is; V is stored transposed (d-major), so both
+// products read MFMA operands with plain LDS loads:
+//   S^T = K Q^T     (v_mfma_f32_16x16x32_bf16, A = a K tile, B = 16 queries)
 //   O^T += V^T P^T  (A = a V^T tile, B = P^T straight from the S^T accumulators)
-// S^T puts the scores of one query in one lane column, 8 keys per lane, so the online
-// softmax reduces over two cross-lane steps and P^T needs no shuffle: the k order of the
-// second product is permuted to match (slot t of lane group g is key 4g + t for t < 4
-// and 16 + 4g + t - 4 after), and the V^T operand is read in the same order.
+// S^T puts the scores of one query in one lane column, 8 keys per lane, so P^T needs no
+// shuffle: the k order of the second product is permuted to match (slot t of lane group
+// g is key 4g + t for t < 4 and 16 + 4g + t - 4 after), and V^T is read in that order.
+// The running maximum is raised only when a score exceeds it by more than 2^8 (weights
+// then stay below 256, exact enough in fp32 and bf16), so the rescaling of the output
+// accumulators is off the steady-state path.
 #include "ubt_device.h"
 #include "ubt_launch.h"
 
@@ -30,11 +35,14 @@ typedef uint32_t v2u __attribute__((ext_vector_type(2)));
 typedef float v4f __attribute__((ext_vector_type(4)));
 typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
 
-constexpr int kAttnWaves = 4;
-constexpr int kAttnRows = 16 * kAttnWaves;  // query rows per workgroup
-constexpr int kKB = 32;                      // keys per block
+constexpr int kAttnWaves = 8;
+constexpr int kAttnThreads = kAttnWaves * kWave;
+constexpr int kTilesPerWave = 3;
+constexpr int kAttnRows = 16 * kAttnWaves * kTilesPerWave;  // query rows per workgroup (384)
+constexpr int kKB = 32;                                      // keys per block
 constexpr int kVtStride = 36;  // bf16 per V^T row: 32 keys + 4, so the transposing writes
                                // of one wave hit each bank at most twice
+constexpr float kRescaleGap = 8.f;  // log2 units a score may exceed the running maximum
 
 template <int D>
 struct AttnLds {
@@ -42,14 +50,15 @@ struct AttnLds {
   uint16_t vt[2][D][kVtStride];
 };
 
+typedef __bf16 v2bf __attribute__((ext_vector_type(2)));
+typedef float v2f __attribute__((ext_vector_type(2)));
+
 __device__ __forceinline__ v8bf as_v8bf(v4u v) { return __builtin_bit_cast(v8bf, v); }
 
-// Round-to-nearest-even to bf16 of a finite non-negative float (the probabilities).
-__device__ __forceinline__ uint32_t bf16_rne(float f) {
-  const uint32_t u = __float_as_uint(f);
-  return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+// Two floats to bf16, round to nearest even (one v_cvt_pk_bf16_f32).
+__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((v2f{lo, hi}), v2bf));
 }
-__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) { return bf16_rne(lo) | (bf16_rne(hi) << 16); }
 
 struct AttnArgs {
   const uint16_t* q;
@@ -60,7 +69,7 @@ struct AttnArgs {
   const uint16_t* vt;
   const uint32_t* mask;
   const int32_t* n_nodes;
-  int B, N, H, Hkv, g, R, tiles;  // R = N * g query rows per key/value head; tiles = ceil(R / 64)
+  int B, N, H, Hkv, g, R, groups;  // R = N * g query rows per key/value head, in groups of 384
   int64_t Pmax;
   float scale_log2;  // scale * log2(e)
   void* out;
@@ -74,7 +83,7 @@ struct AttnArgs {
 template <int D>
 struct Stage {
   static constexpr int kChunks = D / 8;                                  // chunks per key row
-  static constexpr int kKPerThread = (kKB * kChunks + 255) / 256;        // 2 (D = 128) or 1 (D = 64)
+  static constexpr int kKPerThread = (kKB * kChunks + kAttnThreads - 1) / kAttnThreads;  // 1
   v4u k[kKPerThread];
   v4u v0, v1;
 };
@@ -92,7 +101,7 @@ __device__ __forceinline__ void stage_load(const AttnArgs& p, Stage<D>& s, int b
   const v4u zero = v4u{0u, 0u, 0u, 0u};
 #pragma unroll
   for (int i = 0; i < Stage<D>::kKPerThread; ++i) {
-    const int id = t + 256 * i;
+    const int id = t + kAttnThreads * i;
     const int row = id / C, c = id % C;
     const int key = base + row;
     s.k[i] = (row < kKB && key < lim)
@@ -101,7 +110,7 @@ __device__ __forceinline__ void stage_load(const AttnArgs& p, Stage<D>& s, int b
   }
   const int kp = t % 16, c = t / 16;
   const int k0 = base + 2 * kp;
-  const bool in = c < C;
+  const bool in = c < C;  // 16 key pairs x C chunks: the first 16 C threads
   s.v0 = (in && k0 < lim) ? *reinterpret_cast<const v4u*>(vs + ((static_cast<int64_t>(b) * S + k0) * p.Hkv + h) * D + 8 * c)
                           : zero;
   s.v1 = (in && k0 + 1 < lim)
@@ -114,7 +123,7 @@ __device__ __forceinline__ void stage_store(AttnLds<D>& lds, int st, const Stage
   constexpr int C = Stage<D>::kChunks;
 #pragma unroll
   for (int i = 0; i < Stage<D>::kKPerThread; ++i) {
-    const int id = t + 256 * i;
+    const int id = t + kAttnThreads * i;
     const int row = id / C, c = id % C;
     if (row < kKB) *reinterpret_cast<v4u*>(&lds.k[st][row][8 * c]) = s.k[i];
   }
@@ -130,25 +139,27 @@ __device__ __forceinline__ void stage_store(AttnLds<D>& lds, int st, const Stage
 }
 
 template <int D>
-__global__ __launch_bounds__(256) void tree_attention_kernel(AttnArgs p) {
+__global__ __launch_bounds__(kAttnThreads) void tree_attention_kernel(AttnArgs p) {
   constexpr int DS = D / 32;  // k steps of S^T
   constexpr int DT = D / 16;  // output tiles of O^T
+  constexpr int TW = kTilesPerWave;
   __shared__ AttnLds<D> lds;
 
-  // Workgroup -> (sequence, key/value head, row tile).  Consecutive workgroups go to
-  // different XCDs; the remap puts the row tiles of one (sequence, head) on one XCD, so
-  // their key/value blocks are shared through that XCD's L2.
-  const int total = p.B * p.Hkv * p.tiles;
+  // Workgroup -> (sequence, key/value head, row group).  Consecutive workgroups go to
+  // different XCDs; the remap puts the row groups of one (sequence, head) on one XCD, so
+  // they share its key/value blocks through that XCD's L2.
+  const int total = p.B * p.Hkv * p.groups;
   const int L = static_cast<int>(blockIdx.x);
   const int T8 = total - total % 8;
   const int id = L < T8 ? (L % 8) * (T8 / 8) + L / 8 : L;
-  const int tile = id % p.tiles;
-  const int bh = id / p.tiles;
+  const int grp = id % p.groups;
+  const int bh = id / p.groups;
   const int h = bh % p.Hkv;
   const int b = bh / p.Hkv;
 
   const int t = static_cast<int>(threadIdx.x);
-  const int w = t / kWave, lane = t % kWave;
+  const int w = __builtin_amdgcn_readfirstlane(t / kWave);
+  const int lane = t % kWave;
   const int lr = lane & 15, kg = lane >> 4;
 
   const int P = min(max(p.prefix_len[b], 0), static_cast<int>(p.Pmax));
@@ -157,25 +168,40 @@ __global__ __launch_bounds__(256) void tree_attention_kernel(AttnArgs p) {
   const int nblk = npb + (nn + kKB - 1) / kKB;
   const int words = (p.N + 31) / 32;
 
-  // This lane's query row (B operand column and softmax column).
-  const int r = tile * kAttnRows + w * 16 + lr;
-  const bool rin = r < p.R;
-  const int n = rin ? r / p.g : 0;
-  const int head = h * p.g + (rin ? r % p.g : 0);
-  const bool live = rin && n < nn;
-  v4u qf[DS];
-  {
-    const uint16_t* qr = p.q + ((static_cast<int64_t>(b) * p.N + n) * p.H + head) * D;
+  // Tile j of this wave holds query rows r0 + 16 (w + 8 j) + [0, 16); this lane is the
+  // column lr of each.
+  const int r0 = grp * kAttnRows;
+  int ntile = 0;  // tiles of this wave with at least one row (wave-uniform)
+#pragma unroll
+  for (int j = 0; j < TW; ++j) ntile += (r0 + 16 * (w + kAttnWaves * j) < p.R) ? 1 : 0;
+  int n_of[TW], head_of[TW];
+  bool rin[TW], live[TW];
+  v4u qf[TW][DS];
+  const uint32_t* mrow[TW];
+#pragma unroll
+  for (int j = 0; j < TW; ++j) {
+    const int r = r0 + 16 * (w + kAttnWaves * j) + lr;
+    rin[j] = r < p.R;
+    n_of[j] = rin[j] ? r / p.g : 0;
+    head_of[j] = h * p.g + (rin[j] ? r % p.g : 0);
+    live[j] = rin[j] && n_of[j] < nn;
+    const uint16_t* qr = p.q + ((static_cast<int64_t>(b) * p.N + n_of[j]) * p.H + head_of[j]) * D;
 #pragma unroll
     for (int s = 0; s < DS; ++s)
-      qf[s] = live ? *reinterpret_cast<const v4u*>(qr + 32 * s + 8 * kg) : v4u{0u, 0u, 0u, 0u};
+      qf[j][s] = live[j] ? *reinterpret_cast<const v4u*>(qr + 32 * s + 8 * kg) : v4u{0u, 0u, 0u, 0u};
+    mrow[j] = p.mask + (static_cast<int64_t>(b) * p.N + n_of[j]) * words;
   }
-  const uint32_t* mrow = p.mask + (static_cast<int64_t>(b) * p.N + n) * words;
 
-  v4f o[DT];
+  v4f o[TW][DT];
+  float m_run[TW], l_part[TW];
 #pragma unroll
-  for (int i = 0; i < DT; ++i) o[i] = v4f{0.f, 0.f, 0.f, 0.f};
-  float m_run = neg_inf(), l_part = 0.f;
+  for (int j = 0; j < TW; ++j) {
+#pragma unroll
+    for (int i = 0; i < DT; ++i) o[j][i] = v4f{0.f, 0.f, 0.f, 0.f};
+    m_run[j] = neg_inf();
+    l_part[j] = 0.f;
+  }
+  const float c = p.scale_log2;
 
   Stage<D> sg;
   if (nblk > 0) {
@@ -187,58 +213,93 @@ __global__ __launch_bounds__(256) void tree_attention_kernel(AttnArgs p) {
     const int st = blk & 1;
     if (blk + 1 < nblk) stage_load<D>(p, sg, b, h, blk + 1, npb, P, nn, t);
 
-    // ---- S^T = K Q^T for 32 keys ----
-    v4f s0 = v4f{0.f, 0.f, 0.f, 0.f}, s1 = v4f{0.f, 0.f, 0.f, 0.f};
+    // ---- S^T = K Q^T for 32 keys and each tile ----
+    v4f s0[TW], s1[TW];
+#pragma unroll
+    for (int j = 0; j < TW; ++j) s0[j] = s1[j] = v4f{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int s = 0; s < DS; ++s) {
       const v4u a0 = *reinterpret_cast<const v4u*>(&lds.k[st][lr][32 * s + 8 * kg]);
       const v4u a1 = *reinterpret_cast<const v4u*>(&lds.k[st][16 + lr][32 * s + 8 * kg]);
-      s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_v8bf(a0), as_v8bf(qf[s]), s0, 0, 0, 0);
-      s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_v8bf(a1), as_v8bf(qf[s]), s1, 0, 0, 0);
+#pragma unroll
+      for (int j = 0; j < TW; ++j) {
+        if (j < ntile) {
+          s0[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_v8bf(a0), as_v8bf(qf[j][s]), s0[j], 0, 0, 0);
+          s1[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_v8bf(a1), as_v8bf(qf[j][s]), s1[j], 0, 0, 0);
+        }
+      }
     }
 
-    // ---- which of the lane's 8 keys this query sees ----
-    // bit t of vis: key 4 kg + t (t < 4) or 16 + 4 kg + t - 4 (t >= 4) of this block.
-    uint32_t vis;
-    if (blk < npb) {
-      const int left = P - blk * kKB;  // keys of the block inside the prefix
-      uint32_t all = left >= 32 ? ~0u : ((1u << left) - 1u);
-      vis = ((all >> (4 * kg)) & 0xFu) | (((all >> (16 + 4 * kg)) & 0xFu) << 4);
+    // ---- softmax weights: which of the lane's 8 keys each query sees ----
+    // Bit t of vis: key 4 kg + t (t < 4) or 16 + 4 kg + t - 4 (t >= 4) of this block.
+    const bool full = blk < npb && (blk + 1) * kKB <= P;  // a context block wholly inside the prefix
+    uint32_t vis[TW];
+    if (full) {
+#pragma unroll
+      for (int j = 0; j < TW; ++j) vis[j] = live[j] ? 0xFFu : 0u;
+    } else if (blk < npb) {
+      const int left = P - blk * kKB;  // 1..31 keys of the block inside the prefix
+      const uint32_t all = (1u << left) - 1u;
+      const uint32_t v = ((all >> (4 * kg)) & 0xFu) | (((all >> (16 + 4 * kg)) & 0xFu) << 4);
+#pragma unroll
+      for (int j = 0; j < TW; ++j) vis[j] = live[j] ? v : 0u;
     } else {
       const int tb = blk - npb;
       const int left = nn - tb * kKB;
       const uint32_t in = left >= 32 ? ~0u : ((1u << left) - 1u);
-      const uint32_t bits = live ? (mrow[tb] & in) : 0u;
-      vis = ((bits >> (4 * kg)) & 0xFu) | (((bits >> (16 + 4 * kg)) & 0xFu) << 4);
+#pragma unroll
+      for (int j = 0; j < TW; ++j) {
+        const uint32_t bits = live[j] ? (mrow[j][tb] & in) : 0u;
+        vis[j] = ((bits >> (4 * kg)) & 0xFu) | (((bits >> (16 + 4 * kg)) & 0xFu) << 4);
+      }
     }
-    if (!live) vis = 0u;
-    float x[8];
+    float sc[TW][8];
+    bool grow = false;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      x[j] = ((vis >> j) & 1u) ? s0[j] * p.scale_log2 : neg_inf();
-      x[4 + j] = ((vis >> (4 + j)) & 1u) ? s1[j] * p.scale_log2 : neg_inf();
+    for (int j = 0; j < TW; ++j) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        sc[j][e] = ((vis[j] >> e) & 1u) ? s0[j][e] : neg_inf();
+        sc[j][4 + e] = ((vis[j] >> (4 + e)) & 1u) ? s1[j][e] : neg_inf();
+      }
+      float mx = sc[j][0];
+#pragma unroll
+      for (int e = 1; e < 8; ++e) mx = fmaxf(mx, sc[j][e]);
+      grow = grow || (mx * c > m_run[j] + kRescaleGap);
     }
-    float mb = x[0];
+    if (ballot(grow)) {
+      // Raise the running maxima that fell behind (uniform over each query's 4 lanes).
 #pragma unroll
-    for (int j = 1; j < 8; ++j) mb = fmaxf(mb, x[j]);
-    mb = fmaxf(mb, __shfl_xor(mb, 16));
-    mb = fmaxf(mb, __shfl_xor(mb, 32));
-    const float m_new = fmaxf(m_run, mb);
-    const bool any = m_new != neg_inf();
-    const float alpha = any ? __builtin_amdgcn_exp2f(m_run - m_new) : 1.f;
-    float pr[8];
-    float psum = 0.f;
+      for (int j = 0; j < TW; ++j) {
+        float mx = sc[j][0];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      pr[j] = ((vis >> j) & 1u) ? __builtin_amdgcn_exp2f(x[j] - m_new) : 0.f;
-      psum += pr[j];
+        for (int e = 1; e < 8; ++e) mx = fmaxf(mx, sc[j][e]);
+        mx *= c;
+        mx = fmaxf(mx, __shfl_xor(mx, 16));
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        if (mx > m_run[j] + kRescaleGap) {
+          const float alpha = __builtin_amdgcn_exp2f(m_run[j] - mx);
+          m_run[j] = mx;
+          l_part[j] *= alpha;
+#pragma unroll
+          for (int i = 0; i < DT; ++i) o[j][i] *= alpha;
+        }
+      }
     }
-    l_part = l_part * alpha + psum;
-    m_run = m_new;
+    v4u pt[TW];
 #pragma unroll
-    for (int i = 0; i < DT; ++i) o[i] *= alpha;
-    const v4u pt = v4u{pack_bf16(pr[0], pr[1]), pack_bf16(pr[2], pr[3]), pack_bf16(pr[4], pr[5]),
-                       pack_bf16(pr[6], pr[7])};
+    for (int j = 0; j < TW; ++j) {
+      float pr[8];
+      // m_run is finite wherever a key is visible (the first visible score raised it).
+      const float nm = -m_run[j];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        pr[e] = ((vis[j] >> e) & 1u) ? __builtin_amdgcn_exp2f(fmaf(sc[j][e], c, nm)) : 0.f;
+        l_part[j] += pr[e];
+      }
+      pt[j] = v4u{pack_bf16(pr[0], pr[1]), pack_bf16(pr[2], pr[3]), pack_bf16(pr[4], pr[5]),
+                  pack_bf16(pr[6], pr[7])};
+    }
 
     // ---- O^T += V^T P^T ----
 #pragma unroll
@@ -247,40 +308,38 @@ __global__ __launch_bounds__(256) void tree_attention_kernel(AttnArgs p) {
       const v2u lo = *reinterpret_cast<const v2u*>(vrow + 4 * kg);
       const v2u hi = *reinterpret_cast<const v2u*>(vrow + 16 + 4 * kg);
       const v4u a = v4u{lo.x, lo.y, hi.x, hi.y};
-      o[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_v8bf(a), as_v8bf(pt), o[i], 0, 0, 0);
+#pragma unroll
+      for (int j = 0; j < TW; ++j)
+        if (j < ntile) o[j][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_v8bf(a), as_v8bf(pt[j]), o[j][i], 0, 0, 0);
     }
 
     if (blk + 1 < nblk) stage_store<D>(lds, st ^ 1, sg, t);
     __syncthreads();
   }
 
-  // ---- normalise and store: lane (lr, kg) holds d = 16 i + 4 kg + j of its query ----
-  float l = l_part + __shfl_xor(l_part, 16);
-  l = l + __shfl_xor(l, 32);
-  if (!rin) return;
-  const bool has = live && l > 0.f;
-  const float inv = has ? 1.f / l : 0.f;
-  const int64_t orow = (static_cast<int64_t>(b) * p.N + n) * p.H + head;
-  if (p.out_f32) {
-    float* op = static_cast<float*>(p.out) + orow * D;
+  // ---- normalise and store: lane (lr, kg) holds d = 16 i + 4 kg + e of its query ----
 #pragma unroll
-    for (int i = 0; i < DT; ++i) *reinterpret_cast<v4f*>(op + 16 * i + 4 * kg) = o[i] * inv;
-  } else {
-    uint16_t* op = static_cast<uint16_t*>(p.out) + orow * D;
+  for (int j = 0; j < TW; ++j) {
+    float l = l_part[j] + __shfl_xor(l_part[j], 16);
+    l = l + __shfl_xor(l, 32);
+    if (!rin[j]) continue;
+    const bool has = live[j] && l > 0.f;
+    const float inv = has ? 1.f / l : 0.f;
+    const int64_t orow = (static_cast<int64_t>(b) * p.N + n_of[j]) * p.H + head_of[j];
+    if (p.out_f32) {
+      float* op = static_cast<float*>(p.out) + orow * D;
 #pragma unroll
-    for (int i = 0; i < DT; ++i) {
-      const v4f v = o[i] * inv;
-      // The output rounds to nearest even like the probabilities, here with sign.
-      uint32_t e[4];
+      for (int i = 0; i < DT; ++i) *reinterpret_cast<v4f*>(op + 16 * i + 4 * kg) = o[j][i] * inv;
+    } else {
+      uint16_t* op = static_cast<uint16_t*>(p.out) + orow * D;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const uint32_t u = __float_as_uint(v[j]);
-        e[j] = (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+      for (int i = 0; i < DT; ++i) {
+        const v4f v = o[j][i] * inv;
+        *reinterpret_cast<v2u*>(op + 16 * i + 4 * kg) = v2u{pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3])};
       }
-      *reinterpret_cast<v2u*>(op + 16 * i + 4 * kg) = v2u{e[0] | (e[1] << 16), e[2] | (e[3] << 16)};
     }
+    if (p.lse && kg == 0) p.lse[orow] = has ? (m_run[j] + __builtin_amdgcn_logf(l)) * kLn2 : neg_inf();
   }
-  if (p.lse && kg == 0) p.lse[orow] = has ? (m_run + __builtin_amdgcn_logf(l)) * kLn2 : neg_inf();
 }
 
 // ---- acceptance walk: one wave per sequence ----------------------------------------------
@@ -373,17 +432,17 @@ hipError_t launch_tree_attention(const TreeAttnArgs& a, hipStream_t stream) {
   p.Hkv = a.Hkv;
   p.g = a.H / a.Hkv;
   p.R = a.N * p.g;
-  p.tiles = (p.R + kAttnRows - 1) / kAttnRows;
+  p.groups = (p.R + kAttnRows - 1) / kAttnRows;
   p.Pmax = a.Pmax;
   p.scale_log2 = a.scale * kLog2e;
   p.out = a.out;
   p.out_f32 = a.out_f32;
   p.lse = a.lse;
-  const dim3 grid(static_cast<unsigned>(p.B * p.Hkv * p.tiles));
+  const dim3 grid(static_cast<unsigned>(p.B * p.Hkv * p.groups));
   if (a.D == 128)
-    hipLaunchKernelGGL(tree_attention_kernel<128>, grid, dim3(256), 0, stream, p);
+    hipLaunchKernelGGL(tree_attention_kernel<128>, grid, dim3(kAttnThreads), 0, stream, p);
   else
-    hipLaunchKernelGGL(tree_attention_kernel<64>, grid, dim3(256), 0, stream, p);
+    hipLaunchKernelGGL(tree_attention_kernel<64>, grid, dim3(kAttnThreads), 0, stream, p);
   return hipGetLastError();
 }
 
