@@ -17,6 +17,10 @@
  *   ubt_verify_accept  the accepted path and the bonus token
  *   ubt_commit_kv      the accepted path's keys and values appended to the cache
  *
+ * Training uses
+ *
+ *   ubt_tree_kl_loss   the renormalised-KL objective and its gradients
+ *
  * ubt_draft_tree does ubt_bigram_scores + ubt_build_tree in one call (one launch for
  * the common shapes).
  *
@@ -324,6 +328,48 @@ ubt_status_t ubt_commit_kv(const void* k_tree, const void* v_tree, const int32_t
                            const int32_t* accept_len, int32_t* prefix_len, void* k_cache,
                            void* v_cache, int B, int N, int H_kv, int D, int64_t P_max,
                            hipStream_t stream);
+
+/* ------------------------------------------------------------------------------------
+ * ubt_tree_kl_loss -- UBTree's training objective and its gradients.  Method /
+ * Tree-native Training, Eq. (ubtree-training-distributions) and Eq.
+ * (ubtree-training-loss).
+ *
+ * For sequence b and position i (row (b, i), depth i + 1) with ground-truth token
+ * y = y_star[b, i] and predecessor a = anchor[b] (i = 0) or y_star[b, i - 1]:
+ *   s(c)   = alpha[i] u_i(c) + lambda[i] delta_i(a, c),  delta_i(a, c) = (P(h_i) * phi(a)) . psi(c)
+ *   p~(c)  = softmax over c in C_i of z_i(c) / T_train  (T_train = 0: uniform over the
+ *            maximisers of z_i on C_i, the limit T -> 0+)
+ *   q~(c)  = softmax over c in C_i of s(c)
+ *   kl     = sum_c p~ (log p~ - log q~),   ce = -log q_i(y) = lse[b, i] - u_i(y)
+ *   loss   = kl + beta * ce
+ *   grad_s[b, i, j]      = d loss / d s(C_i[j]) = q~ - p~
+ *   grad_logits[b, i, v] = d loss / d u_i(v) = beta (exp(u_i(v) - lse) - [v = y])
+ *                          + alpha[i] [v in C_i] (q~ - p~)(v)
+ * Positions with y outside [0, V) are not valid: loss, kl, ce, grad_s and the gradient row
+ * are 0.  A predecessor outside [0, V) gives delta = 0.
+ *
+ * logits, dt, B, gamma, V, stride_b, stride_i : the proposer logits u, as for ubt_topk.
+ * lse, cand_ids, cand_logit, K : ubt_topk's outputs for these logits (C_i and u_i(C_i));
+ *               the ids of one row must be distinct and in [0, V).
+ * target_logits : the target logits z, dtype dt, [B, gamma, V] with strides t_stride_b,
+ *               t_stride_i (only the entries of C_i are read); finite on C_i.
+ * y_star        : int32 [B, gamma]; anchor : int32 [B].
+ * phi_tab, psi_tab, gate, feat_dt, r, alpha, lambda : the selector's inputs, with
+ *               the checks of ubt_bigram_scores.
+ * T_train >= 0, beta >= 0, both finite.
+ * loss [B, gamma] required; kl, ce [B, gamma], grad_s [B, gamma, K] and grad_logits
+ * float [B, gamma, V] (contiguous, 16-byte aligned) optional.  With grad_logits, two
+ * launches: a dense pass over the logits, then the per-position kernel.
+ * ------------------------------------------------------------------------------------ */
+ubt_status_t ubt_tree_kl_loss(const void* logits, ubt_dtype_t dt, int B, int gamma, int64_t V,
+                              int64_t stride_b, int64_t stride_i, const float* lse,
+                              const int32_t* cand_ids, const float* cand_logit, int K,
+                              const void* target_logits, int64_t t_stride_b, int64_t t_stride_i,
+                              const int32_t* y_star, const int32_t* anchor, const void* phi_tab,
+                              const void* psi_tab, const void* gate, ubt_dtype_t feat_dt, int r,
+                              const float* alpha, const float* lambda, float T_train, float beta,
+                              float* loss, float* kl, float* ce, float* grad_s, float* grad_logits,
+                              hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -38,7 +38,8 @@ STATUS = {0: "UBT_OK", 1: "UBT_ERR_NULL", 2: "UBT_ERR_SHAPE", 3: "UBT_ERR_VALUE"
 # Every symbol include/ubt.h declares.
 EXPORTS = ("ubt_status_str", "ubt_abi_version", "ubt_last_hip_error", "ubt_topk",
            "ubt_bigram_scores", "ubt_build_tree", "ubt_draft_tree", "ubt_draft_step_workspace_bytes",
-           "ubt_draft_step", "ubt_tree_mask", "ubt_tree_attention", "ubt_verify_accept", "ubt_commit_kv")
+           "ubt_draft_step", "ubt_tree_mask", "ubt_tree_attention", "ubt_verify_accept", "ubt_commit_kv",
+           "ubt_tree_kl_loss")
 
 _p = ctypes.c_void_p
 _i32 = ctypes.c_int
@@ -85,8 +86,10 @@ def lib() -> ctypes.CDLL:
                                          _p, _i32, _p, _p]
         L.ubt_verify_accept.argtypes = [_p, _p, _p, _p, _i32, _i32, _p, _p, _p, _p]
         L.ubt_commit_kv.argtypes = [_p, _p, _p, _p, _p, _p, _p, _i32, _i32, _i32, _i32, _i64, _p]
+        L.ubt_tree_kl_loss.argtypes = [_p, _i32, _i32, _i32, _i64, _i64, _i64, _p, _p, _p, _i32, _p, _i64, _i64, _p,
+                                       _p, _p, _p, _p, _i32, _i32, _p, _p, _f32, _f32, _p, _p, _p, _p, _p, _p]
         for f in (L.ubt_topk, L.ubt_bigram_scores, L.ubt_build_tree, L.ubt_draft_tree, L.ubt_tree_mask,
-                  L.ubt_draft_step, L.ubt_tree_attention, L.ubt_verify_accept, L.ubt_commit_kv):
+                  L.ubt_draft_step, L.ubt_tree_attention, L.ubt_verify_accept, L.ubt_commit_kv, L.ubt_tree_kl_loss):
             f.restype = _i32
         _lib = L
     return _lib
@@ -364,6 +367,39 @@ def commit_kv(k_tree: torch.Tensor, v_tree: torch.Tensor, accept_nodes: torch.Te
     st = lib().ubt_commit_kv(_ptr(k_tree), _ptr(v_tree), _ptr(accept_nodes), _ptr(accept_len), _ptr(prefix_len),
                              _ptr(k_cache), _ptr(v_cache), B, N, Hkv, D, k_cache.shape[1], _stream(stream))
     _check("ubt_commit_kv", st)
+
+
+def tree_kl_loss(logits: torch.Tensor, cand: dict, target_logits: torch.Tensor, y_star: torch.Tensor,
+                 anchor: torch.Tensor, phi: torch.Tensor, psi: torch.Tensor, gate: torch.Tensor, alpha, lam,
+                 T_train: float = 1.0, beta: float = 0.1, with_grad: bool = True, out: dict | None = None,
+                 stream=None) -> dict:
+    """``ubt_tree_kl_loss``: the renormalised-KL objective per position and its gradients.
+    ``cand`` holds ``ubt_topk``'s ``cand_ids``, ``cand_logit`` and ``lse`` for ``logits``;
+    ``target_logits`` has the logits' shape and dtype (unit stride along V)."""
+    _need_gpu(logits, target_logits, y_star, anchor, phi, psi, gate)
+    B, gamma, V = logits.shape
+    K = cand["cand_ids"].shape[2]
+    r = phi.shape[1]
+    if logits.stride(2) != 1 or target_logits.stride(2) != 1 or target_logits.shape != logits.shape:
+        raise ValueError("logits and target_logits must be [B, gamma, V] with unit stride along V")
+    if target_logits.dtype != logits.dtype:
+        raise TypeError("target_logits must have the logits' dtype")
+    a = (ctypes.c_float * gamma)(*[float(x) for x in alpha])
+    l = (ctypes.c_float * gamma)(*[float(x) for x in lam])
+    if out is None:
+        f32 = dict(dtype=torch.float32, device=logits.device)
+        out = dict(loss=torch.empty(B, gamma, **f32), kl=torch.empty(B, gamma, **f32),
+                   ce=torch.empty(B, gamma, **f32), grad_s=torch.empty(B, gamma, K, **f32),
+                   grad_logits=torch.empty(B, gamma, V, **f32) if with_grad else None)
+    st = lib().ubt_tree_kl_loss(_ptr(logits), _dtype_code(logits), B, gamma, V, logits.stride(0), logits.stride(1),
+                                _ptr(cand["lse"]), _ptr(cand["cand_ids"]), _ptr(cand["cand_logit"]), K,
+                                _ptr(target_logits), target_logits.stride(0), target_logits.stride(1), _ptr(y_star),
+                                _ptr(anchor), _ptr(phi), _ptr(psi), _ptr(gate), _dtype_code(phi), r, a, l,
+                                float(T_train), float(beta), _ptr(out["loss"]), _ptr(out.get("kl")),
+                                _ptr(out.get("ce")), _ptr(out.get("grad_s")), _ptr(out.get("grad_logits")),
+                                _stream(stream))
+    _check("ubt_tree_kl_loss", st)
+    return out
 
 
 class DraftStep:

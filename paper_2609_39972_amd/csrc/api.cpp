@@ -299,4 +299,59 @@ ubt_status_t ubt_commit_kv(const void* k_tree, const void* v_tree, const int32_t
                                           N, H_kv, D, P_max, stream));
 }
 
+ubt_status_t ubt_tree_kl_loss(const void* logits, ubt_dtype_t dt, int B, int gamma, int64_t V, int64_t stride_b,
+                              int64_t stride_i, const float* lse, const int32_t* cand_ids, const float* cand_logit,
+                              int K, const void* target_logits, int64_t t_stride_b, int64_t t_stride_i,
+                              const int32_t* y_star, const int32_t* anchor, const void* phi_tab, const void* psi_tab,
+                              const void* gate, ubt_dtype_t feat_dt, int r, const float* alpha, const float* lambda,
+                              float T_train, float beta, float* loss, float* kl, float* ce, float* grad_s,
+                              float* grad_logits, hipStream_t stream) {
+  if (!logits || !lse || !target_logits || !y_star || !loss) return UBT_ERR_NULL;
+  if (!valid_dtype(dt)) return UBT_ERR_VALUE;
+  ubt::Scales sc;
+  ubt_status_t st = check_selector(phi_tab, psi_tab, gate, feat_dt, V, r, anchor, cand_ids, cand_logit, alpha, lambda,
+                                   B, gamma, K, sc);
+  if (st != UBT_OK) return st;
+  if (stride_i < V || stride_b < static_cast<int64_t>(gamma) * stride_i || t_stride_i < V ||
+      t_stride_b < static_cast<int64_t>(gamma) * t_stride_i)
+    return UBT_ERR_SHAPE;
+  if (static_cast<int64_t>(B) * gamma >= (int64_t(1) << 31) || (V + 8191) / 8192 > 65535) return UBT_ERR_SHAPE;
+  if (!(isfinite(T_train) && T_train >= 0.f && isfinite(beta) && beta >= 0.f)) return UBT_ERR_VALUE;
+  if (feat_dt == UBT_F32 && !(aligned16(phi_tab) && aligned16(psi_tab) && aligned16(gate))) return UBT_ERR_UNSUPPORTED;
+  if (grad_logits && !aligned16(grad_logits)) return UBT_ERR_UNSUPPORTED;
+  const int64_t es = dt == UBT_BF16 ? 2 : 4;
+  ubt::TreeKlArgs a{};
+  a.logits = logits;
+  a.target = target_logits;
+  a.dtype = static_cast<int>(dt);
+  a.feat_dtype = static_cast<int>(feat_dt);
+  a.B = B;
+  a.gamma = gamma;
+  a.K = K;
+  a.r = r;
+  a.V = V;
+  a.stride_b = stride_b;
+  a.stride_i = stride_i;
+  a.t_stride_b = t_stride_b;
+  a.t_stride_i = t_stride_i;
+  a.vec = V % 8 == 0 && aligned16(logits) && (stride_b * es) % 16 == 0 && (stride_i * es) % 16 == 0;
+  a.lse = lse;
+  a.cand_ids = cand_ids;
+  a.cand_logit = cand_logit;
+  a.y_star = y_star;
+  a.anchor = anchor;
+  a.phi = phi_tab;
+  a.psi = psi_tab;
+  a.gate = gate;
+  a.sc = sc;
+  a.T = T_train;
+  a.beta = beta;
+  a.loss = loss;
+  a.kl = kl;
+  a.ce = ce;
+  a.grad_s = grad_s;
+  a.grad = grad_logits;
+  return hip_status(ubt::launch_tree_kl_loss(a, stream));
+}
+
 }  // extern "C"

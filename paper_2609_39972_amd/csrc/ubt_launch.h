@@ -101,4 +101,29 @@ hipError_t launch_commit_kv(const void* k_tree, const void* v_tree, const int32_
                             const int32_t* accept_len, int32_t* prefix_len, void* k_cache, void* v_cache, int B, int N,
                             int Hkv, int D, int64_t Pmax, hipStream_t stream);
 
+// ---- renormalised-KL training objective -------------------------------------------------
+struct TreeKlArgs {
+  const void* logits;  // [B, gamma, V] with strides, dtype
+  const void* target;  // same dtype, its own strides
+  int dtype, feat_dtype, B, gamma, K, r;
+  int64_t V, stride_b, stride_i, t_stride_b, t_stride_i;
+  bool vec;  // 16-byte aligned rows of V % 8 == 0 elements
+  const float* lse;
+  const int32_t* cand_ids;
+  const float* cand_logit;
+  const int32_t* y_star;
+  const int32_t* anchor;
+  const void* phi;
+  const void* psi;
+  const void* gate;
+  Scales sc;
+  float T, beta;
+  float* loss;
+  float* kl;
+  float* ce;
+  float* grad_s;
+  float* grad;  // [B, gamma, V] or null
+};
+hipError_t launch_tree_kl_loss(const TreeKlArgs& a, hipStream_t stream);
+
 }  // namespace ubt

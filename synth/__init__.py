@@ -256,3 +256,34 @@ def verify_targets(seed: int, token: np.ndarray, parent: np.ndarray, n_nodes: np
             tgt[b, cur] = token[b, c]
             cur = c
     return tgt
+
+
+# ---- training-objective inputs ------------------------------------------------------------
+F_TNOISE, F_YSTAR = 30, 31
+
+
+def loss_inputs(w: Workload, buf: int = 0, invalid_frac: float = 0.05) -> dict:
+    """Synthetic operands of the training objective for workload ``w``:
+
+    * ``target_logits [B, gamma, V]`` (stored like the logits): each proposer row plus
+      N(0, 1) noise, so the target agrees with the proposer only roughly;
+    * ``y_star int32[B, gamma]``: the ground-truth tokens.  For Zipf rows the token of
+      rank k (in the row's permutation) with probability proportional to k^-s over the
+      first 64 ranks, so it usually lies in the candidate set; for normal rows a uniform
+      token.  A share ``invalid_frac`` of the positions is -1 (not valid)."""
+    rng = _rng(w.cfg, buf, F_YSTAR)
+    z = np.empty((w.rows, w.V), dtype=np.uint16 if w.dtype == "bf16" else np.float32)
+    y = np.empty(w.rows, np.int32)
+    ranks = np.arange(1, 65, dtype=np.float64)
+    pr = ranks ** -w.zipf_s
+    pr /= pr.sum()
+    for row in range(w.rows):
+        u = logit_row(w, buf, row)
+        z[row] = store(u + _rng(w.cfg, buf, F_TNOISE, row).normal(0.0, 1.0, w.V), w.dtype)
+        if w.logits == "zipf":
+            perm = _rng(w.cfg, buf, F_PERM, row).permutation(w.V)
+            y[row] = perm[int(rng.choice(64, p=pr))]
+        else:
+            y[row] = int(rng.integers(0, w.V))
+    y[rng.random(w.rows) < invalid_frac] = -1
+    return dict(target_logits=z.reshape(w.B, w.gamma, w.V), y_star=y.reshape(w.B, w.gamma))

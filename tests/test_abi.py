@@ -193,3 +193,25 @@ def test_commit_kv_validation(kw, code):
     a.update(kw)
     assert ubt.lib().ubt_commit_kv(a["kt"], a["vt"], a["nodes"], a["alen"], a["plen"], a["kc"], a["vc"], a["B"],
                                    a["N"], a["Hkv"], a["D"], a["Pmax"], None) == code
+
+
+def _kl(**kw):
+    g = kw.pop("gamma", 3)
+    a = (ctypes.c_float * 64)(*([1.0] * 64))
+    args = dict(logits=FAKE, dt=1, B=2, gamma=g, V=1000, sb=3000, si=1000, lse=FAKE, ids=FAKE, cl=FAKE, K=8, z=FAKE,
+                tsb=3000, tsi=1000, y=FAKE, anchor=FAKE, phi=FAKE, psi=FAKE, gate=FAKE, fdt=1, r=64, alpha=a, lam=a,
+                T=1.0, beta=0.1, loss=FAKE, kl=None, ce=None, gs=None, grad=None)
+    args.update(kw)
+    v = list(args.values())
+    return ubt.lib().ubt_tree_kl_loss(*v, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(logits=None), 1), (dict(lse=None), 1), (dict(z=None), 1), (dict(y=None), 1), (dict(loss=None), 1),
+    (dict(ids=None), 1), (dict(phi=None), 1), (dict(anchor=None), 1),
+    (dict(dt=4), 3), (dict(fdt=4), 3), (dict(T=-0.5), 3), (dict(T=float("nan")), 3), (dict(beta=-1.0), 3),
+    (dict(B=0), 2), (dict(K=65), 2), (dict(r=24), 2), (dict(si=999), 2), (dict(tsi=999), 2), (dict(tsb=2999), 2),
+    (dict(grad=ctypes.c_void_p(0x10004)), 4), (dict(gate=ctypes.c_void_p(0x10008)), 4),
+])
+def test_tree_kl_loss_validation(kw, code):
+    assert _kl(**kw) == code
