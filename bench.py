@@ -204,6 +204,94 @@ def bench_verify(args, dev) -> int:
     return 0
 
 
+def bench_loss(args, dev) -> int:
+    """The renormalised-KL objective with its logit gradient on the headline workload's
+    logits (B=32, gamma=15, V=151936 bf16, K=8, r=128): the dense gradient pass (the
+    dominant kernel: it reads every logit and writes an fp32 gradient) and the
+    per-position kernel, timed together and apart."""
+    import numpy as np
+    import torch
+
+    import paper_2609_39972_amd as ubt
+    import synth
+
+    w = synth.WORKLOADS[3]
+    d = synth.inputs(w, 0)
+    li = synth.loss_inputs(w, 0)
+    bits = lambda a: ubt.bf16_tensor_from_bits(a, dev)
+    logits, z = bits(d["logits"]), bits(li["target_logits"])
+    y = torch.from_numpy(li["y_star"]).to(dev)
+    anchor = torch.from_numpy(d["anchor"]).to(dev)
+    phi, psi, gate = bits(d["phi"]), bits(d["psi"]), bits(d["gate"])
+    cand = ubt.topk(logits, w.K)
+    out = ubt.tree_kl_loss(logits, cand, z, y, anchor, phi, psi, gate, d["alpha"], d["lam"])
+    no_grad = {k: (v if k != "grad_logits" else None) for k, v in out.items()}
+    torch.cuda.synchronize()
+    stream = torch.cuda.Stream(device=dev)
+
+    def timed(fn, n=100, replays=4):
+        with torch.cuda.stream(stream):
+            fn()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=stream):
+            for _ in range(n):
+                fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        with torch.cuda.stream(stream):
+            g.replay()
+            a.record(stream)
+            for _ in range(replays):
+                g.replay()
+            b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) * 1e3 / (n * replays)
+
+    both_us = timed(lambda: ubt.tree_kl_loss(logits, cand, z, y, anchor, phi, psi, gate, d["alpha"], d["lam"],
+                                             out=out, stream=stream))
+    pos_us = timed(lambda: ubt.tree_kl_loss(logits, cand, z, y, anchor, phi, psi, gate, d["alpha"], d["lam"],
+                                            out=no_grad, stream=stream))
+    dense_us = max(both_us - pos_us, 1e-3)
+    dense_bytes = w.rows * w.V * (2 + 4)  # read bf16 logits, write fp32 gradient
+    gbps = dense_bytes / (dense_us * 1e-6) / 1e9
+    log(f"loss + gradient {both_us:.2f} us (dense pass ~{dense_us:.2f} us, {gbps:.0f} GB/s; per-position kernel "
+        f"{pos_us:.2f} us)")
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        import oracle.loss as ol
+
+        c = oracle.topk(d["logits"][:1], w.K)
+        t0, reps = time.perf_counter(), 0
+        while True:
+            ol.tree_kl_loss(d["logits"][:1], c["cand_ids"], li["target_logits"][:1], li["y_star"][:1],
+                            d["anchor"][:1], d["phi"], d["psi"], d["gate"][:1], d["alpha"], d["lam"], 1.0, 0.1)
+            reps += 1
+            if time.perf_counter() - t0 >= min(args.cpu_seconds, 10.0):
+                break
+        el = time.perf_counter() - t0
+        cpu = {"value": round(reps * w.gamma / el, 3), "unit": "positions/s", "cores": 1, "kind": "oracle",
+               "sample": f"{reps} x sequence 0 ({w.gamma} positions, loss and full logit gradient), fp64 numpy "
+                         f"oracle, {el:.1f} s"}
+    res = {
+        "metric": "training objective + logit gradient us/call at B=32, gamma=15, V=151936 (bf16), K=8",
+        "value": round(w.rows / (both_us * 1e-6), 1), "unit": "positions/s", "n_gpus": 1, "steps": 400,
+        "warmup": 100, "ms_per_step": round(both_us / 1e3, 6), "us_per_step": round(both_us, 3),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "kl-loss-" + w.name, "B": w.B, "gamma": w.gamma, "V": w.V, "K": w.K, "r": w.r,
+                   "T_train": 1.0, "beta": 0.1},
+        "kernels_us": {"loss_and_gradient": round(both_us, 3), "kl_position_kernel": round(pos_us, 3),
+                       "kl_dense_kernel (difference)": round(dense_us, 3)},
+        "roofline": {"bound": "hbm", "kernel": "kl_dense_kernel", "achieved": round(gbps, 1), "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": round(gbps / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "algorithmic_bytes_per_launch": dense_bytes},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(res), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -212,9 +300,10 @@ def main() -> int:
     ap.add_argument("--workload", type=int, default=3, help="synthetic workload id (3 = B=32, V=151936 headline)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="minimum oracle time for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--mode", choices=("step", "tree", "separate", "verify"), default="tree",
+    ap.add_argument("--mode", choices=("step", "tree", "separate", "verify", "loss"), default="tree",
                     help="step: one ubt_draft_step call; tree: ubt_topk + ubt_draft_tree; separate: ubt_topk + "
-                         "ubt_bigram_scores + ubt_build_tree; verify: tree verification (its own JSON line)")
+                         "ubt_bigram_scores + ubt_build_tree; verify: tree verification; loss: the training "
+                         "objective (each its own JSON line)")
     ap.add_argument("--sweep-launches", type=int, default=200, help="launches per kernel in the per-kernel timing")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run a plain device copy of known size (counter calibration) and exit")
@@ -245,6 +334,8 @@ def main() -> int:
         return 0
     if args.mode == "verify":
         return bench_verify(args, dev)
+    if args.mode == "loss":
+        return bench_loss(args, dev)
 
     w = synth.WORKLOADS[args.workload]
     pool = max(1, -(-POOL_BYTES // w.logit_bytes))
