@@ -88,34 +88,37 @@ struct Stage {
   v4u v0, v1;
 };
 
+// Every load is issued unconditionally (clamped to a valid row, the value then dropped),
+// so the number of loads in flight is the same on every path and the compiler waits for
+// exactly the ones a value needs.
 template <int D>
 __device__ __forceinline__ void stage_load(const AttnArgs& p, Stage<D>& s, int b, int h, int blk, int npb, int P,
                                            int nn, int t) {
   constexpr int C = Stage<D>::kChunks;
   const bool tree = blk >= npb;
   const int base = tree ? (blk - npb) * kKB : blk * kKB;
-  const int lim = tree ? nn : P;
+  const int lim = tree ? nn : P;  // >= base + 1 for every block that exists
   const int64_t S = tree ? p.N : p.Pmax;
   const uint16_t* ks = tree ? p.kt : p.kc;
   const uint16_t* vs = tree ? p.vt : p.vc;
   const v4u zero = v4u{0u, 0u, 0u, 0u};
+  auto row_ptr = [&](const uint16_t* src, int key, int c) {
+    const int kk = min(key, lim - 1);
+    return reinterpret_cast<const v4u*>(src + ((static_cast<int64_t>(b) * S + kk) * p.Hkv + h) * D + 8 * c);
+  };
 #pragma unroll
   for (int i = 0; i < Stage<D>::kKPerThread; ++i) {
     const int id = t + kAttnThreads * i;
-    const int row = id / C, c = id % C;
-    const int key = base + row;
-    s.k[i] = (row < kKB && key < lim)
-                 ? *reinterpret_cast<const v4u*>(ks + ((static_cast<int64_t>(b) * S + key) * p.Hkv + h) * D + 8 * c)
-                 : zero;
+    const int row = min(id / C, kKB - 1), c = id % C;
+    const v4u v = *row_ptr(ks, base + row, c);
+    s.k[i] = (id / C < kKB && base + row < lim) ? v : zero;
   }
-  const int kp = t % 16, c = t / 16;
+  const int kp = t % 16, c = min(t / 16, C - 1);
   const int k0 = base + 2 * kp;
-  const bool in = c < C;  // 16 key pairs x C chunks: the first 16 C threads
-  s.v0 = (in && k0 < lim) ? *reinterpret_cast<const v4u*>(vs + ((static_cast<int64_t>(b) * S + k0) * p.Hkv + h) * D + 8 * c)
-                          : zero;
-  s.v1 = (in && k0 + 1 < lim)
-             ? *reinterpret_cast<const v4u*>(vs + ((static_cast<int64_t>(b) * S + k0 + 1) * p.Hkv + h) * D + 8 * c)
-             : zero;
+  const bool in = t / 16 < C;  // 16 key pairs x C chunks: the first 16 C threads
+  const v4u a = *row_ptr(vs, k0, c), bb = *row_ptr(vs, k0 + 1, c);
+  s.v0 = (in && k0 < lim) ? a : zero;
+  s.v1 = (in && k0 + 1 < lim) ? bb : zero;
 }
 
 template <int D>
@@ -187,8 +190,10 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attention_kernel(AttnArgs p
     live[j] = rin[j] && n_of[j] < nn;
     const uint16_t* qr = p.q + ((static_cast<int64_t>(b) * p.N + n_of[j]) * p.H + head_of[j]) * D;
 #pragma unroll
-    for (int s = 0; s < DS; ++s)
-      qf[j][s] = live[j] ? *reinterpret_cast<const v4u*>(qr + 32 * s + 8 * kg) : v4u{0u, 0u, 0u, 0u};
+    for (int s = 0; s < DS; ++s) {
+      const v4u v = *reinterpret_cast<const v4u*>(qr + 32 * s + 8 * kg);
+      qf[j][s] = live[j] ? v : v4u{0u, 0u, 0u, 0u};
+    }
     mrow[j] = p.mask + (static_cast<int64_t>(b) * p.N + n_of[j]) * words;
   }
 
@@ -208,10 +213,19 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attention_kernel(AttnArgs p
     stage_load<D>(p, sg, b, h, 0, npb, P, nn, t);
     stage_store<D>(lds, 0, sg, t);
   }
+  // Nothing is in flight when the loop starts: the first MFMA of each block then waits
+  // for no global load, and the next block's loads stay in flight behind the compute.
+  __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   for (int blk = 0; blk < nblk; ++blk) {
     const int st = blk & 1;
-    if (blk + 1 < nblk) stage_load<D>(p, sg, b, h, blk + 1, npb, P, nn, t);
+    // This block's mask words, then the next block's K/V (the last block loads itself
+    // again, unused), all unconditional.
+    const int tb = blk >= npb ? blk - npb : 0;
+    uint32_t mw[TW];
+#pragma unroll
+    for (int j = 0; j < TW; ++j) mw[j] = mrow[j][tb];
+    stage_load<D>(p, sg, b, h, blk + 1 < nblk ? blk + 1 : blk, npb, P, nn, t);
 
     // ---- S^T = K Q^T for 32 keys and each tile ----
     v4f s0[TW], s1[TW];
@@ -244,12 +258,11 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attention_kernel(AttnArgs p
 #pragma unroll
       for (int j = 0; j < TW; ++j) vis[j] = live[j] ? v : 0u;
     } else {
-      const int tb = blk - npb;
       const int left = nn - tb * kKB;
       const uint32_t in = left >= 32 ? ~0u : ((1u << left) - 1u);
 #pragma unroll
       for (int j = 0; j < TW; ++j) {
-        const uint32_t bits = live[j] ? (mrow[j][tb] & in) : 0u;
+        const uint32_t bits = live[j] ? (mw[j] & in) : 0u;
         vis[j] = ((bits >> (4 * kg)) & 0xFu) | (((bits >> (16 + 4 * kg)) & 0xFu) << 4);
       }
     }
