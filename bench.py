@@ -39,6 +39,12 @@ def log(msg: str) -> None:
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
+VERIFY_PROFILE = os.path.join(ROOT, "profiles", "tree_attention_verify-b32-n65-p4096.md")
+VERIFY_SOURCES = ("verify.hip", "ubt_device.h")
+LOSS_PROFILE = os.path.join(ROOT, "profiles", "kl_loss_zipf-v151936-b32.md")
+LOSS_SOURCES = ("loss.hip", "ubt_device.h")
+
+
 def source_hash(files=SWEEP_SOURCES) -> str:
     h = hashlib.sha256()
     for f in files:
@@ -47,15 +53,15 @@ def source_hash(files=SWEEP_SOURCES) -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic() -> dict | None:
-    """HBM bytes per sweep launch from the committed counter summary, if it was taken on
-    the current source of that kernel (and on the headline workload)."""
-    if not os.path.exists(TRAFFIC_PROFILE):
+def measured_traffic(profile: str = TRAFFIC_PROFILE, files=SWEEP_SOURCES) -> dict | None:
+    """HBM bytes per launch of a dominant kernel from its committed counter summary, if
+    that summary was taken on the kernel's current source."""
+    if not os.path.exists(profile):
         return None
-    txt = open(TRAFFIC_PROFILE).read()
+    txt = open(profile).read()
     m_hash = re.search(r"source hash:\s*`?([0-9a-f]{16})", txt)
     m_bytes = re.search(r"hbm bytes per launch:\s*([0-9.eE+]+)", txt)
-    if not (m_hash and m_bytes) or m_hash.group(1) != source_hash():
+    if not (m_hash and m_bytes) or m_hash.group(1) != source_hash(files):
         return None
     return {"bytes": float(m_bytes.group(1))}
 
@@ -195,7 +201,8 @@ def bench_verify(args, dev) -> int:
                      "peak": HBM_PEAK_GBPS if bound == "hbm" else MFMA_BF16_PEAK_TFLOPS,
                      "unit": "GB/s" if bound == "hbm" else "TFLOP/s",
                      "frac": round(gbps / HBM_PEAK_GBPS if bound == "hbm" else tflops / MFMA_BF16_PEAK_TFLOPS, 4),
-                     "traffic": None, "algorithmic_bytes_per_launch": att_bytes, "algorithmic_flops": flops,
+                     "traffic": (measured_traffic(VERIFY_PROFILE, VERIFY_SOURCES) or {}).get("bytes"),
+                     "algorithmic_bytes_per_launch": att_bytes, "algorithmic_flops": flops,
                      "other": {"TFLOP/s": round(tflops, 1), "mfma_frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4),
                                "GB/s": round(gbps, 1), "hbm_frac": round(gbps / HBM_PEAK_GBPS, 4)}},
         "cpu_baseline": cpu,
@@ -284,7 +291,8 @@ def bench_loss(args, dev) -> int:
         "kernels_us": {"loss_and_gradient": round(both_us, 3), "kl_position_kernel": round(pos_us, 3),
                        "kl_dense_kernel (difference)": round(dense_us, 3)},
         "roofline": {"bound": "hbm", "kernel": "kl_dense_kernel", "achieved": round(gbps, 1), "peak": HBM_PEAK_GBPS,
-                     "unit": "GB/s", "frac": round(gbps / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "unit": "GB/s", "frac": round(gbps / HBM_PEAK_GBPS, 4),
+                     "traffic": (measured_traffic(LOSS_PROFILE, LOSS_SOURCES) or {}).get("bytes"),
                      "algorithmic_bytes_per_launch": dense_bytes},
         "cpu_baseline": cpu,
     }
