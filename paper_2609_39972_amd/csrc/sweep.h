@@ -328,7 +328,21 @@ struct WaveState {
   uint32_t thr;   // candidate threshold key (0 = none): groups need max key >= thr
   int nbuf;       // groups waiting in the LDS buffer
   bool overflow;  // a group that passed could not be buffered
+  // K > 16: a full buffer is merged into a running top K instead (lanes 0..K-1 of
+  // cur_key/cur_id), and the threshold tightens to its K-th key (strictly, once K are held:
+  // later elements carry larger ids).
+  bool strict, merged;
+  uint32_t cur_key, cur_id;
 };
+
+// Buffers the groups of pending that pass.  kBig (K > 16): a full buffer is merged into
+// the running top K, the threshold tightened, and the rest re-filtered, until every
+// passing group is held.  Otherwise a group that does not fit sets `overflow` (exact
+// re-scan at the end).
+template <typename T, bool kBig>
+__device__ __forceinline__ void push_groups(const u32x4 (&buf)[kSubGroups], const float (&gmax)[kSubGroups],
+                                            uint32_t pending, int64_t c0, int64_t V, int K, int lane, WaveLds& s,
+                                            WaveState& st);
 
 // Max and exp-sum of one tile, folded into the lane's running (lm, ls): ls is the
 // sum of exp(x - lm) over the lane's elements so far, where lm may trail the lane's true
@@ -485,6 +499,36 @@ __device__ uint2 rescan(__amdgpu_buffer_rsrc_t rsrc, const T* rp, int64_t first,
   return make_uint2(cur_key, cur_id);
 }
 
+template <typename T, bool kBig>
+__device__ __forceinline__ void push_groups(const u32x4 (&buf)[kSubGroups], const float (&gmax)[kSubGroups],
+                                            uint32_t pending, int64_t c0, int64_t V, int K, int lane, WaveLds& s,
+                                            WaveState& st) {
+  pending = buffer_groups<T>(buf, pending, c0, lane, s, st.nbuf);
+  if (!ballot(pending != 0)) return;
+  if (!kBig) {
+    st.overflow = true;
+    return;
+  }
+  do {
+    __builtin_amdgcn_wave_barrier();
+    const uint2 c = flush<T, false>(s, st.nbuf, V, st.thr, st.strict, K, lane, st.cur_key, st.cur_id);
+    st.cur_key = c.x;
+    st.cur_id = c.y;
+    st.nbuf = 0;
+    st.merged = true;
+    __builtin_amdgcn_wave_barrier();
+    if (popc(ballot(st.cur_key != 0)) >= K) {
+      const uint32_t mn = kth_key(st.cur_key, K, lane);
+      if (mn > st.thr || (mn == st.thr && !st.strict)) {
+        st.thr = mn;
+        st.strict = true;
+      }
+    }
+    pending &= passing_groups<T>(gmax, c0, V, st.thr, st.strict, lane);
+    pending = buffer_groups<T>(buf, pending, c0, lane, s, st.nbuf);
+  } while (ballot(pending != 0));
+}
+
 // Where a row's results go.  With `coherent`, the stores are device-coherent (they reach
 // the point of coherence of all XCDs), for a reader in another workgroup of the same
 // launch that waits on a flag.
@@ -506,7 +550,7 @@ struct RowOut {
 
 // The row at rp (V elements) of global row index `row`; the workgroup has up to MW waves
 // and `lds` is its shared memory.  Writes cand_*[row * K, row * K + K) and lse[row].
-template <typename T, bool kAligned, int MW = kWaves>
+template <typename T, bool kAligned, int MW = kWaves, bool kBig = false>
 __device__ __forceinline__ void sweep_row(RowLdsT<MW>& lds, const T* __restrict__ rp, int64_t V, int K, int64_t row,
                                           const RowOut& out) {
   constexpr int EPG = Traits<T>::kPer;
@@ -521,7 +565,7 @@ __device__ __forceinline__ void sweep_row(RowLdsT<MW>& lds, const T* __restrict_
   const uint32_t lane_off = static_cast<uint32_t>(lane * EPG * sizeof(T));
   WaveLds& s = lds.wave[w];
 
-  WaveState st{neg_inf(), 0.f, 0u, 0, false};
+  WaveState st{neg_inf(), 0.f, 0u, 0, false, false, false, 0u, 0u};
   u32x4 bufA[kSubGroups], bufB[kSubGroups];
   float gmax[kSubGroups];
   // Tiles [0, nfull) stream through the pipeline (aligned rows only, with the ragged last
@@ -550,7 +594,19 @@ __device__ __forceinline__ void sweep_row(RowLdsT<MW>& lds, const T* __restrict_
     if (threadIdx.x == 0) lds.thr2 = 0;
   }
   __syncthreads();
-  {
+  if (kBig) {
+    // T = (a lower bound of) the K-th largest of all the lane maxima: K of them, maxima of
+    // disjoint elements, reach it.  For large K this is far tighter than the K-th column
+    // maximum (each column maximum covers all the waves' lanes).
+    uint32_t lk[MW];
+    uint64_t lv[MW];
+#pragma unroll
+    for (int j = 0; j < MW; ++j) {
+      lk[j] = j < nw ? lds.lane_max[j * kWave + lane] : 0u;
+      lv[j] = ballot(lk[j] != 0u);
+    }
+    st.thr = wave_threshold<MW>(lk, lv, K, K + K / 4);
+  } else {
     // T = the K-th largest of the 64 column maxima (lane l's largest lane maximum over the
     // waves): K distinct groups reach it, so it is a lower bound of the row's K-th largest
     // element.  Each lane counts the column maxima above its own.
@@ -571,7 +627,7 @@ __device__ __forceinline__ void sweep_row(RowLdsT<MW>& lds, const T* __restrict_
   }
   if (sc < nfull) {
     const uint32_t p = passing_groups<T>(gmax, sc * SUB, V, st.thr, false, lane);
-    if (ballot(p != 0) && ballot(buffer_groups<T>(bufA, p, sc * SUB, lane, s, st.nbuf) != 0)) st.overflow = true;
+    if (ballot(p != 0)) push_groups<T, kBig>(bufA, gmax, p, sc * SUB, V, K, lane, s, st);
   }
   sc += nw;
 
@@ -580,8 +636,8 @@ __device__ __forceinline__ void sweep_row(RowLdsT<MW>& lds, const T* __restrict_
     if (c0 == last_c0) mask_tail<T>(buf, c0, V, lane);
     reduce_sub<T>(buf, gmax, st.lm, st.ls);
     if (!st.overflow && any_pass_full<T>(gmax, st.thr)) {
-      const uint32_t p = passing_groups<T>(gmax, c0, V, st.thr, false, lane);
-      if (ballot(buffer_groups<T>(buf, p, c0, lane, s, st.nbuf) != 0)) st.overflow = true;
+      const uint32_t p = passing_groups<T>(gmax, c0, V, st.thr, st.strict, lane);
+      if (ballot(p != 0)) push_groups<T, kBig>(buf, gmax, p, c0, V, K, lane, s, st);
     }
   };
   // The remaining tiles, the next one always in flight; the last tile issues no load.
@@ -613,8 +669,8 @@ __device__ __forceinline__ void sweep_row(RowLdsT<MW>& lds, const T* __restrict_
     load_checked<T, kAligned>(bufA, rsrc, rp, sr * SUB, V, lane);
     reduce_sub<T>(bufA, gmax, st.lm, st.ls);
     if (!st.overflow) {
-      const uint32_t p = passing_groups<T>(gmax, sr * SUB, V, st.thr, false, lane);
-      if (ballot(p != 0) && ballot(buffer_groups<T>(bufA, p, sr * SUB, lane, s, st.nbuf) != 0)) st.overflow = true;
+      const uint32_t p = passing_groups<T>(gmax, sr * SUB, V, st.thr, st.strict, lane);
+      if (ballot(p != 0)) push_groups<T, kBig>(bufA, gmax, p, sr * SUB, V, K, lane, s, st);
     }
   }
 
@@ -622,10 +678,17 @@ __device__ __forceinline__ void sweep_row(RowLdsT<MW>& lds, const T* __restrict_
   // the buffer, or, when there are more than 64 of them or the buffer overflowed, the top
   // K picked by the radix selection.
   int n = 0;
-  if (!st.overflow) n = st.nbuf > 0 ? stage_live<T>(s, st.nbuf, V, st.thr, lane) : 0;
-  if (st.overflow || n > kWave) {
+  if (!st.overflow && !(kBig && st.merged)) n = st.nbuf > 0 ? stage_live<T>(s, st.nbuf, V, st.thr, lane) : 0;
+  if (st.overflow || (kBig && st.merged) || n > kWave) {
     uint32_t ck = 0, ci = 0;
-    if (!st.overflow) {
+    if (kBig && st.merged) {
+      // The running top K plus what the buffer still holds.
+      __builtin_amdgcn_wave_barrier();
+      const uint2 c = st.nbuf > 0 ? flush<T, false>(s, st.nbuf, V, st.thr, st.strict, K, lane, st.cur_key, st.cur_id)
+                                  : make_uint2(st.cur_key, st.cur_id);
+      ck = c.x;
+      ci = c.y;
+    } else if (!st.overflow) {
       __builtin_amdgcn_wave_barrier();
       const uint2 c = flush<T, true>(s, st.nbuf, V, st.thr, false, K, lane, 0u, 0u);
       ck = c.x;

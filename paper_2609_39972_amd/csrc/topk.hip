@@ -10,7 +10,8 @@
 namespace ubt {
 namespace {
 
-template <typename T, bool kAligned>
+// kBig: K > 16 (a tighter first threshold and a running top K instead of the re-scan).
+template <typename T, bool kAligned, bool kBig>
 __global__ __launch_bounds__(kWave* kWaves, 4) void topk_row_kernel(const T* __restrict__ logits, int gamma,
                                                                     int64_t V, int64_t stride_b, int64_t stride_i,
                                                                     int K, int32_t* __restrict__ cand_ids,
@@ -20,7 +21,7 @@ __global__ __launch_bounds__(kWave* kWaves, 4) void topk_row_kernel(const T* __r
   __shared__ RowLds lds;
   const int64_t row = blockIdx.x;
   const int64_t b = row / gamma, i = row - b * gamma;
-  sweep_row<T, kAligned>(lds, logits + b * stride_b + i * stride_i, V, K, row,
+  sweep_row<T, kAligned, kWaves, kBig>(lds, logits + b * stride_b + i * stride_i, V, K, row,
                          RowOut{cand_ids, cand_logit, cand_logprob, lse, false});
 }
 
@@ -28,9 +29,14 @@ template <typename T, bool kAligned>
 void launch_typed(const void* logits, int B, int gamma, int64_t V, int64_t stride_b, int64_t stride_i, int K,
                   int32_t* cand_ids, float* cand_logit, float* cand_logprob, float* lse, hipStream_t stream) {
   const int64_t rows = static_cast<int64_t>(B) * gamma;
-  hipLaunchKernelGGL((topk_row_kernel<T, kAligned>), dim3(static_cast<unsigned>(rows)), dim3(kWave * kWaves), 0,
-                     stream, static_cast<const T*>(logits), gamma, V, stride_b, stride_i, K, cand_ids, cand_logit,
-                     cand_logprob, lse);
+  if (K > 16)
+    hipLaunchKernelGGL((topk_row_kernel<T, kAligned, true>), dim3(static_cast<unsigned>(rows)), dim3(kWave * kWaves),
+                       0, stream, static_cast<const T*>(logits), gamma, V, stride_b, stride_i, K, cand_ids, cand_logit,
+                       cand_logprob, lse);
+  else
+    hipLaunchKernelGGL((topk_row_kernel<T, kAligned, false>), dim3(static_cast<unsigned>(rows)), dim3(kWave * kWaves),
+                       0, stream, static_cast<const T*>(logits), gamma, V, stride_b, stride_i, K, cand_ids, cand_logit,
+                       cand_logprob, lse);
 }
 
 }  // namespace
