@@ -31,7 +31,7 @@ __device__ __forceinline__ int div_k(int e, uint64_t magic) {
 //    of them with broadcast reads, so F_d needs no sort and no reordering of registers.
 //  * the supertree keys of all depths are loaded once into registers for Top_budget;
 //    the ancestor mask is built by pointer jumping (ceil(log2(gamma+1)) rounds).
-constexpr int kFastMaxWK = 512;
+constexpr int kFastMaxWK = 1024;
 constexpr int kFastMaxGW = 1024;
 constexpr int kFastMaxW = 64;
 constexpr int kStageLive = 272;                // up to 255 selected entries + 16 zero entries
@@ -50,8 +50,10 @@ __host__ __device__ inline FastLayout fast_layout(int gamma, int K, int W) {
     p += static_cast<uint32_t>((bytes + 15) & ~static_cast<size_t>(15));
     return at;
   };
-  L.slab = take(static_cast<size_t>(gamma) * K * K * sizeof(float));
-  L.rmax = take(static_cast<size_t>(gamma) * K * sizeof(float));
+  // K = 64: the slabs (gamma K^2 floats) do not fit; slab rows are read from memory.
+  const bool in_lds = K <= 16;
+  L.slab = take(in_lds ? static_cast<size_t>(gamma) * K * K * sizeof(float) : 0);
+  L.rmax = take(in_lds ? static_cast<size_t>(gamma) * K * sizeof(float) : 0);
   L.cids = take(static_cast<size_t>(gamma) * K * sizeof(int32_t));
   L.xpose = take(kFastMaxWK * sizeof(float));
   L.stage = take(kStageCap * sizeof(uint2));
@@ -66,7 +68,8 @@ __host__ __device__ inline FastLayout fast_layout(int gamma, int K, int W) {
 }
 
 __host__ __device__ inline bool fast_tree_fits(int gamma, int K, int W) {
-  return (K == 4 || K == 8 || K == 16) && W <= kFastMaxW && W * K <= kFastMaxWK && gamma * W <= kFastMaxGW;
+  const bool shape = ((K == 4 || K == 8 || K == 16) && W * K <= 512) || (K == 64 && W * K <= kFastMaxWK);
+  return shape && W <= kFastMaxW && gamma * W <= kFastMaxGW;
 }
 
 // Selects the `need` best live entries under (key desc, index asc), where entry (r, lane)
@@ -184,6 +187,28 @@ __device__ __forceinline__ int rank_in_stage(const uint2* stage, int n, uint64_t
   return rank;
 }
 
+// A slab row from memory (K = 64: the slabs stay in memory), with its maximum.
+template <int KT>
+__device__ __forceinline__ float load_row_global(const float* row, bool vec, float (&v)[KT]) {
+  if (vec) {
+#pragma unroll
+    for (int i = 0; i < KT / 4; ++i) {
+      const float4 t = reinterpret_cast<const float4*>(row)[i];
+      v[4 * i] = t.x;
+      v[4 * i + 1] = t.y;
+      v[4 * i + 2] = t.z;
+      v[4 * i + 3] = t.w;
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < KT; ++i) v[i] = row[i];
+  }
+  float m = v[0];
+#pragma unroll
+  for (int i = 1; i < KT; ++i) m = fmaxf(m, v[i]);
+  return m;
+}
+
 template <int KT>
 __device__ __forceinline__ void load_row(const float* row, float (&v)[KT]) {
 #pragma unroll
@@ -279,16 +304,24 @@ __device__ __forceinline__ void wait_slab(uint32_t* ready, int i) {
 template <int KT, int R, bool kWait>
 __device__ __forceinline__ void expand_depths(const TreeArgs& a, const FastSmem& sm, int64_t b, int lane,
                                               int& total) {
-  constexpr int kLogK = KT == 4 ? 2 : (KT == 8 ? 3 : 4);
+  constexpr int kLogK = KT == 4 ? 2 : (KT == 8 ? 3 : (KT == 16 ? 4 : 6));
+  constexpr bool kMemSlab = KT > 16;  // slab rows come from logq in memory
   const int gamma = a.gamma, W = a.W;
+  const float* gq = a.logq + b * gamma * KT * KT;
+  const bool vec = (reinterpret_cast<uintptr_t>(a.logq) & 15u) == 0;
   // Frontier entry on lane j < np: score key, position in F, and its slab row for the
   // next depth (prefetched as soon as the entry's candidate rank is known).
   uint32_t fkey = f32_key(0.f);
   int fpos = 0;
   float nq[KT];
-  if (kWait) wait_slab(sm.ready, 0);
-  load_row<KT>(sm.slab, nq);  // depth 1 extends the root through row 0
-  float rm = sm.rmax[0];
+  float rm;
+  if (kMemSlab) {
+    rm = load_row_global<KT>(gq, vec, nq);  // depth 1 extends the root through row 0
+  } else {
+    if (kWait) wait_slab(sm.ready, 0);
+    load_row<KT>(sm.slab, nq);  // depth 1 extends the root through row 0
+    rm = sm.rmax[0];
+  }
   int np = 1;
   total = 0;
   const float zeta = a.zeta;
@@ -340,9 +373,13 @@ __device__ __forceinline__ void expand_depths(const TreeArgs& a, const FastSmem&
     const int p = e >> kLogK;
     const int c = e & (KT - 1);
     if (d < gamma) {
-      if (kWait) wait_slab(sm.ready, d);
-      load_row<KT>(sm.slab + (d * KT + c) * KT, nq);
-      rm = sm.rmax[d * KT + c];
+      if (kMemSlab) {
+        rm = load_row_global<KT>(gq + (d * KT + c) * KT, vec, nq);
+      } else {
+        if (kWait) wait_slab(sm.ready, d);
+        load_row<KT>(sm.slab + (d * KT + c) * KT, nq);
+        rm = sm.rmax[d * KT + c];
+      }
     }
     const int rank = rank_in_stage(sm.stage, w_d, order_value(mx, my));
     const int fb = (d - 1) * W;

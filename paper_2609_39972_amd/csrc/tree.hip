@@ -332,22 +332,25 @@ __global__ __launch_bounds__(kWave) void build_tree_fast_kernel(TreeArgs a, uint
   const int64_t b = blockIdx.x;
   const int gamma = a.gamma;
   const FastSmem sm = fast_smem(smem_raw, fast_layout(gamma, KT, a.W));
-  // Stage this sequence's score slabs and candidate ids.
-  const int ns = gamma * KT * KT;
-  const float* gslab = a.logq + b * ns;
-  if ((reinterpret_cast<uintptr_t>(gslab) & 15u) == 0) {
-    const float4* src = reinterpret_cast<const float4*>(gslab);
-    float4* dst = reinterpret_cast<float4*>(sm.slab);
+  // Stage this sequence's score slabs (K <= 16; at K = 64 the search reads the rows it
+  // needs from memory) and candidate ids.
+  if (KT <= 16) {
+    const int ns = gamma * KT * KT;
+    const float* gslab = a.logq + b * ns;
+    if ((reinterpret_cast<uintptr_t>(gslab) & 15u) == 0) {
+      const float4* src = reinterpret_cast<const float4*>(gslab);
+      float4* dst = reinterpret_cast<float4*>(sm.slab);
 #pragma unroll 4
-    for (int e = lane; e < ns / 4; e += kWave) dst[e] = src[e];
-  } else {
+      for (int e = lane; e < ns / 4; e += kWave) dst[e] = src[e];
+    } else {
 #pragma unroll 4
-    for (int e = lane; e < ns; e += kWave) sm.slab[e] = gslab[e];
+      for (int e = lane; e < ns; e += kWave) sm.slab[e] = gslab[e];
+    }
   }
   const int32_t* gids = a.cand_ids + b * gamma * KT;
   for (int e = lane; e < gamma * KT; e += kWave) sm.cids[e] = gids[e];
   __syncthreads();
-  slab_row_max<KT>(sm.slab, sm.rmax, lane, gamma * KT, kWave);
+  if (KT <= 16) slab_row_max<KT>(sm.slab, sm.rmax, lane, gamma * KT, kWave);
   __syncthreads();
   fast_search<KT, R, false>(a, sm, b, lane, magic_w);
 }
@@ -450,12 +453,19 @@ hipError_t launch_build_tree(const TreeArgs& a, hipStream_t stream) {
     else                        \
       UBT_FAST_LAUNCH(KK, 8);   \
   } while (0)
-    if (a.K == 4)
+    if (a.K == 4) {
       UBT_FAST_ROWS(4);
-    else if (a.K == 8)
+    } else if (a.K == 8) {
       UBT_FAST_ROWS(8);
-    else
+    } else if (a.K == 16) {
       UBT_FAST_ROWS(16);
+    } else if (wk <= 512) {
+      UBT_FAST_ROWS(64);
+    } else if (wk <= 768) {
+      UBT_FAST_LAUNCH(64, 12);
+    } else {
+      UBT_FAST_LAUNCH(64, 16);
+    }
 #undef UBT_FAST_ROWS
 #undef UBT_FAST_LAUNCH
     return hipGetLastError();
@@ -490,7 +500,7 @@ hipError_t launch_build_tree(const TreeArgs& a, hipStream_t stream) {
 }
 
 bool draft_tree_fused(int feat_dtype, int gamma, int K, int W) {
-  return feat_dtype == 1 && fast_tree_fits(gamma, K, W);
+  return feat_dtype == 1 && K <= 16 && fast_tree_fits(gamma, K, W);
 }
 
 hipError_t launch_draft_tree(const SelectorArgs& s, const TreeArgs& a, hipStream_t stream) {

@@ -54,6 +54,10 @@ def _compare(B, gamma, K, W, budget, zeta=0.0, seed=0, tie_frac=0.0, levels=64):
     # 255 nodes, gamma = 64; and the general search just outside it (K = 13, 17, 7; W = 65)
     (2, 16, 8, 64, 255), (3, 32, 4, 32, 255), (2, 12, 16, 32, 200), (2, 64, 4, 16, 255), (2, 9, 16, 24, 200),
     (2, 20, 13, 30, 150), (2, 6, 7, 9, 40), (2, 10, 17, 12, 64), (2, 6, 4, 65, 100), (2, 64, 2, 16, 255),
+    # K = 64 in the register-resident search (slab rows read from memory): W*K = 1024, 768 (the paper's
+    # W = 12), 512, 64; gamma*W at its limit; and W = 17 just outside (general search)
+    (2, 15, 64, 16, 255), (4, 15, 64, 12, 64), (2, 40, 64, 8, 200), (3, 7, 64, 1, 7), (2, 64, 64, 16, 255),
+    (2, 5, 64, 17, 80),
 ])
 def test_dyadic_exact(B, gamma, K, W, budget):
     _compare(B, gamma, K, W, budget, seed=B + gamma + K)
@@ -70,6 +74,7 @@ def test_exact_ties(tie_frac, levels):
     _compare(2, 6, 16, 20, 100, seed=8, tie_frac=tie_frac, levels=levels)
     _compare(2, 20, 8, 12, 200, seed=9, tie_frac=tie_frac, levels=levels)
     _compare(4, 15, 8, 12, 64, seed=10, tie_frac=tie_frac, levels=levels)
+    _compare(2, 15, 64, 12, 64, seed=11, tie_frac=tie_frac, levels=levels)
 
 
 @pytest.mark.parametrize("zeta", [-0.125, -1.0, -1000.0])
