@@ -266,28 +266,32 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attention_kernel(AttnArgs p
         vis[j] = ((bits >> (4 * kg)) & 0xFu) | (((bits >> (16 + 4 * kg)) & 0xFu) << 4);
       }
     }
-    float sc[TW][8];
+    // Fully visible blocks use the scores as they are; only partial blocks mask: the
+    // maximum over visible scores, and a zero weight for each invisible key.
     bool grow = false;
+    float mxs[TW];
 #pragma unroll
     for (int j = 0; j < TW; ++j) {
+      float mx;
+      if (full) {
+        mx = fmaxf(fmaxf(fmaxf(s0[j][0], s0[j][1]), fmaxf(s0[j][2], s0[j][3])),
+                   fmaxf(fmaxf(s1[j][0], s1[j][1]), fmaxf(s1[j][2], s1[j][3])));
+      } else {
+        mx = neg_inf();
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        sc[j][e] = ((vis[j] >> e) & 1u) ? s0[j][e] : neg_inf();
-        sc[j][4 + e] = ((vis[j] >> (4 + e)) & 1u) ? s1[j][e] : neg_inf();
+        for (int e = 0; e < 4; ++e) {
+          mx = ((vis[j] >> e) & 1u) ? fmaxf(mx, s0[j][e]) : mx;
+          mx = ((vis[j] >> (4 + e)) & 1u) ? fmaxf(mx, s1[j][e]) : mx;
+        }
       }
-      float mx = sc[j][0];
-#pragma unroll
-      for (int e = 1; e < 8; ++e) mx = fmaxf(mx, sc[j][e]);
-      grow = grow || (mx * c > m_run[j] + kRescaleGap);
+      mxs[j] = mx * c;
+      grow = grow || (mxs[j] > m_run[j] + kRescaleGap);
     }
     if (ballot(grow)) {
       // Raise the running maxima that fell behind (uniform over each query's 4 lanes).
 #pragma unroll
       for (int j = 0; j < TW; ++j) {
-        float mx = sc[j][0];
-#pragma unroll
-        for (int e = 1; e < 8; ++e) mx = fmaxf(mx, sc[j][e]);
-        mx *= c;
+        float mx = mxs[j];
         mx = fmaxf(mx, __shfl_xor(mx, 16));
         mx = fmaxf(mx, __shfl_xor(mx, 32));
         if (mx > m_run[j] + kRescaleGap) {
@@ -302,14 +306,20 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attention_kernel(AttnArgs p
     v4u pt[TW];
 #pragma unroll
     for (int j = 0; j < TW; ++j) {
-      float pr[8];
-      // m_run is finite wherever a key is visible (the first visible score raised it).
+      // A stored row sees a visible key in its first block, so m_run is finite there; rows
+      // never stored may turn NaN, which stays in their own column.
       const float nm = -m_run[j];
+      float pr[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        pr[e] = ((vis[j] >> e) & 1u) ? __builtin_amdgcn_exp2f(fmaf(sc[j][e], c, nm)) : 0.f;
-        l_part[j] += pr[e];
+      for (int e = 0; e < 4; ++e) {
+        pr[e] = __builtin_amdgcn_exp2f(fmaf(s0[j][e], c, nm));
+        pr[4 + e] = __builtin_amdgcn_exp2f(fmaf(s1[j][e], c, nm));
       }
+      if (!full) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) pr[e] = ((vis[j] >> e) & 1u) ? pr[e] : 0.f;
+      }
+      l_part[j] += ((pr[0] + pr[1]) + (pr[2] + pr[3])) + ((pr[4] + pr[5]) + (pr[6] + pr[7]));
       pt[j] = v4u{pack_bf16(pr[0], pr[1]), pack_bf16(pr[2], pr[3]), pack_bf16(pr[4], pr[5]),
                   pack_bf16(pr[6], pr[7])};
     }
@@ -342,12 +352,13 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attention_kernel(AttnArgs p
     if (p.out_f32) {
       float* op = static_cast<float*>(p.out) + orow * D;
 #pragma unroll
-      for (int i = 0; i < DT; ++i) *reinterpret_cast<v4f*>(op + 16 * i + 4 * kg) = o[j][i] * inv;
+      for (int i = 0; i < DT; ++i)
+        *reinterpret_cast<v4f*>(op + 16 * i + 4 * kg) = has ? o[j][i] * inv : v4f{0.f, 0.f, 0.f, 0.f};
     } else {
       uint16_t* op = static_cast<uint16_t*>(p.out) + orow * D;
 #pragma unroll
       for (int i = 0; i < DT; ++i) {
-        const v4f v = o[j][i] * inv;
+        const v4f v = has ? o[j][i] * inv : v4f{0.f, 0.f, 0.f, 0.f};
         *reinterpret_cast<v2u*>(op + 16 * i + 4 * kg) = v2u{pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3])};
       }
     }
