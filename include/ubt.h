@@ -209,21 +209,21 @@ ubt_status_t ubt_draft_tree(const void* phi_tab, const void* psi_tab, const void
  * order).
  *
  * When the rows are 16-byte aligned, the features are bf16, B <= 64, B is below the
- * device's compute-unit count, gamma >= 2, and the search shape is one ubt_draft_tree
- * handles in one launch, the step is TWO kernel launches: the first sweeps draft
- * positions 0..d1-1 of every sequence (d1 about gamma / 2); the second sweeps the
- * remaining positions while one workgroup per sequence computes the score slabs and
- * runs the search, taking each remaining position as soon as its row is out.  That
- * second launch needs `workspace`: device memory of at least
- * ubt_draft_step_workspace_bytes(B, gamma, V, K, dt) bytes (256 + 4 * B * gamma),
- * 256-byte aligned, owned by the caller and ZERO-FILLED before its first use.  It holds
- * an error word (the first 4 bytes) and one ready flag per row; each call resets the
- * flags it raised, so one workspace serves any number of consecutive calls on one stream;
- * calls that may overlap need separate workspaces.  The error word becomes nonzero if a
- * wait inside the launch timed out (1 s; outputs are then unspecified and the workspace
- * must be zero-filled again); this never happens in normal operation.  A missing, short
- * or misaligned workspace returns UBT_ERR_WORKSPACE.  Other shapes run the two calls'
- * kernels in order on `stream` and ignore the workspace.
+ * device's compute-unit count, and the search shape is one ubt_draft_tree handles in one
+ * launch, the step is ONE kernel launch: the rows are swept in depth order, each cut
+ * into at most 2 chunks whose LSE and top K are merged per row, while one workgroup per
+ * sequence merges each row as soon as its chunks are in, computes the score slab and
+ * runs the search.  That launch needs `workspace`: device memory of at least
+ * ubt_draft_step_workspace_bytes(B, gamma, V, K, dt) bytes (about
+ * 256 + B * gamma * (4 + 2 * (8K + 4))), 256-byte aligned, owned by the caller and
+ * ZERO-FILLED before its first use.  It holds an error word (the first 4 bytes), one
+ * chunk counter per row (from byte 256) and the chunks' partial results; each call
+ * resets the counters it raised, so one workspace serves any number of consecutive calls
+ * on one stream; calls that may overlap need separate workspaces.  The error word
+ * becomes nonzero if a wait inside the launch timed out (1 s; outputs are then
+ * unspecified and the workspace must be zero-filled again); this never happens in normal
+ * operation.  A missing, short or misaligned workspace returns UBT_ERR_WORKSPACE.  Other
+ * shapes run the two calls' kernels in order on `stream` and ignore the workspace.
  * ------------------------------------------------------------------------------------ */
 size_t ubt_draft_step_workspace_bytes(int B, int gamma, int64_t V, int K, ubt_dtype_t dt);
 

@@ -14,8 +14,8 @@ Calls, in pipeline order (the paper's section and equation names in brackets):
 * :func:`build_tree` -- beam search with global pruning and the ancestor mask
   [Appendix A, Algorithm 1];
 * :func:`tree_mask` -- the ancestor mask of any parent-pointer tree;
-* :func:`draft_step` -- the whole step in one call (two kernel launches for the common
-  shapes, the search overlapping the second half of the sweep; it needs a zero-filled
+* :func:`draft_step` -- the whole step in one call (one kernel launch for the common
+  shapes: rows swept in depth order while the searchers run; it needs a zero-filled
   workspace from :func:`draft_step_workspace`).
 
 :class:`DraftStep` preallocates everything for one workload shape and runs the step on

@@ -178,9 +178,7 @@ size_t ubt_draft_step_workspace_bytes(int B, int gamma, int64_t V, int K, ubt_dt
   if (B < 1 || gamma < 1 || gamma > UBT_MAX_GAMMA || K < 1 || K > UBT_MAX_K || V < K || V >= (int64_t(1) << 31) ||
       !valid_dtype(dt))
     return 0;
-  (void)V;
-  (void)K;
-  return ubt::step_workspace_bytes(B, gamma);
+  return ubt::step_workspace_bytes(B, gamma, V, K, dt == UBT_BF16 ? 1 : 0);
 }
 
 ubt_status_t ubt_draft_step(const void* logits, ubt_dtype_t dt, int B, int gamma, int64_t V, int64_t stride_b,
@@ -216,7 +214,7 @@ ubt_status_t ubt_draft_step(const void* logits, ubt_dtype_t dt, int B, int gamma
                           stream);
   }
   if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0 ||
-      workspace_bytes < ubt::step_workspace_bytes(B, gamma))
+      workspace_bytes < ubt::step_workspace_bytes(B, gamma, V, K, static_cast<int>(dt)))
     return UBT_ERR_WORKSPACE;
   ubt::SelectorArgs s;
   s.phi = static_cast<const uint16_t*>(phi_tab);

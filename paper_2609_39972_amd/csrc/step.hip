@@ -1,4 +1,4 @@
-// The whole draft step as two launches: softmax statistics and top-K candidates over the
+// The whole draft step in one launch: softmax statistics and top-K candidates over the
 // vocabulary, the selector scores, and the tree search with its ancestor mask.
 //
 // Method / Unigram Proposer, Eq. (ubtree-unigram) and "Candidate Sets" (per-position LSE
@@ -7,26 +7,31 @@
 // Appendix A, Algorithm 1 with Eqs. (ubtree-frontier) and (ubtree-pruning) (the tree);
 // Appendix A / Verification via Tree-attention (the mask).
 //
-// The sweep is bound by HBM bandwidth and the search of one sequence is a long chain of
-// dependent steps on one wave, and the search of depth d needs only the rows of
-// positions up to d.  So the rows are swept in two parts:
-//   * the head launch sweeps positions 0..d1-1 of every sequence, one row per workgroup
-//     of 8 waves, as the top-K kernel does;
-//   * the tail launch sweeps positions d1..gamma-1 the same way while one searcher
-//     workgroup per sequence (the lowest workgroup indices, so they are dispatched
-//     first) computes the score slabs of the head positions and searches them.  A tail
-//     row publishes its candidates with device-coherent stores and a flag; the searcher
-//     takes each tail position as soon as its flag is up, and finishes the search.
-// d1 is about half of gamma, and small enough that the tail's row workgroups and the
-// searchers take at most one compute unit each.  (Measured at B = 32, gamma = 15: d1 = 8
-// beat every other split from 6 to 12, and 8-wave workgroups beat 16-wave ones in both
-// launches.)  Each row's results are those of ubt_topk, and the
-// slabs and the search are the code of ubt_draft_tree, so every output is that of the
-// two separate calls (LSE and log-probs in the same order too).
+// The sweep is bound by HBM bandwidth; the search of one sequence is a long chain of
+// dependent steps on one wave, and its depth d needs only the rows of positions up to d.
+// If every row is swept by its own workgroup, all rows finish together near the end of
+// the sweep and the search can only start then.  Here the rows are swept in depth order
+// instead, each row cut into C chunks of whole tiles, so the early positions come out
+// first and the search runs while the later ones are swept:
+//   * workgroups 0..B-1 are the searchers, one per sequence (the lowest indices, so they
+//     are dispatched first).  Their helper waves merge a row's C chunk results into its
+//     LSE and sorted top K as soon as the last chunk is in, compute that position's score
+//     slab, and publish it to wave 0, which runs the search;
+//   * workgroup B + t sweeps work item t: chunk t % C of sequence (t / C) % B at position
+//     t / (B C).  Workgroups are dispatched in index order as earlier ones retire, so the
+//     items run depth-major with a window of resident items (two workgroups per compute
+//     unit: at B = 32, C = 2 about eight positions in flight, the first rows ready after
+//     about 12 of 31 us of sweep).  An item runs the one-row sweep on its chunk, writes the chunk's
+//     LSE and top K (ids relative to the chunk) with device-coherent stores, waits for
+//     them to complete, and adds 1 to the row's counter.
+// The merge of the chunks is exact for the candidates (a selection on the same order
+// values) and sums the chunks' exponentials in chunk order, so the candidates, the slabs
+// and the tree are those of ubt_topk followed by ubt_draft_tree, and LSE and log-probs
+// agree with them to fp32 rounding.
 //
-// Row workers never wait; searcher waves wait only on flags that tail rows of the same
-// launch set unconditionally, each wait bounded in time.  The flags are reset by the
-// searcher that read them, leaving the workspace ready for the next call.
+// Sweep workgroups never wait.  Searcher waves wait only on counters that sweep
+// workgroups of the same launch raise unconditionally, each wait bounded in time; the
+// searcher that read a counter resets it, leaving the workspace ready for the next call.
 #include "bigram_tile.h"
 #include "search.h"
 #include "sweep.h"
@@ -35,9 +40,14 @@
 namespace ubt {
 namespace {
 
-constexpr int kRowWaves = kWaves;  // waves per workgroup of both launches (8)
+// Waves per workgroup, and chunks per row (C K <= 64 as well).  Measured at B = 32,
+// gamma = 15, V = 151936, K = 8: C = 2 gave 45.4 us per call; C = 1 50.7 us (every row
+// finishes near the end of the sweep), C = 4 53 us and C = 8 75 us (each item is too
+// short to cover its own load latency and merge); 4-wave workgroups with C = 4 48.8 us.
+constexpr int kPipeWaves = 8;
+constexpr int kPipeMaxChunks = 2;
 constexpr uint64_t kWaitTicks = 100000000ull;  // 1 s of the 100 MHz real-time counter
-constexpr uint32_t kFlagBase = 256;            // byte offset of the row flags in the workspace
+constexpr uint32_t kCountBase = 256;           // byte offset of the row counters in the workspace
 
 __device__ __forceinline__ void store_agent32(uint32_t* p, uint32_t v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -52,48 +62,58 @@ __device__ __forceinline__ void wait_all_memory() {
   __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
-struct RowArgs {
+struct PipeArgs {
   const void* logits;
   int64_t V, stride_b, stride_i;
   int B, gamma, K;
-  int d1;  // positions 0..d1-1 belong to the head launch
+  int chunks;         // C: chunks per row
+  int64_t chunk_len;  // elements per chunk, a whole number of tiles; the last chunk is shorter
   int32_t* cand_ids;
   float* cand_logit;
   float* cand_logprob;
   float* lse;
-  uint32_t* err;   // set when a searcher wait timed out
-  uint32_t* flag;  // [B * gamma] 1 once a tail row's candidates are out
+  uint32_t* err;      // set when a searcher wait timed out
+  uint32_t* count;    // [B * gamma] chunks of the row whose results are out
+  int32_t* part_ids;  // [B * gamma * C * K] chunk top K, ids relative to the chunk
+  float* part_logit;  // [B * gamma * C * K]
+  float* part_lse;    // [B * gamma * C] chunk LSE
 };
 
-// Sweeps output row (b, i) with the workgroup's kRowWaves waves.
-template <typename T, bool kCoherent>
-__device__ __forceinline__ void sweep_one(const RowArgs& p, RowLdsT<kRowWaves>& lds, int b, int i) {
-  const int64_t orow = static_cast<int64_t>(b) * p.gamma + i;
-  const T* rp = static_cast<const T*>(p.logits) + b * p.stride_b + i * p.stride_i;
-  sweep_row<T, true, kRowWaves>(lds, rp, p.V, p.K, orow,
-                                RowOut{p.cand_ids, p.cand_logit, p.cand_logprob, p.lse, kCoherent});
-}
-
-// Head launch: positions 0..d1-1 of every sequence, one row per workgroup.
+// Sweeps work item t (depth-major: position, then sequence, then chunk).
 template <typename T>
-__global__ __launch_bounds__(kRowWaves* kWave, 4) void head_rows_kernel(RowArgs p) {
-  __shared__ RowLdsT<kRowWaves> lds;
-  const int r = static_cast<int>(blockIdx.x);
-  sweep_one<T, false>(p, lds, r % p.B, r / p.B);
+__device__ __forceinline__ void pipe_worker(const PipeArgs& p, RowLdsT<kPipeWaves>& lds, int t) {
+  const int w = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) / kWave);
+  const int lane = static_cast<int>(threadIdx.x) % kWave;
+  const int per_depth = p.B * p.chunks;
+  const int i = t / per_depth;
+  const int rem = t - i * per_depth;
+  const int b = rem / p.chunks, c = rem - b * p.chunks;
+  const int64_t row = static_cast<int64_t>(b) * p.gamma + i;
+  const int64_t c0 = static_cast<int64_t>(c) * p.chunk_len;
+  const int64_t len = p.V - c0 < p.chunk_len ? p.V - c0 : p.chunk_len;
+  const T* rp = static_cast<const T*>(p.logits) + b * p.stride_b + i * p.stride_i + c0;
+  sweep_row<T, true, kPipeWaves>(lds, rp, len, p.K, row * p.chunks + c,
+                                 RowOut{p.part_ids, p.part_logit, nullptr, p.part_lse, true});
+  // Wave 0 wrote the chunk's results (device-coherent stores); once they have completed,
+  // the row's counter goes up.
+  if (w == 0) {
+    wait_all_memory();
+    if (lane == 0) __hip_atomic_fetch_add(&p.count[row], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
 }
 
-// Spins until *f is set; false if the wait ran out of time.
-__device__ __forceinline__ bool wait_flag(const uint32_t* f, uint64_t t0) {
+// Spins until *f reaches n; false if the wait ran out of time.
+__device__ __forceinline__ bool wait_count(const uint32_t* f, uint32_t n, uint64_t t0) {
   for (;;) {
-    if (__builtin_amdgcn_readfirstlane(load_agent32(f)) != 0u) return true;
+    if (__builtin_amdgcn_readfirstlane(load_agent32(f)) >= n) return true;
     if (__builtin_amdgcn_s_memrealtime() - t0 > kWaitTicks) return false;
-    __builtin_amdgcn_s_sleep(4);
+    __builtin_amdgcn_s_sleep(2);
   }
 }
 
 struct SearcherLayout {
   FastLayout fast;
-  uint32_t clogit, rready, total;
+  uint32_t clogit, rready, mstage, total;
 };
 
 __host__ __device__ inline SearcherLayout searcher_layout(int gamma, int K, int W) {
@@ -104,29 +124,79 @@ __host__ __device__ inline SearcherLayout searcher_layout(int gamma, int K, int 
   q += static_cast<uint32_t>((gamma * K * sizeof(float) + 15) & ~static_cast<size_t>(15));
   L.rready = q;
   q += static_cast<uint32_t>((gamma * sizeof(uint32_t) + 15) & ~static_cast<size_t>(15));
+  L.mstage = q;  // one 64-entry order-value stage per wave
+  q += static_cast<uint32_t>(kPipeWaves * kWave * sizeof(uint64_t));
   L.total = q;
   return L;
 }
 
-// One sequence's selector slabs and tree search.  Wave 0 searches; waves 1.. take the
-// positions round-robin: they bring the position's candidates into LDS (a head row from
-// memory written by the head launch; a tail row once its flag is up, with device-coherent
-// loads), compute its slab once the predecessor position's candidates are in, and
-// publish it to the search wave.
-template <int KT, int R>
-__device__ __forceinline__ void searcher(const RowArgs& p, const TreeArgs& a, const SelectorArgs& s, uint64_t magic_w,
-                                         unsigned char* smem, int w, int nw, int lane) {
+// Merges the C chunk results of row (b, i) into the row's LSE and sorted top K: lane
+// e < C K holds entry e % K of chunk e / K, ranked among all of them by order value (key
+// desc, id asc).  Writes the caller's outputs and the candidates into LDS.
+template <typename T, int KT>
+__device__ __forceinline__ void merge_chunks(const PipeArgs& p, int64_t row, int i, uint64_t* stage, int32_t* cids,
+                                             float* clogit, int lane) {
+  const int C = p.chunks;
+  uint64_t mine = 0;
+  int32_t id = 0;
+  float v = 0.f;
+  if (lane < C * KT) {
+    const int c = lane / KT, e = lane - c * KT;
+    const int64_t c0 = static_cast<int64_t>(c) * p.chunk_len;
+    const int64_t len = p.V - c0 < p.chunk_len ? p.V - c0 : p.chunk_len;
+    if (e < len) {
+      const int64_t o = (row * C + c) * KT + e;
+      id = static_cast<int32_t>(load_agent32(reinterpret_cast<const uint32_t*>(p.part_ids) + o) + c0);
+      v = __uint_as_float(load_agent32(reinterpret_cast<const uint32_t*>(p.part_logit) + o));
+      mine = cand_order(Traits<T>::key_value(v), static_cast<uint32_t>(id));
+    }
+  }
+  float l = neg_inf();
+  if (lane < C) l = __uint_as_float(load_agent32(reinterpret_cast<const uint32_t*>(p.part_lse) + row * C + lane));
+  stage[lane] = mine;
+  __builtin_amdgcn_wave_barrier();
+  const int r = mine != 0 ? count_above(stage, C * KT, mine) : kWave;
+  __builtin_amdgcn_wave_barrier();
+  // LSE over the chunks, summed in chunk order.
+  float m = neg_inf();
+  for (int c = 0; c < C; ++c) m = fmaxf(m, __shfl(l, c));
+  float e = 0.f;
+  for (int c = 0; c < C; ++c) {
+    const float lc = __shfl(l, c);
+    if (lc != neg_inf()) e += fast_exp2((lc - m) * kLog2e);
+  }
+  const float lse = (m == neg_inf()) ? neg_inf() : m + fast_log2(e) * kLn2;
+  if (r < KT) {
+    const int64_t o = row * KT + r;
+    cids[i * KT + r] = id;
+    clogit[i * KT + r] = v;
+    p.cand_ids[o] = id;
+    p.cand_logit[o] = v;
+    if (p.cand_logprob) p.cand_logprob[o] = v - lse;
+  }
+  if (lane == 0 && p.lse) p.lse[row] = lse;
+}
+
+// One sequence's merges, selector slabs and tree search.  Wave 0 searches; waves 1..
+// take the positions round-robin: they wait for the position's chunks, merge them,
+// compute the slab once the predecessor position's candidates are in, and publish it to
+// the search wave.
+template <typename T, int KT, int R>
+__device__ __forceinline__ void searcher(const PipeArgs& p, const TreeArgs& a, const SelectorArgs& s,
+                                         uint64_t magic_w, unsigned char* smem, int w, int nw, int lane) {
   const int b = static_cast<int>(blockIdx.x);
   const int gamma = a.gamma;
   const SearcherLayout L = searcher_layout(gamma, KT, a.W);
   const FastSmem sm = fast_smem(smem, L.fast);
   float* clogit = reinterpret_cast<float*>(smem + L.clogit);
   uint32_t* rready = reinterpret_cast<uint32_t*>(smem + L.rready);
+  uint64_t* stage = reinterpret_cast<uint64_t*>(smem + L.mstage) + w * kWave;
   for (int e = static_cast<int>(threadIdx.x); e < gamma; e += static_cast<int>(blockDim.x)) {
     sm.ready[e] = 0u;
     rready[e] = 0u;
   }
   __syncthreads();
+  __builtin_amdgcn_s_setprio(3);
   if (w == 0) {
     fast_search<KT, R, true>(a, sm, b, lane, magic_w);
     return;
@@ -134,21 +204,9 @@ __device__ __forceinline__ void searcher(const RowArgs& p, const TreeArgs& a, co
   const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
   for (int i = w - 1; i < gamma; i += nw - 1) {
     const int64_t bi = static_cast<int64_t>(b) * gamma + i;
-    if (i < p.d1) {
-      if (lane < KT) {
-        sm.cids[i * KT + lane] = p.cand_ids[bi * KT + lane];
-        clogit[i * KT + lane] = p.cand_logit[bi * KT + lane];
-      }
-    } else {
-      if (!wait_flag(&p.flag[bi], t0) && lane == 0) store_agent32(p.err, 1u);
-      if (lane < KT) {
-        sm.cids[i * KT + lane] = static_cast<int32_t>(load_agent32(reinterpret_cast<const uint32_t*>(p.cand_ids) +
-                                                                   bi * KT + lane));
-        clogit[i * KT + lane] =
-            __uint_as_float(load_agent32(reinterpret_cast<const uint32_t*>(p.cand_logit) + bi * KT + lane));
-      }
-      if (lane == 0) store_agent32(&p.flag[bi], 0u);  // read: ready for the next call
-    }
+    if (!wait_count(&p.count[bi], static_cast<uint32_t>(p.chunks), t0) && lane == 0) store_agent32(p.err, 1u);
+    merge_chunks<T, KT>(p, bi, i, stage, sm.cids, clogit, lane);
+    if (lane == 0) store_agent32(&p.count[bi], 0u);  // read: ready for the next call
     publish_slab(rready, i);
     if (i > 0) wait_slab(rready, i - 1);
     float* slab = sm.slab + i * KT * KT;
@@ -163,28 +221,19 @@ __device__ __forceinline__ void searcher(const RowArgs& p, const TreeArgs& a, co
   }
 }
 
-// Tail launch: workgroups 0..B-1 search; the others sweep positions d1..gamma-1
-// (depth-major) and raise each row's flag once its candidates have completed.
+// Workgroups 0..B-1 search; workgroup B + t sweeps work item t.
 template <typename T, int KT, int R>
-__global__ __launch_bounds__(kRowWaves* kWave, 4) void draft_tail_kernel(RowArgs p, TreeArgs a, SelectorArgs s,
-                                                                          uint64_t magic_w) {
+__global__ __launch_bounds__(kPipeWaves* kWave, 4) void draft_pipe_kernel(PipeArgs p, TreeArgs a, SelectorArgs s,
+                                                                           uint64_t magic_w) {
   extern __shared__ __align__(16) unsigned char smem_raw[];
   const int w = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) / kWave);
   const int lane = static_cast<int>(threadIdx.x) % kWave;
   const int nw = static_cast<int>(blockDim.x) / kWave;
   if (static_cast<int>(blockIdx.x) < p.B) {
-    searcher<KT, R>(p, a, s, magic_w, smem_raw, w, nw, lane);
+    searcher<T, KT, R>(p, a, s, magic_w, smem_raw, w, nw, lane);
     return;
   }
-  const int r = static_cast<int>(blockIdx.x) - p.B;
-  const int b = r % p.B, i = p.d1 + r / p.B;
-  sweep_one<T, true>(p, *reinterpret_cast<RowLdsT<kRowWaves>*>(smem_raw), b, i);
-  // Wave 0 wrote the row's results (device-coherent stores); once they have completed,
-  // the flag goes up.
-  if (w == 0) {
-    wait_all_memory();
-    if (lane == 0) store_agent32(&p.flag[static_cast<int64_t>(b) * p.gamma + i], 1u);
-  }
+  pipe_worker<T>(p, *reinterpret_cast<RowLdsT<kPipeWaves>*>(smem_raw), static_cast<int>(blockIdx.x) - p.B);
 }
 
 int compute_units() {
@@ -194,23 +243,43 @@ int compute_units() {
   return cus;
 }
 
+// Chunks per row and elements per chunk: at most kPipeMaxChunks chunks with C K <= 64, each a
+// whole number of tiles; no chunk is empty.
+void pipe_chunks(int64_t V, int K, int dtype, int& C, int64_t& len) {
+  const int64_t tile = static_cast<int64_t>(kSubGroups) * kWave * (dtype == 1 ? 8 : 4);
+  const int64_t tiles = (V + tile - 1) / tile;
+  int c = kPipeMaxChunks;
+  while (c > 1 && c * K > kWave) --c;
+  if (c > tiles) c = static_cast<int>(tiles);
+  len = (tiles + c - 1) / c * tile;
+  C = static_cast<int>((V + len - 1) / len);
+}
+
+size_t align256(size_t n) { return (n + 255) & ~static_cast<size_t>(255); }
+
+struct PipeWorkspace {
+  size_t count, part_ids, part_logit, part_lse, total;
+};
+
+PipeWorkspace pipe_workspace(int B, int gamma, int64_t V, int K, int dtype) {
+  int C = 1;
+  int64_t len = 0;
+  pipe_chunks(V, K, dtype, C, len);
+  const size_t rows = static_cast<size_t>(B) * gamma;
+  PipeWorkspace w{};
+  w.count = kCountBase;
+  w.part_ids = w.count + align256(rows * sizeof(uint32_t));
+  w.part_logit = w.part_ids + align256(rows * C * K * sizeof(int32_t));
+  w.part_lse = w.part_logit + align256(rows * C * K * sizeof(float));
+  w.total = w.part_lse + align256(rows * C * sizeof(float));
+  return w;
+}
+
 }  // namespace
 
 // ---- host side ------------------------------------------------------------------------------
-size_t step_workspace_bytes(int B, int gamma) {
-  return kFlagBase + static_cast<size_t>(B) * gamma * sizeof(uint32_t);
-}
-
-// Positions 0..d1-1 go to the head launch: at least half of them, and few enough that
-// the tail's rows and the searchers take at most one workgroup per compute unit.  0 if no
-// such split exists.
-int step_split(int B, int gamma) {
-  const int cus = compute_units();
-  if (gamma < 2 || cus <= 0 || B >= cus) return 0;
-  int d1 = (gamma + 1) / 2;
-  const int tail_max = (cus - B) / B;  // tail positions that fit beside the searchers
-  if (gamma - d1 > tail_max) d1 = gamma - tail_max;
-  return d1 < gamma ? d1 : 0;
+size_t step_workspace_bytes(int B, int gamma, int64_t V, int K, int dtype) {
+  return pipe_workspace(B, gamma, V, K, dtype).total;
 }
 
 bool draft_step_fused(int dtype, bool aligned, int B, int gamma, int64_t V, int K, int feat_dtype, int W) {
@@ -218,14 +287,15 @@ bool draft_step_fused(int dtype, bool aligned, int B, int gamma, int64_t V, int 
   if (!draft_tree_fused(feat_dtype, gamma, K, W)) return false;
   (void)dtype;
   (void)V;
-  return step_split(B, gamma) > 0;
+  const int cus = compute_units();
+  return cus > 0 && B < cus;
 }
 
 hipError_t launch_draft_step(const void* logits, int dtype, int B, int gamma, int64_t V, int64_t stride_b,
                              int64_t stride_i, int K, int32_t* cand_ids, float* cand_logit, float* cand_logprob,
                              float* lse, const SelectorArgs& s, const TreeArgs& a, void* workspace,
                              hipStream_t stream) {
-  RowArgs p{};
+  PipeArgs p{};
   p.logits = logits;
   p.V = V;
   p.stride_b = stride_b;
@@ -233,64 +303,61 @@ hipError_t launch_draft_step(const void* logits, int dtype, int B, int gamma, in
   p.B = B;
   p.gamma = gamma;
   p.K = K;
-  p.d1 = step_split(B, gamma);
+  pipe_chunks(V, K, dtype, p.chunks, p.chunk_len);
   p.cand_ids = cand_ids;
   p.cand_logit = cand_logit;
   p.cand_logprob = cand_logprob;
   p.lse = lse;
+  const PipeWorkspace pw = pipe_workspace(B, gamma, V, K, dtype);
   char* ws = static_cast<char*>(workspace);
   p.err = reinterpret_cast<uint32_t*>(ws);
-  p.flag = reinterpret_cast<uint32_t*>(ws + kFlagBase);
-
-  const dim3 block(kRowWaves * kWave);
-  if (dtype == 1)
-    hipLaunchKernelGGL(head_rows_kernel<uint16_t>, dim3(static_cast<unsigned>(B * p.d1)), block, 0, stream, p);
-  else
-    hipLaunchKernelGGL(head_rows_kernel<float>, dim3(static_cast<unsigned>(B * p.d1)), block, 0, stream, p);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  p.count = reinterpret_cast<uint32_t*>(ws + pw.count);
+  p.part_ids = reinterpret_cast<int32_t*>(ws + pw.part_ids);
+  p.part_logit = reinterpret_cast<float*>(ws + pw.part_logit);
+  p.part_lse = reinterpret_cast<float*>(ws + pw.part_lse);
 
   const uint64_t magic_w = (0x100000000ull + a.W - 1) / a.W;
-  const size_t row_smem = sizeof(RowLdsT<kRowWaves>);
+  const size_t row_smem = sizeof(RowLdsT<kPipeWaves>);
   const size_t search_smem = searcher_layout(gamma, K, a.W).total;
   const size_t smem = row_smem > search_smem ? row_smem : search_smem;
-  const dim3 grid(static_cast<unsigned>(B + B * (gamma - p.d1)));
+  const dim3 grid(static_cast<unsigned>(B + B * gamma * p.chunks));
+  const dim3 block(kPipeWaves * kWave);
   const int wk = a.W * K;
-#define UBT_TAIL_LAUNCH(TT, KK, RR)                                                                         \
+#define UBT_PIPE_LAUNCH(TT, KK, RR)                                                                         \
   do {                                                                                                      \
-    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&draft_tail_kernel<TT, KK, RR>),               \
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&draft_pipe_kernel<TT, KK, RR>),               \
                               hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(smem));          \
-    hipLaunchKernelGGL((draft_tail_kernel<TT, KK, RR>), grid, block, smem, stream, p, a, s, magic_w);      \
+    hipLaunchKernelGGL((draft_pipe_kernel<TT, KK, RR>), grid, block, smem, stream, p, a, s, magic_w);      \
   } while (0)
-#define UBT_TAIL_ROWS(TT, KK)       \
+#define UBT_PIPE_ROWS(TT, KK)       \
   do {                              \
     if (wk <= 64)                   \
-      UBT_TAIL_LAUNCH(TT, KK, 1);   \
+      UBT_PIPE_LAUNCH(TT, KK, 1);   \
     else if (wk <= 128)             \
-      UBT_TAIL_LAUNCH(TT, KK, 2);   \
+      UBT_PIPE_LAUNCH(TT, KK, 2);   \
     else if (wk <= 256)             \
-      UBT_TAIL_LAUNCH(TT, KK, 4);   \
+      UBT_PIPE_LAUNCH(TT, KK, 4);   \
     else if (wk <= 384)             \
-      UBT_TAIL_LAUNCH(TT, KK, 6);   \
+      UBT_PIPE_LAUNCH(TT, KK, 6);   \
     else                            \
-      UBT_TAIL_LAUNCH(TT, KK, 8);   \
+      UBT_PIPE_LAUNCH(TT, KK, 8);   \
   } while (0)
-#define UBT_TAIL_K(TT)         \
+#define UBT_PIPE_K(TT)         \
   do {                         \
     if (K == 4)                \
-      UBT_TAIL_ROWS(TT, 4);    \
+      UBT_PIPE_ROWS(TT, 4);    \
     else if (K == 8)           \
-      UBT_TAIL_ROWS(TT, 8);    \
+      UBT_PIPE_ROWS(TT, 8);    \
     else                       \
-      UBT_TAIL_ROWS(TT, 16);   \
+      UBT_PIPE_ROWS(TT, 16);   \
   } while (0)
   if (dtype == 1)
-    UBT_TAIL_K(uint16_t);
+    UBT_PIPE_K(uint16_t);
   else
-    UBT_TAIL_K(float);
-#undef UBT_TAIL_K
-#undef UBT_TAIL_ROWS
-#undef UBT_TAIL_LAUNCH
+    UBT_PIPE_K(float);
+#undef UBT_PIPE_K
+#undef UBT_PIPE_ROWS
+#undef UBT_PIPE_LAUNCH
   return hipGetLastError();
 }
 

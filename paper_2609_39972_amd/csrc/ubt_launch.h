@@ -63,13 +63,14 @@ struct SelectorArgs {
 bool draft_tree_fused(int feat_dtype, int gamma, int K, int W);
 hipError_t launch_draft_tree(const SelectorArgs& s, const TreeArgs& a, hipStream_t stream);
 
-// ---- the whole step: head rows, then tail rows beside the searchers -----------------
+// ---- the whole step: depth-major chunked sweep beside per-sequence searchers ----------
 constexpr int kMaxStepSequences = 64;   // searcher workgroups
-// Workspace bytes of launch_draft_step: an error word and one flag per row.
-size_t step_workspace_bytes(int B, int gamma);
-// True if the two-launch step handles the shape: aligned rows, bf16 features, the
-// register-resident search, B <= kMaxStepSequences, and enough compute units that the
-// searchers and the tail rows fit side by side.
+// Workspace bytes of launch_draft_step: an error word, one chunk counter per row and the
+// chunks' partial results (dtype 1 = bf16 logits, 0 = fp32).
+size_t step_workspace_bytes(int B, int gamma, int64_t V, int K, int dtype);
+// True if the one-launch step handles the shape: aligned rows, bf16 features, the
+// register-resident search, B <= kMaxStepSequences, and fewer sequences than compute
+// units (the searchers and the workers are resident together).
 bool draft_step_fused(int dtype, bool aligned, int B, int gamma, int64_t V, int K, int feat_dtype, int W);
 hipError_t launch_draft_step(const void* logits, int dtype, int B, int gamma, int64_t V, int64_t stride_b,
                              int64_t stride_i, int K, int32_t* cand_ids, float* cand_logit, float* cand_logprob,

@@ -215,3 +215,30 @@ def _kl(**kw):
 ])
 def test_tree_kl_loss_validation(kw, code):
     assert _kl(**kw) == code
+
+
+def _step_ws_expected(B, gamma, V, K, es):
+    """Workspace of the one-launch step: an error word, then 256-byte aligned regions
+    for the row counters, the chunk ids and logits (C K each per row) and the chunk LSEs,
+    with C = min(2, 64 // K, tiles per row) chunks of whole tiles (64 lanes x 64 bytes)."""
+    al = lambda n: (n + 255) // 256 * 256
+    tile = 64 * 64 // es
+    tiles = -(-V // tile)
+    c = min(2, max(1, 64 // K), tiles)
+    length = -(-tiles // c) * tile
+    C = -(-V // length)
+    rows = B * gamma
+    return 256 + al(rows * 4) + 2 * al(rows * C * K * 4) + al(rows * C * 4)
+
+
+@pytest.mark.parametrize("B,gamma,V,K,dt", [
+    (32, 15, 151936, 8, 1), (32, 15, 151936, 16, 1), (1, 7, 32000, 4, 0), (2, 4, 2048, 8, 1), (3, 2, 100, 16, 0),
+    (64, 2, 3000, 4, 1), (2, 4, 8200, 16, 1),
+])
+def test_draft_step_workspace_bytes(B, gamma, V, K, dt):
+    L = ubt.lib()
+    got = L.ubt_draft_step_workspace_bytes(B, gamma, V, K, dt)
+    assert got == _step_ws_expected(B, gamma, V, K, 2 if dt == 1 else 4)
+    assert got >= 256 + 4 * B * gamma
+    assert L.ubt_draft_step_workspace_bytes(0, gamma, V, K, dt) == 0
+    assert L.ubt_draft_step_workspace_bytes(B, gamma, K - 1, K, dt) == 0

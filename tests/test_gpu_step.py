@@ -1,13 +1,14 @@
-"""GPU tests of ubt_draft_step, the whole step in one call (a head launch over the
-first draft positions, then a launch that sweeps the rest beside the searchers).  Its candidates, logq and trees must be bit-identical to ubt_topk
+"""GPU tests of ubt_draft_step, the whole step in one launch (rows swept depth by depth in
+chunks beside per-sequence searchers that merge the chunks and search as the rows come
+out).  Its candidates, logq and trees must be bit-identical to ubt_topk
 followed by the separate selector and search calls (whose parity with the oracle the
 pipeline tests establish); its LSE and log-probs are summed in another order and must
 agree with the oracle within the fp32 score tolerance.  Also: the workspace flags are
 reset and its error word clear after every call, repeated calls on one workspace
 give identical bits, graph replays match eager calls, and the shapes that stress the
 split (ties across many tiles, rows whose top elements sit late in the row, few tiles
-per row, fp32 logits, one position, 64 sequences) and the fallback to the separate
-calls."""
+per row, a last chunk shorter than K, fp32 logits, one position, 64 sequences) and the
+fallback to the separate calls."""
 from __future__ import annotations
 
 import numpy as np
@@ -54,12 +55,12 @@ def _run_both(w: synth.Workload, d: dict, W: int) -> tuple[dict, dict, object]:
 
 
 def _check_workspace(step) -> None:
-    """The error word is clear and every row's ready flag is back to zero."""
+    """The error word is clear and every row's chunk counter is back to zero."""
     B, gamma = step.shape[:2]
     ws = step.workspace.cpu().numpy()
     assert ws.size >= 256 + B * gamma * 4
     assert int(ws[:4].view(np.uint32)[0]) == 0, "a wait inside the launch timed out"
-    assert not ws[256:256 + B * gamma * 4].any(), "row flags were not reset"
+    assert not ws[256:256 + B * gamma * 4].any(), "row counters were not reset"
 
 
 def _same(a: dict, b: dict, logit_dtype: str) -> None:
@@ -177,6 +178,7 @@ def _custom(cfg: int, **kw) -> synth.Workload:
     dict(B=1, L=2, K=16, W=8, budget=40),             # one position
     dict(B=2, L=9, V=5000, K=4, W=3, budget=12),      # 3 tiles per row
     dict(B=2, L=9, V=16384 + 8, K=8),                 # a ragged last tile of 8 elements
+    dict(B=2, L=5, V=8192 + 8, K=16, W=8, budget=40), # a last chunk of 8 elements, fewer than K
     dict(B=64, L=3, V=3000, K=4, W=4, budget=16),     # 64 searchers
     dict(B=2, L=6, V=30000, dtype="f32", feat_dtype="bf16", K=8),  # fp32 logits
     dict(B=2, L=6, V=10000, K=16, W=32, budget=60),   # W * K = 512
