@@ -169,7 +169,9 @@ __device__ __forceinline__ int rank_in_stage(const uint2* stage, int n, uint64_t
   uint4 cur[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i) cur[i] = s4[i];
-  int rank = 0;
+  // Four independent counts: on a lone wave, one running count would make every
+  // compare-and-add wait for the previous one.
+  int acc[4] = {0, 0, 0, 0};
   for (int ch = 0; ch < chunks; ++ch) {
     uint4 nxt[8];
     if (ch + 1 < chunks) {
@@ -178,13 +180,13 @@ __device__ __forceinline__ int rank_in_stage(const uint2* stage, int n, uint64_t
     }
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      rank += order_value(cur[i].x, cur[i].y) > mine ? 1 : 0;
-      rank += order_value(cur[i].z, cur[i].w) > mine ? 1 : 0;
+      acc[i & 3] += order_value(cur[i].x, cur[i].y) > mine ? 1 : 0;
+      acc[i & 3] += order_value(cur[i].z, cur[i].w) > mine ? 1 : 0;
     }
 #pragma unroll
     for (int i = 0; i < 8; ++i) cur[i] = nxt[i];
   }
-  return rank;
+  return (acc[0] + acc[1]) + (acc[2] + acc[3]);
 }
 
 // A slab row from memory (K = 64: the slabs stay in memory), with its maximum.

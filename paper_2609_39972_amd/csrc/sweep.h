@@ -274,16 +274,18 @@ __device__ __forceinline__ uint64_t cand_order(uint32_t key, uint32_t id) {
 }
 // Number of the n order values at v[0..n) (LDS, 16-byte aligned, 64 entries readable)
 // greater than `mine`.  Eight entries per round trip.
+// Four independent counts, so that the compares of one round trip do not wait on each
+// other (a lone wave would otherwise stall on every add).
 __device__ __forceinline__ int count_above(const uint64_t* v, int n, uint64_t mine) {
-  int c = 0;
+  int c[4] = {0, 0, 0, 0};
   for (int j0 = 0; j0 < n; j0 += 8) {
     ulonglong2 p[4];
 #pragma unroll
     for (int q = 0; q < 4; ++q) p[q] = *reinterpret_cast<const ulonglong2*>(v + j0 + 2 * q);
 #pragma unroll
-    for (int q = 0; q < 4; ++q) c += (j0 + 2 * q < n && p[q].x > mine) + (j0 + 2 * q + 1 < n && p[q].y > mine);
+    for (int q = 0; q < 4; ++q) c[q] += (j0 + 2 * q < n && p[q].x > mine) + (j0 + 2 * q + 1 < n && p[q].y > mine);
   }
-  return c;
+  return (c[0] + c[1]) + (c[2] + c[3]);
 }
 // Stages the buffered elements with key >= thr to s.cand (in buffer order); returns how
 // many there are (only the first 64 are staged).
