@@ -180,6 +180,8 @@ def _custom(cfg: int, **kw) -> synth.Workload:
     dict(B=2, L=9, V=16384 + 8, K=8),                 # a ragged last tile of 8 elements
     dict(B=2, L=5, V=8192 + 8, K=16, W=8, budget=40), # a last chunk of 8 elements, fewer than K
     dict(B=64, L=3, V=3000, K=4, W=4, budget=16),     # 64 searchers
+    dict(B=8, L=33, V=6000, K=8, W=8, budget=64),     # 32 positions over 7 helper waves
+    dict(B=2, L=65, V=4000, K=4, W=8, budget=100),    # the longest block (gamma = 64)
     dict(B=2, L=6, V=30000, dtype="f32", feat_dtype="bf16", K=8),  # fp32 logits
     dict(B=2, L=6, V=10000, K=16, W=32, budget=60),   # W * K = 512
     dict(B=2, L=6, V=10000, K=5, W=4, budget=20),     # K outside {4, 8, 16}: the separate calls
