@@ -521,7 +521,9 @@ def main() -> int:
                            "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(step_gbps / HBM_PEAK_GBPS, 4),
                            "traffic": straffic["bytes"] if straffic is not None and args.workload == 3 else None,
                            "algorithmic_bytes_per_launch": step_bytes,
-                           "source_hash": source_hash(STEP_SOURCES)}
+                           "source_hash": source_hash(STEP_SOURCES),
+                           "note": "one launch holds the logit sweep, the selector and the tree search; "
+                                   "the sweep on its own is sweep_alone"}
     else:
         res["roofline"] = {"bound": "hbm", "kernel": SWEEP_KERNEL, "achieved": round(sweep_gbps, 1),
                            "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(sweep_gbps / HBM_PEAK_GBPS, 4),
