@@ -82,21 +82,97 @@ def one_launch_step(w, dev) -> bool:
             and (w.V * (2 if w.dtype == "bf16" else 4)) % 16 == 0)
 
 
-def cpu_baseline(w, d, min_seconds: float) -> dict:
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(w, d, min_seconds: float) -> tuple[dict, dict]:
+    """The fp64 oracle on pool buffer 0: full steps on the host threads for at least
+    `min_seconds`, then one step on one thread.  Returns the baseline and the oracle's
+    outputs of the first step (the parity reference)."""
     import oracle
 
     threads = oracle.default_threads()
-    reps, t0 = 0, time.perf_counter()
+    args = (d["logits"], d["phi"], d["psi"], d["gate"], d["anchor"], d["alpha"], d["lam"], w.K, w.W, w.budget, w.zeta)
+    reps, t0, ref = 0, time.perf_counter(), None
     while True:
-        oracle.pipeline(d["logits"], d["phi"], d["psi"], d["gate"], d["anchor"], d["alpha"], d["lam"], w.K, w.W,
-                        w.budget, w.zeta, threads=threads)
+        out = oracle.pipeline(*args, threads=threads)
+        ref = out if ref is None else ref
         reps += 1
         el = time.perf_counter() - t0
         if el >= min_seconds:
             break
+    t1 = time.perf_counter()
+    oracle.pipeline(*args, threads=1)
+    el1 = time.perf_counter() - t1
     return {"value": round(reps * w.B / el, 3), "unit": "trees/s", "cores": threads, "kind": "oracle",
             "sample": f"{reps} full step(s) of the workload ({reps * w.B} trees, {reps * w.rows} logit rows) on "
-                      f"pool buffer 0, fp64 C++ oracle, {threads} threads, {el:.1f} s"}
+                      f"pool buffer 0, fp64 C++ oracle, {threads} threads, {el:.1f} s",
+            "cpu_model": cpu_model(), "host_cpus": os.cpu_count(),
+            "single_thread": {"value": round(w.B / el1, 3), "unit": "trees/s",
+                              "sample": f"1 full step ({w.B} trees) on 1 thread, {el1:.2f} s"}}, ref
+
+
+EXACT_KEYS = ("cand_ids", "cand_logit", "logq", "n_nodes", "token", "parent", "depth", "cand_rank", "score", "mask")
+
+
+def step_parity(w, d, step, logits, ref) -> dict:
+    """The timed step's outputs for pool buffer 0 (left by the last graph replay) against
+    the oracle's: candidate ids exact, LSE, log-probs and logq within 1e-5 * max(1, |ref|),
+    and each tree exact or within the 1e-5 tie gap.  The guided tie check reads the
+    supertree, which only the separate calls can dump: their outputs on the same logits
+    must first be bit-identical to the timed step's.  Counts trees."""
+    import numpy as np
+    import torch
+
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    import parity
+
+    import paper_2609_39972_amd as ubt
+
+    got = {k: v.detach().cpu().numpy() for k, v in step.outputs().items() if v is not None}
+    got["mask"] = got["mask"].view(np.uint32)
+    B, gamma, V, K, W, budget = step.shape
+    sep = ubt.DraftStep(B, gamma, V, K, W, budget, step.phi, step.psi, step.gate, step.anchor, step.alpha, step.lam,
+                        step.zeta, fused=False, debug=True)
+    dump = {k: v.detach().cpu().numpy() for k, v in sep.run(logits).items() if v is not None}
+    torch.cuda.synchronize()
+    dump["mask"] = dump["mask"].view(np.uint32)
+    same = all(np.array_equal(np.asarray(got[k]).view(np.uint32) if got[k].dtype == np.float32 else got[k],
+                              np.asarray(dump[k]).view(np.uint32) if dump[k].dtype == np.float32 else dump[k])
+               for k in EXACT_KEYS)
+    g = dict(got)
+    for k in ("f_count", "f_parent", "f_cand", "f_score"):
+        g[k] = dump[k]
+    counts = {"exact": 0, "excused": 0, "failed": 0}
+    first_failure = None
+    for b in range(B):
+        try:
+            if not same:
+                raise AssertionError("the timed step's outputs differ from the separate calls'")
+            sub = {k: got[k][b:b + 1] for k in ("cand_ids", "cand_logit", "cand_logprob", "lse")}
+            parity.check_topk(sub, {k: ref[k][b:b + 1] for k in ("cand_ids", "cand_logit", "cand_logprob", "lse")})
+            parity.close(got["logq"][b], ref["logq"][b], "logq")
+            c = parity.check_tree(g, {k: ref[k][b:b + 1] for k in ("n_nodes", "parent", "cand_rank", "token", "mask",
+                                                                  "score")},
+                                  ref["logq"][b:b + 1], ref["cand_ids"][b:b + 1], d["anchor"][b:b + 1], W, budget,
+                                  w.zeta, seqs=[b])
+            counts["exact"] += c["exact"]
+            counts["excused"] += c["excused"]
+        except AssertionError as e:
+            counts["failed"] += 1
+            first_failure = first_failure or f"sequence {b}: {e}"
+    out = {**counts, "trees": B, "sample": f"pool buffer 0 ({B} trees) of the timed step vs the fp64 oracle",
+           "tie_gap": 1e-5}
+    if first_failure:
+        out["first_failure"] = first_failure[:300]
+    return out
 
 
 MFMA_BF16_PEAK_TFLOPS = 2500.0
@@ -477,12 +553,18 @@ def main() -> int:
     if step_us is not None:
         log(f"ubt_draft_step {step_us:.2f} us ({step_bytes / (step_us * 1e-6) / 1e9:.0f} GB/s)")
 
+    # Every one-launch call's bounded waits completed (the workspaces' error words are 0).
+    for _, st in bufs:
+        st.check()
     traffic = measured_traffic()
     cpu = None
+    par = None
     if not args.no_cpu_baseline:
         log("timing the oracle on the host cores ...")
-        cpu = cpu_baseline(w, host0, args.cpu_seconds)
+        cpu, ref = cpu_baseline(w, host0, args.cpu_seconds)
         log(f"oracle: {cpu['value']} trees/s on {cpu['cores']} threads")
+        par = step_parity(w, host0, bufs[0][1], bufs[0][0], ref)
+        log(f"parity of pool buffer 0 vs the oracle: {par}")
 
     value = w.B / (ms_per_step * 1e-3)
     res = {
@@ -510,6 +592,7 @@ def main() -> int:
         "sweep_alone": {"kernel": SWEEP_KERNEL, "us": round(sweep_us, 3), "GB/s": round(sweep_gbps, 1),
                         "frac": round(sweep_gbps / HBM_PEAK_GBPS, 4), "bytes": sweep_bytes},
         "cpu_baseline": cpu,
+        "parity": par,
     }
     # The roofline is that of the dominant kernel: the one-launch step when ubt_draft_step
     # runs as one launch (its algorithmic bytes: logits, selector gathers and writes,
@@ -534,7 +617,7 @@ def main() -> int:
                                  "GB/s": round(step_bytes / (step_us * 1e-6) / 1e9, 1)}
     res = {k: res[k] for k in ("metric", "value", "unit", "n_gpus", "steps", "warmup", "ms_per_step", "us_per_step",
                                "higher_is_better", "scaling", "vs_baseline", "dtype", "data", "config", "kernels_us",
-                               "step_calls", "roofline", "sweep_alone", "step_effective", "cpu_baseline")
+                               "step_calls", "roofline", "sweep_alone", "step_effective", "cpu_baseline", "parity")
            if k in res}
     print(json.dumps(res), flush=True)
     return 0

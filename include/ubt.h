@@ -185,7 +185,10 @@ ubt_status_t ubt_build_tree(const int32_t* anchor, const int32_t* cand_ids, cons
  * With bf16 features, K in {4, 8, 16}, W <= 64, W*K <= 512 and gamma*W <= 1024, one
  * kernel launch computes each sequence's score slabs in on-chip memory and searches
  * them there (logq is still written out).  Other shapes launch the two calls' kernels
- * in order on `stream`.
+ * in order on `stream`.  In the one-launch kernel the search waits for slabs that other
+ * waves of its workgroup compute; each wait is bounded (1 s).  A sequence whose wait ran
+ * out of time (a stalled device; never in normal operation) is written with n_nodes = 0
+ * and its other outputs are unspecified.
  * ------------------------------------------------------------------------------------ */
 ubt_status_t ubt_draft_tree(const void* phi_tab, const void* psi_tab, const void* gate,
                             ubt_dtype_t feat_dt, int64_t V, int r, const int32_t* anchor,
@@ -219,11 +222,15 @@ ubt_status_t ubt_draft_tree(const void* phi_tab, const void* psi_tab, const void
  * ZERO-FILLED before its first use.  It holds an error word (the first 4 bytes), one
  * chunk counter per row (from byte 256) and the chunks' partial results; each call
  * resets the counters it raised, so one workspace serves any number of consecutive calls
- * on one stream; calls that may overlap need separate workspaces.  The error word
- * becomes nonzero if a wait inside the launch timed out (1 s; outputs are then
- * unspecified and the workspace must be zero-filled again); this never happens in normal
- * operation.  A missing, short or misaligned workspace returns UBT_ERR_WORKSPACE.  Other
- * shapes run the two calls' kernels in order on `stream` and ignore the workspace.
+ * on one stream; calls that may overlap need separate workspaces.  A chunk's results are
+ * published by an agent-scope release on its row counter and read after an agent-scope
+ * acquire.  Every wait inside the launch is bounded (1 s).  If one runs out of time (a
+ * stalled device; never in normal operation) the error word becomes nonzero, the
+ * affected sequences are written with n_nodes = 0, the call's outputs are unspecified,
+ * and the workspace must be zero-filled again before the next call (a late chunk may
+ * still raise a counter).  A missing, short or misaligned workspace returns
+ * UBT_ERR_WORKSPACE.  Other shapes run the two calls' kernels in order on `stream` and
+ * ignore the workspace.
  * ------------------------------------------------------------------------------------ */
 size_t ubt_draft_step_workspace_bytes(int B, int gamma, int64_t V, int K, ubt_dtype_t dt);
 

@@ -16,7 +16,8 @@ Calls, in pipeline order (the paper's section and equation names in brackets):
 * :func:`tree_mask` -- the ancestor mask of any parent-pointer tree;
 * :func:`draft_step` -- the whole step in one call (one kernel launch for the common
   shapes: rows swept in depth order while the searchers run; it needs a zero-filled
-  workspace from :func:`draft_step_workspace`).
+  workspace from :func:`draft_step_workspace`, whose error word
+  :func:`draft_step_error` reads).
 
 :class:`DraftStep` preallocates everything for one workload shape and runs the step on
 one stream (graph-capturable).
@@ -275,6 +276,17 @@ def draft_step_workspace(B: int, gamma: int, V: int, K: int, dtype=torch.bfloat1
     return ws
 
 
+class StepTimeout(RuntimeError):
+    """A bounded wait inside a one-launch ``ubt_draft_step`` ran out of time."""
+
+
+def draft_step_error(workspace: torch.Tensor) -> int:
+    """The error word of a :func:`draft_step` workspace (its first 4 bytes; nonzero after
+    a wait inside the launch timed out).  Reads device memory, so it synchronises with the
+    workspace's device."""
+    return int(workspace[:4].cpu().view(torch.int32)[0].item())
+
+
 def draft_step(logits: torch.Tensor, phi: torch.Tensor, psi: torch.Tensor, gate: torch.Tensor, anchor: torch.Tensor,
                alpha, lam, K: int, W: int, budget: int, zeta: float = 0.0, workspace: torch.Tensor | None = None,
                cand: dict | None = None, logq: torch.Tensor | None = None, out: dict | None = None,
@@ -431,6 +443,24 @@ class DraftStep:
         self.one_call = one_call and self.fused
         self.workspace = draft_step_workspace(B, gamma, V, K, logit_dtype, dev) if self.one_call else None
         self.logit_dtype_code = UBT_BF16 if logit_dtype == torch.bfloat16 else UBT_F32
+
+    def outputs(self) -> dict:
+        """The step's output tensors (candidates, selector scores, tree)."""
+        return {**self.cand, **self.sel, **self.tree}
+
+    def check(self) -> None:
+        """Synchronises the device and raises :class:`StepTimeout` if a bounded wait inside
+        an earlier one-launch call ran out of time (the workspace's error word is set; the
+        affected trees carry ``n_nodes == 0``).  The workspace is then zero-filled again, so
+        later calls start clean.  Does nothing for the multi-launch paths."""
+        if self.workspace is None:
+            return
+        torch.cuda.synchronize(self.workspace.device)
+        if draft_step_error(self.workspace):
+            self.workspace.zero_()
+            torch.cuda.synchronize(self.workspace.device)
+            raise StepTimeout("ubt_draft_step: a wait inside the launch timed out; outputs of that call are "
+                              "unspecified (the workspace has been cleared)")
 
     def run(self, logits: torch.Tensor, stream=None) -> dict:
         if self.one_call:

@@ -181,13 +181,19 @@ size_t ubt_draft_step_workspace_bytes(int B, int gamma, int64_t V, int K, ubt_dt
   return ubt::step_workspace_bytes(B, gamma, V, K, dt == UBT_BF16 ? 1 : 0);
 }
 
-ubt_status_t ubt_draft_step(const void* logits, ubt_dtype_t dt, int B, int gamma, int64_t V, int64_t stride_b,
-                            int64_t stride_i, int K, const void* phi_tab, const void* psi_tab, const void* gate,
-                            ubt_dtype_t feat_dt, int r, const int32_t* anchor, const float* alpha,
-                            const float* lambda, int W, int budget, float zeta, int32_t* cand_ids, float* cand_logit,
-                            float* cand_logprob, float* lse, float* logq, int32_t* n_nodes, int32_t* token,
-                            int32_t* parent, int32_t* depth, int32_t* cand_rank, float* score, uint32_t* mask,
-                            void* workspace, size_t workspace_bytes, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+// ubt_draft_step: argument checks, then the one-launch kernel (with the caller's
+// workspace) or the separate kernels.
+ubt_status_t draft_step_impl(const void* logits, ubt_dtype_t dt, int B, int gamma, int64_t V, int64_t stride_b,
+                             int64_t stride_i, int K, const void* phi_tab, const void* psi_tab, const void* gate,
+                             ubt_dtype_t feat_dt, int r, const int32_t* anchor, const float* alpha,
+                             const float* lambda, int W, int budget, float zeta, int32_t* cand_ids, float* cand_logit,
+                             float* cand_logprob, float* lse, float* logq, int32_t* n_nodes, int32_t* token,
+                             int32_t* parent, int32_t* depth, int32_t* cand_rank, float* score, uint32_t* mask,
+                             void* workspace, size_t workspace_bytes, hipStream_t stream) {
   if (!logits || !cand_ids || !cand_logit || !logq) return UBT_ERR_NULL;
   if (!valid_dtype(dt)) return UBT_ERR_VALUE;
   if (B < 1 || gamma < 1 || gamma > UBT_MAX_GAMMA || K < 1 || K > UBT_MAX_K || V < K || V >= (int64_t(1) << 31))
@@ -213,9 +219,10 @@ ubt_status_t ubt_draft_step(const void* logits, ubt_dtype_t dt, int B, int gamma
                           gamma, K, W, budget, zeta, logq, n_nodes, token, parent, depth, cand_rank, score, mask,
                           stream);
   }
-  if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0 ||
-      workspace_bytes < ubt::step_workspace_bytes(B, gamma, V, K, static_cast<int>(dt)))
+  const size_t need = ubt::step_workspace_bytes(B, gamma, V, K, static_cast<int>(dt));
+  if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0 || workspace_bytes < need) {
     return UBT_ERR_WORKSPACE;
+  }
   ubt::SelectorArgs s;
   s.phi = static_cast<const uint16_t*>(phi_tab);
   s.psi = static_cast<const uint16_t*>(psi_tab);
@@ -227,6 +234,22 @@ ubt_status_t ubt_draft_step(const void* logits, ubt_dtype_t dt, int B, int gamma
   s.sc = sc;
   return hip_status(ubt::launch_draft_step(logits, static_cast<int>(dt), B, gamma, V, stride_b, stride_i, K, cand_ids,
                                            cand_logit, cand_logprob, lse, s, a, workspace, stream));
+}
+
+}  // namespace
+
+extern "C" {
+
+ubt_status_t ubt_draft_step(const void* logits, ubt_dtype_t dt, int B, int gamma, int64_t V, int64_t stride_b,
+                            int64_t stride_i, int K, const void* phi_tab, const void* psi_tab, const void* gate,
+                            ubt_dtype_t feat_dt, int r, const int32_t* anchor, const float* alpha,
+                            const float* lambda, int W, int budget, float zeta, int32_t* cand_ids, float* cand_logit,
+                            float* cand_logprob, float* lse, float* logq, int32_t* n_nodes, int32_t* token,
+                            int32_t* parent, int32_t* depth, int32_t* cand_rank, float* score, uint32_t* mask,
+                            void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  return draft_step_impl(logits, dt, B, gamma, V, stride_b, stride_i, K, phi_tab, psi_tab, gate, feat_dt, r, anchor,
+                         alpha, lambda, W, budget, zeta, cand_ids, cand_logit, cand_logprob, lse, logq, n_nodes,
+                         token, parent, depth, cand_rank, score, mask, workspace, workspace_bytes, stream);
 }
 
 ubt_status_t ubt_tree_mask(const int32_t* parent, const int32_t* n_nodes, int B, int N, uint32_t* mask,

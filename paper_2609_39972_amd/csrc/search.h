@@ -39,7 +39,7 @@ constexpr int kStageCap = kStageLive + kWave;  // + one dummy slot per lane
 constexpr int kMaskWords = 8;                  // ceil(256 / 32)
 
 struct FastLayout {
-  uint32_t slab, rmax, cids, xpose, stage, s_key, s_info, f_slot, anc, mk, ready, total;
+  uint32_t slab, rmax, cids, xpose, stage, s_key, s_info, f_slot, anc, mk, ready, fail, total;
 };
 
 __host__ __device__ inline FastLayout fast_layout(int gamma, int K, int W) {
@@ -63,6 +63,7 @@ __host__ __device__ inline FastLayout fast_layout(int gamma, int K, int W) {
   L.anc = take(kMaxNodes * sizeof(int32_t));
   L.mk = take(kMaxNodes * kMaskWords * sizeof(uint32_t));
   L.ready = take(static_cast<size_t>(gamma) * sizeof(uint32_t));
+  L.fail = take(sizeof(uint32_t));
   L.total = p;
   return L;
 }
@@ -234,7 +235,8 @@ struct FastSmem {
   int32_t* f_slot;
   int32_t* anc;
   uint32_t* mk;
-  uint32_t* ready;  // per position: its slab is in LDS (one-launch kernel only)
+  uint32_t* ready;  // per position: its slab is in LDS (one-launch kernels only)
+  uint32_t* fail;   // nonzero once a wait of this workgroup ran out of time (one-launch kernels only)
 };
 
 // Top_budget over the supertree: stages the selected entries (as compact_selected does).
@@ -265,6 +267,7 @@ __device__ __forceinline__ FastSmem fast_smem(unsigned char* raw, const FastLayo
   sm.anc = reinterpret_cast<int32_t*>(raw + L.anc);
   sm.mk = reinterpret_cast<uint32_t*>(raw + L.mk);
   sm.ready = reinterpret_cast<uint32_t*>(raw + L.ready);
+  sm.fail = reinterpret_cast<uint32_t*>(raw + L.fail);
   return sm;
 }
 
@@ -288,15 +291,29 @@ __device__ __forceinline__ void publish_slab(uint32_t* ready, int i) {
   __hip_atomic_store(&ready[i], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 
-// Waits until slab i has been published.  Its producer is another wave of the same
-// workgroup that runs unconditionally, so the flag is always set; the wait is bounded
-// all the same.
-__device__ __forceinline__ void wait_slab(uint32_t* ready, int i) {
-  for (int spin = 0; spin < (1 << 22); ++spin) {
-    const uint32_t f = __hip_atomic_load(&ready[i], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP);
-    if (__builtin_amdgcn_readfirstlane(f) != 0u) return;
+// Bound of every wait inside a launch: 1 s of the 100 MHz real-time counter.  The
+// producers a wait depends on run unconditionally in the same launch, so the bound is
+// only reached on a stalled device; the wait then reports failure instead of spinning on.
+constexpr uint64_t kWaitTicks = 100000000ull;
+
+// Waits until the workgroup-scope flag *f is set by another wave of the same workgroup.
+// Returns false if the wait ran out of time (t0: the waiting wave's start time); the
+// workgroup's fail word is then set.
+__device__ __forceinline__ bool wait_flag(uint32_t* f, uint32_t* fail, uint64_t t0) {
+  for (;;) {
+    const uint32_t v = __hip_atomic_load(f, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP);
+    if (__builtin_amdgcn_readfirstlane(v) != 0u) return true;
+    if (__builtin_amdgcn_s_memrealtime() - t0 > kWaitTicks) {
+      __hip_atomic_store(fail, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+      return false;
+    }
     __builtin_amdgcn_s_sleep(1);
   }
+}
+
+// Waits until slab i has been published.
+__device__ __forceinline__ bool wait_slab(const FastSmem& sm, int i, uint64_t t0) {
+  return wait_flag(&sm.ready[i], sm.fail, t0);
 }
 
 // Depth-wise expansion (Eq. ubtree-frontier): F_d = Top_W(E_d) for d = 1..gamma.  F_d is
@@ -317,10 +334,11 @@ __device__ __forceinline__ void expand_depths(const TreeArgs& a, const FastSmem&
   int fpos = 0;
   float nq[KT];
   float rm;
+  const uint64_t t0 = kWait ? __builtin_amdgcn_s_memrealtime() : 0ull;
   if (kMemSlab) {
     rm = load_row_global<KT>(gq, vec, nq);  // depth 1 extends the root through row 0
   } else {
-    if (kWait) wait_slab(sm.ready, 0);
+    if (kWait) wait_slab(sm, 0, t0);
     load_row<KT>(sm.slab, nq);  // depth 1 extends the root through row 0
     rm = sm.rmax[0];
   }
@@ -378,7 +396,7 @@ __device__ __forceinline__ void expand_depths(const TreeArgs& a, const FastSmem&
       if (kMemSlab) {
         rm = load_row_global<KT>(gq + (d * KT + c) * KT, vec, nq);
       } else {
-        if (kWait) wait_slab(sm.ready, d);
+        if (kWait) wait_slab(sm, d, t0);
         load_row<KT>(sm.slab + (d * KT + c) * KT, nq);
         rm = sm.rmax[d * KT + c];
       }
@@ -457,8 +475,15 @@ __device__ __forceinline__ void fast_search(const TreeArgs& a, const FastSmem& s
   int32_t* dep = a.depth + b * N;
   int32_t* crk = a.cand_rank + b * N;
   float* scr = a.score + b * N;
+  // A wait of this workgroup that ran out of time (one-launch kernels) leaves scores
+  // that were never published behind the tree: the sequence is then marked with
+  // n_nodes = 0, and the launch's error word is set if it has one.
+  const bool failed =
+      kWait && __builtin_amdgcn_readfirstlane(__hip_atomic_load(sm.fail, __ATOMIC_RELAXED,
+                                                                __HIP_MEMORY_SCOPE_WORKGROUP)) != 0u;
   if (lane == 0) {
-    a.n_nodes[b] = n_nodes;
+    a.n_nodes[b] = failed ? 0 : n_nodes;
+    if (failed && a.err) __hip_atomic_store(a.err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     tok[0] = a.anchor[b];
     par[0] = -1;
     dep[0] = 0;

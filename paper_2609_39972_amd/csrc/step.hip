@@ -21,9 +21,10 @@
 //     t / (B C).  Workgroups are dispatched in index order as earlier ones retire, so the
 //     items run depth-major with a window of resident items (two workgroups per compute
 //     unit: at B = 32, C = 2 about eight positions in flight, the first rows ready after
-//     about 12 of 31 us of sweep).  An item runs the one-row sweep on its chunk, writes the chunk's
-//     LSE and top K (ids relative to the chunk) with device-coherent stores, waits for
-//     them to complete, and adds 1 to the row's counter.
+//     about 12 of 31 us of sweep).  An item runs the one-row sweep on its chunk, writes the
+//     chunk's LSE and top K (ids relative to the chunk) with device-coherent stores, and
+//     raises the row's counter with an agent-scope release; the helper that sees the count
+//     complete acquires at agent scope before it reads the chunks.
 // The merge of the chunks is exact for the candidates (a selection on the same order
 // values) and sums the chunks' exponentials in chunk order, so the candidates, the slabs
 // and the tree are those of ubt_topk followed by ubt_draft_tree, and LSE and log-probs
@@ -46,7 +47,6 @@ namespace {
 // short to cover its own load latency and merge); 4-wave workgroups with C = 4 48.8 us.
 constexpr int kPipeWaves = 8;
 constexpr int kPipeMaxChunks = 2;
-constexpr uint64_t kWaitTicks = 100000000ull;  // 1 s of the 100 MHz real-time counter
 constexpr uint32_t kCountBase = 256;           // byte offset of the row counters in the workspace
 
 __device__ __forceinline__ void store_agent32(uint32_t* p, uint32_t v) {
@@ -54,12 +54,6 @@ __device__ __forceinline__ void store_agent32(uint32_t* p, uint32_t v) {
 }
 __device__ __forceinline__ uint32_t load_agent32(const uint32_t* p) {
   return __hip_atomic_load(const_cast<uint32_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-// Waits until every memory operation issued so far by this wave has completed.
-__device__ __forceinline__ void wait_all_memory() {
-  __atomic_signal_fence(__ATOMIC_SEQ_CST);
-  __builtin_amdgcn_s_waitcnt(0);
-  __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
 struct PipeArgs {
@@ -94,18 +88,22 @@ __device__ __forceinline__ void pipe_worker(const PipeArgs& p, RowLdsT<kPipeWave
   const T* rp = static_cast<const T*>(p.logits) + b * p.stride_b + i * p.stride_i + c0;
   sweep_row<T, true, kPipeWaves>(lds, rp, len, p.K, row * p.chunks + c,
                                  RowOut{p.part_ids, p.part_logit, nullptr, p.part_lse, true});
-  // Wave 0 wrote the chunk's results (device-coherent stores); once they have completed,
-  // the row's counter goes up.
-  if (w == 0) {
-    wait_all_memory();
-    if (lane == 0) __hip_atomic_fetch_add(&p.count[row], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
+  // Wave 0 wrote the chunk's results.  After the workgroup barrier one thread raises the
+  // row's counter with release semantics at agent scope, which makes every store that
+  // happens before it (the barrier orders the other lanes' stores) visible to a wave that
+  // acquires the count.
+  __syncthreads();
+  if (w == 0 && lane == 0) __hip_atomic_fetch_add(&p.count[row], 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Spins until *f reaches n; false if the wait ran out of time.
+// Spins until *f reaches n, then acquires at agent scope (pairing with the workers'
+// release of the count); false if the wait ran out of time.
 __device__ __forceinline__ bool wait_count(const uint32_t* f, uint32_t n, uint64_t t0) {
   for (;;) {
-    if (__builtin_amdgcn_readfirstlane(load_agent32(f)) >= n) return true;
+    if (__builtin_amdgcn_readfirstlane(load_agent32(f)) >= n) {
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+      return true;
+    }
     if (__builtin_amdgcn_s_memrealtime() - t0 > kWaitTicks) return false;
     __builtin_amdgcn_s_sleep(2);
   }
@@ -195,6 +193,7 @@ __device__ __forceinline__ void searcher(const PipeArgs& p, const TreeArgs& a, c
     sm.ready[e] = 0u;
     rready[e] = 0u;
   }
+  if (threadIdx.x == 0) *sm.fail = 0u;
   __syncthreads();
   __builtin_amdgcn_s_setprio(3);
   if (w == 0) {
@@ -204,11 +203,14 @@ __device__ __forceinline__ void searcher(const PipeArgs& p, const TreeArgs& a, c
   const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
   for (int i = w - 1; i < gamma; i += nw - 1) {
     const int64_t bi = static_cast<int64_t>(b) * gamma + i;
-    if (!wait_count(&p.count[bi], static_cast<uint32_t>(p.chunks), t0) && lane == 0) store_agent32(p.err, 1u);
+    if (!wait_count(&p.count[bi], static_cast<uint32_t>(p.chunks), t0) && lane == 0) {
+      store_agent32(p.err, 1u);
+      __hip_atomic_store(sm.fail, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    }
     merge_chunks<T, KT>(p, bi, i, stage, sm.cids, clogit, lane);
     if (lane == 0) store_agent32(&p.count[bi], 0u);  // read: ready for the next call
     publish_slab(rready, i);
-    if (i > 0) wait_slab(rready, i - 1);
+    if (i > 0) wait_flag(&rready[i - 1], sm.fail, t0);
     float* slab = sm.slab + i * KT * KT;
     bigram_tile_bf16<1>(s.phi, s.psi, s.gate + bi * s.r, s.V, s.r, i, KT, a.anchor + b,
                         i > 0 ? sm.cids + (i - 1) * KT : sm.cids, sm.cids + i * KT, clogit + i * KT, s.sc.alpha[i],
@@ -315,6 +317,8 @@ hipError_t launch_draft_step(const void* logits, int dtype, int B, int gamma, in
   p.part_ids = reinterpret_cast<int32_t*>(ws + pw.part_ids);
   p.part_logit = reinterpret_cast<float*>(ws + pw.part_logit);
   p.part_lse = reinterpret_cast<float*>(ws + pw.part_lse);
+  TreeArgs ta = a;
+  ta.err = p.err;  // a search that ran out of time also sets the workspace's error word
 
   const uint64_t magic_w = (0x100000000ull + a.W - 1) / a.W;
   const size_t row_smem = sizeof(RowLdsT<kPipeWaves>);
@@ -327,7 +331,7 @@ hipError_t launch_draft_step(const void* logits, int dtype, int B, int gamma, in
   do {                                                                                                      \
     (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&draft_pipe_kernel<TT, KK, RR>),               \
                               hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(smem));          \
-    hipLaunchKernelGGL((draft_pipe_kernel<TT, KK, RR>), grid, block, smem, stream, p, a, s, magic_w);      \
+    hipLaunchKernelGGL((draft_pipe_kernel<TT, KK, RR>), grid, block, smem, stream, p, ta, s, magic_w);      \
   } while (0)
 #define UBT_PIPE_ROWS(TT, KK)       \
   do {                              \

@@ -373,6 +373,7 @@ __global__ __launch_bounds__(kDraftWaves* kWave) void draft_tree_fast_kernel(Tre
   const int32_t* gids = a.cand_ids + b * gamma * KT;
   for (int e = static_cast<int>(threadIdx.x); e < gamma * KT; e += static_cast<int>(blockDim.x)) sm.cids[e] = gids[e];
   for (int e = static_cast<int>(threadIdx.x); e < gamma; e += static_cast<int>(blockDim.x)) sm.ready[e] = 0u;
+  if (threadIdx.x == 0) *sm.fail = 0u;
   __syncthreads();
   const int first = w;
   const int stride = w == 0 ? gamma : nw - 1;

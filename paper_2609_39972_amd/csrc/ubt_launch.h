@@ -41,6 +41,7 @@ struct TreeArgs {
   int32_t* f_parent;
   int32_t* f_cand;
   float* f_score;
+  uint32_t* err;  // one-launch kernels: error word set when a wait inside the launch timed out (may be null)
 };
 hipError_t launch_build_tree(const TreeArgs& a, hipStream_t stream);
 

@@ -15,9 +15,19 @@ be exact for the GPU's tree.
 """
 from __future__ import annotations
 
+import json
+import math
+import os
+
 import numpy as np
 
 EPS = 1e-5
+
+# Largest share of a call's trees that may need the tie excusal.  A selection differs
+# from the oracle's only when two fp64 scores lie within fp32 rounding (about 1e-6) of
+# each other at a selection boundary, which at these score spreads happens for well
+# under one tree in a thousand.
+MAX_EXCUSED_SHARE = 0.05
 
 
 def tol(ref: np.ndarray) -> np.ndarray:
@@ -190,3 +200,15 @@ def _validate_cut(items: list, chosen: set, score: dict, n: int, where: str) -> 
             assert x in chosen, f"{where}: dropped {x} with score {s} above the boundary {boundary}"
         if s < boundary - gap:
             assert x not in chosen, f"{where}: kept {x} with score {s} below the boundary {boundary}"
+
+
+def record(label: str, counts: dict) -> None:
+    """Bounds the excused share of one comparison and, when the environment variable
+    UBT_PARITY_RECORD names a file, appends the counts to it as a JSON line."""
+    trees = counts["exact"] + counts["excused"]
+    assert counts["excused"] <= max(1, math.ceil(MAX_EXCUSED_SHARE * trees)), \
+        f"{label}: {counts['excused']} of {trees} trees needed the tie excusal"
+    path = os.environ.get("UBT_PARITY_RECORD")
+    if path:
+        with open(path, "a") as fh:
+            fh.write(json.dumps({"case": label, **counts, "failed": 0}) + "\n")

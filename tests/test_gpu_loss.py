@@ -60,6 +60,7 @@ def _check(w: synth.Workload, d: dict, li: dict, T: float, beta: float, grad_row
     err = np.abs(gl - rl)
     assert np.all(err <= 1e-5 * np.abs(rl) + 1e-6), f"grad_logits: max error {err.max():.3g}"
     invalid = li["y_star"] < 0
+    assert (~invalid).any(), "the case has no valid position: it would only compare zeros"
     assert not g["loss"][invalid].any() and not g["grad_s"][invalid].any()
     say(f"  valid positions {int((~invalid).sum())}, mean loss {g['loss'][~invalid].mean():.4f}")
 
@@ -69,7 +70,7 @@ def _check(w: synth.Workload, d: dict, li: dict, T: float, beta: float, grad_row
     (dict(B=3, L=6, V=3001, dtype="f32", feat_dtype="f32", K=8, r=32), 0.0),   # T -> 0
     (dict(B=2, L=9, V=4096, dtype="bf16", feat_dtype="bf16", K=16, r=64), 1.0),  # vector pass
     (dict(B=2, L=4, V=2048, dtype="bf16", feat_dtype="f32", K=64, r=16), 0.0),   # K = 64, ties likely
-    (dict(B=1, L=2, V=512, dtype="f32", feat_dtype="bf16", K=1, r=512), 1.0),   # K = 1: KL = 0
+    (dict(B=2, L=4, V=512, dtype="f32", feat_dtype="bf16", K=1, r=512), 1.0),   # K = 1: KL = 0; r = 512
 ])
 def test_loss_small(kw, T):
     base = dict(logits="normal", logit_std=2.0, budget=8, W=3)
@@ -79,6 +80,10 @@ def test_loss_small(kw, T):
     d["alpha"] = rng.uniform(0.5, 2.0, w.gamma).astype(np.float32)
     d["lam"] = rng.uniform(0.5, 2.0, w.gamma).astype(np.float32)
     li = synth.loss_inputs(w, 0, invalid_frac=0.2)
+    # Keep the first position of every sequence valid (its predecessor is the anchor), so
+    # each case compares real losses, also the smallest ones.
+    y = li["y_star"]
+    y[:, 0] = np.where(y[:, 0] < 0, 0, y[:, 0])
     _check(w, d, li, T, 0.1)
 
 

@@ -27,12 +27,16 @@ def _check_workload(w: synth.Workload, W: int, buf: int = 0, allow_ties: bool = 
     counts = parity.check_tree(g, ref, ref_s["logq"], ref_t["cand_ids"], d["anchor"], W, w.budget, w.zeta,
                                allow_ties=allow_ties)
     assert (g["n_nodes"] == w.N).all(), "every tree should use the whole budget"
+    parity.record(f"pipeline wl{w.cfg} buf={buf} W={W}", counts)
     say(f"  trees: {counts}")
     return counts
 
 
 def test_workload1_exact():
-    _check_workload(synth.WORKLOADS[1], synth.WORKLOADS[1].W)
+    """Workload 1 (fp32 logits and features): every tree identical to the oracle's, with
+    no tie excused."""
+    counts = _check_workload(synth.WORKLOADS[1], synth.WORKLOADS[1].W, allow_ties=False)
+    assert counts["excused"] == 0
 
 
 @pytest.mark.parametrize("cfg", [2, 3, 4, 5, 6])

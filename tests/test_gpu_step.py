@@ -1,14 +1,18 @@
 """GPU tests of ubt_draft_step, the whole step in one launch (rows swept depth by depth in
 chunks beside per-sequence searchers that merge the chunks and search as the rows come
-out).  Its candidates, logq and trees must be bit-identical to ubt_topk
-followed by the separate selector and search calls (whose parity with the oracle the
-pipeline tests establish); its LSE and log-probs are summed in another order and must
-agree with the oracle within the fp32 score tolerance.  Also: the workspace flags are
-reset and its error word clear after every call, repeated calls on one workspace
-give identical bits, graph replays match eager calls, and the shapes that stress the
-split (ties across many tiles, rows whose top elements sit late in the row, few tiles
-per row, a last chunk shorter than K, fp32 logits, one position, 64 sequences) and the
-fallback to the separate calls."""
+out).
+
+Every case is checked against the fp64 oracle: candidate ids bit-exact, LSE, log-probs
+and logq within the fp32 score tolerance, and the trees exact or within the 1e-5 tie
+gap.  The guided tie check needs the supertree F_d, which only ubt_build_tree can dump:
+the one-launch outputs are first shown bit-identical to ubt_topk + ubt_bigram_scores +
+ubt_build_tree (candidates, logq, tree and mask), then validated with that path's dump.
+
+Also: the workspace error word is clear and every row counter reset after every call,
+repeated calls on one workspace give identical bits, graph replays match eager calls,
+and the shapes that stress the split (ties across many tiles, rows whose top elements sit
+late in the row, few tiles per row, a last chunk shorter than K, fp32 logits, one
+position, 64 sequences) and the fallback to the separate calls."""
 from __future__ import annotations
 
 import numpy as np
@@ -37,6 +41,8 @@ def _logits_tensor(w: synth.Workload, d: dict):
 
 
 def _run_both(w: synth.Workload, d: dict, W: int) -> tuple[dict, dict, object]:
+    """The separate calls (with the supertree dump) and the one-launch call on the same
+    inputs."""
     import torch
 
     import paper_2609_39972_amd as ubt
@@ -45,12 +51,12 @@ def _run_both(w: synth.Workload, d: dict, W: int) -> tuple[dict, dict, object]:
     args = _args(w, d, W)
     logits = _logits_tensor(w, d)
     dtype = torch.bfloat16 if w.dtype == "bf16" else torch.float32
-    sep = ubt.DraftStep(*args, fused=False)
+    sep = ubt.DraftStep(*args, fused=False, debug=True)
     one = ubt.DraftStep(*args, one_call=True, logit_dtype=dtype)
     a = to_np(sep.run(logits))
     torch.cuda.synchronize()
     b = to_np(one.run(logits))
-    torch.cuda.synchronize()
+    one.check()
     return a, b, one
 
 
@@ -76,7 +82,21 @@ def _same(a: dict, b: dict, logit_dtype: str) -> None:
         assert np.all(np.abs(b[k] - ref) <= 1e-5 * np.maximum(1.0, np.abs(ref))), f"{k} differs beyond 1e-5"
 
 
-def _check(w: synth.Workload, W: int, d: dict | None = None, buf: int = 0, vs_oracle: bool = True) -> None:
+def check_vs_oracle(w: synth.Workload, W: int, d: dict, sep: dict, one: dict) -> dict:
+    """The one-launch outputs against the oracle pipeline; `sep` (bit-identical to `one`
+    on the tree) supplies the supertree dump for the guided tie check.  Returns the tree
+    counts (exact / excused)."""
+    ref = oracle.pipeline(d["logits"], d["phi"], d["psi"], d["gate"], d["anchor"], d["alpha"], d["lam"], w.K, W,
+                          w.budget, w.zeta)
+    parity.check_topk(one, ref)
+    parity.check_selector({"logq": one["logq"]}, ref)
+    g = dict(one)
+    for k in ("f_count", "f_parent", "f_cand", "f_score"):
+        g[k] = sep[k]
+    return parity.check_tree(g, ref, ref["logq"], ref["cand_ids"], d["anchor"], W, w.budget, w.zeta)
+
+
+def _check(w: synth.Workload, W: int, d: dict | None = None, buf: int = 0) -> dict:
     from gpu_util import say
 
     say(f"draft_step workload {w.cfg} buf={buf} W={W}: {w.describe()}")
@@ -86,8 +106,10 @@ def _check(w: synth.Workload, W: int, d: dict | None = None, buf: int = 0, vs_or
     _same(a, b, w.dtype)
     if one.workspace is not None:
         _check_workspace(one)
-    if vs_oracle:
-        parity.check_topk(b, oracle.topk(d["logits"], w.K))
+    counts = check_vs_oracle(w, W, d, a, b)
+    parity.record(f"draft_step wl{w.cfg} W={W}", counts)
+    say(f"  trees vs oracle: {counts}")
+    return counts
 
 
 @pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5, 6])
@@ -99,7 +121,7 @@ def test_step_workload(cfg):
 @pytest.mark.parametrize("cfg", [1, 2, 3, 4])
 def test_step_best_first_width(cfg):
     w = synth.WORKLOADS[cfg]
-    _check(w, w.budget, vs_oracle=False)
+    _check(w, w.budget)
 
 
 def test_step_repeat_and_pool():
@@ -126,7 +148,10 @@ def test_step_repeat_and_pool():
     for k in r0:
         assert np.array_equal(r0[k], r2[k]), f"{k} differs between identical calls"
     assert not np.array_equal(r0["cand_ids"], r1["cand_ids"])
-    parity.check_topk(r1, oracle.topk(d1["logits"], w.K))
+    ref1 = oracle.pipeline(d1["logits"], d1["phi"], d1["psi"], d1["gate"], d1["anchor"], d1["alpha"], d1["lam"], w.K,
+                           w.W, w.budget, w.zeta)
+    parity.check_topk(r1, ref1)
+    parity.check_selector({"logq": r1["logq"]}, ref1)
 
 
 def test_step_graph_replay():
