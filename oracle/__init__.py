@@ -35,7 +35,10 @@ def _load(path: str) -> ctypes.CDLL:
     L.ubt_oracle_build_tree.argtypes = [_p, _p, _p, _i32, _i32, _i32, _i32, _i32, _f64,
                                         _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _i32]
     L.ubt_oracle_tree_mask.argtypes = [_p, _p, _i32, _i32, _p]
-    for f in (L.ubt_oracle_topk, L.ubt_oracle_bigram, L.ubt_oracle_build_tree, L.ubt_oracle_tree_mask):
+    L.ubt_oracle_edge_scores.argtypes = [_p, _p, _p, _p, _i32, _i32, _i32, _p]
+    L.ubt_oracle_best_first.argtypes = [_p, _p, _p, _i32, _i32, _i32, _i32, _f64, _p, _p, _p, _p, _p, _p, _p, _i32]
+    for f in (L.ubt_oracle_topk, L.ubt_oracle_bigram, L.ubt_oracle_build_tree, L.ubt_oracle_tree_mask,
+              L.ubt_oracle_edge_scores, L.ubt_oracle_best_first):
         f.restype = _i32
     return L
 
@@ -159,3 +162,49 @@ def pipeline(logits: np.ndarray, phi: np.ndarray, psi: np.ndarray, gate: np.ndar
     g = bigram(phi, psi, gate, anchor, t["cand_ids"], t["cand_logit"], alpha, lam, threads)
     tr = build_tree(anchor, t["cand_ids"], g["logq"], W, budget, zeta, threads)
     return {**t, **g, **tr}
+
+
+def edge_scores(cand_logprob: np.ndarray, delta: np.ndarray, alpha: np.ndarray, lam: np.ndarray) -> np.ndarray:
+    """Unigram-plus-bigram edge scores ``[B, gamma, K, K]``: alpha_i log q_i(c) + lambda_i
+    delta_i(a, c), not normalised over the successors."""
+    B, gamma, K = cand_logprob.shape
+    lp = np.ascontiguousarray(cand_logprob, np.float64)
+    dl = np.ascontiguousarray(delta, np.float64)
+    al = np.ascontiguousarray(alpha, np.float64)
+    la = np.ascontiguousarray(lam, np.float64)
+    edge = np.empty((B, gamma, K, K), np.float64)
+    _check(lib().ubt_oracle_edge_scores(_ptr(lp), _ptr(dl), _ptr(al), _ptr(la), B, gamma, K, _ptr(edge)),
+           "edge_scores")
+    return edge
+
+
+def best_first(anchor: np.ndarray, cand_ids: np.ndarray, edge: np.ndarray, budget: int, zeta: float = 0.0,
+               threads: int | None = None) -> dict:
+    """Best-first tree over the candidate lattice under cumulative edge scores, grown
+    from the root one node at a time (a node is eligible once its parent is in)."""
+    B, gamma, K = cand_ids.shape
+    N = budget + 1
+    words = (N + 31) // 32
+    anc = np.ascontiguousarray(anchor, np.int32)
+    ids = np.ascontiguousarray(cand_ids, np.int32)
+    e = np.ascontiguousarray(edge, np.float64)
+    o = dict(n_nodes=np.empty(B, np.int32), token=np.empty((B, N), np.int32), parent=np.empty((B, N), np.int32),
+             depth=np.empty((B, N), np.int32), cand_rank=np.empty((B, N), np.int32),
+             score=np.empty((B, N), np.float64), mask=np.empty((B, N, words), np.uint32))
+    _check(lib().ubt_oracle_best_first(_ptr(anc), _ptr(ids), _ptr(e), B, gamma, K, budget, float(zeta),
+                                       _ptr(o["n_nodes"]), _ptr(o["token"]), _ptr(o["parent"]), _ptr(o["depth"]),
+                                       _ptr(o["cand_rank"]), _ptr(o["score"]), _ptr(o["mask"]),
+                                       threads or default_threads()), "best_first")
+    return o
+
+
+def pipeline_unigram_bigram(logits: np.ndarray, phi: np.ndarray, psi: np.ndarray, gate: np.ndarray,
+                            anchor: np.ndarray, alpha: np.ndarray, lam: np.ndarray, K: int, budget: int,
+                            zeta: float = 0.0, threads: int | None = None) -> dict:
+    """The step under the unigram-plus-bigram scoring: candidates, selector scores, edge
+    scores and the best-first tree."""
+    t = topk(logits, K, threads)
+    g = bigram(phi, psi, gate, anchor, t["cand_ids"], t["cand_logit"], alpha, lam, threads)
+    e = edge_scores(t["cand_logprob"], g["delta"], alpha, lam)
+    tr = best_first(anchor, t["cand_ids"], e, budget, zeta, threads)
+    return {**t, **g, "edge": e, **tr}

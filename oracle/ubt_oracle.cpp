@@ -19,6 +19,16 @@
 //                          and Algorithm 1 (construction from precomputed scores).
 //   ubt_oracle_tree_mask   Appendix A / Verification via Tree-attention: every node attends
 //                          to itself and to its ancestors.
+//   ubt_oracle_edge_scores, ubt_oracle_best_first
+//                          the unigram-plus-bigram scoring: each edge scores its
+//                          successor's unigram log-probability (Eq. ubtree-unigram) plus its
+//                          raw selector score (Eq. dflash2-selector), weighted as in Eq.
+//                          ubtree-depth; paths are ranked by the cumulative sum and grown
+//                          best-first (Background, "Tree Drafting": best-first search over
+//                          accumulated scores).  These sums are not monotone along a path,
+//                          so the prefix closure that Appendix A / Global Pruning gets from
+//                          normalisation is enforced by the search itself: a node becomes
+//                          eligible only once its parent is in the tree.
 //
 // Readings where the paper is silent (each is listed with its reason in the design notes):
 //   * ties in C_i go to the lower token id; values compare as real numbers (-0 == +0);
@@ -275,6 +285,112 @@ int ubt_oracle_build_tree(const int32_t* anchor, const int32_t* cand_ids, const 
   });
   for (int s : status)
     if (s) return s;
+  return 0;
+}
+
+// Edge scores of the unigram-plus-bigram scoring.  Inputs as written by ubt_oracle_topk
+// (cand_logprob = log q_i of each candidate, i.e. u - LSE) and ubt_oracle_bigram (delta,
+// [B, gamma, K, K] indexed [b][i][a][c]); alpha, lambda [gamma].  Output edge [B, gamma,
+// K, K], same indexing:
+//   e_i(a, c) = alpha_i * log q_i(C_i[c]) + lambda_i * delta_i(a, c)
+// with no normalisation over the successors.  At i = 0 only row a = 0 (the anchor) is a
+// predecessor; rows 1..K-1 of that slab are written as 0.
+int ubt_oracle_edge_scores(const double* cand_logprob, const double* delta, const double* alpha,
+                           const double* lambda, int B, int gamma, int K, double* edge) {
+  if (!cand_logprob || !delta || !alpha || !lambda || !edge || B < 0 || gamma < 1 || K < 1) return 1;
+  for (int64_t b = 0; b < B; ++b)
+    for (int i = 0; i < gamma; ++i) {
+      const int64_t bi = b * gamma + i;
+      const int n_pred = (i == 0) ? 1 : K;
+      for (int a = 0; a < K; ++a)
+        for (int c = 0; c < K; ++c) {
+          const int64_t o = (bi * K + a) * K + c;
+          edge[o] = (a < n_pred) ? alpha[i] * cand_logprob[bi * K + c] + lambda[i] * delta[o] : 0.0;
+        }
+    }
+  return 0;
+}
+
+// Best-first tree over the candidate lattice for B independent sequences.  Inputs:
+// anchor [B], cand_ids [B, gamma, K], edge [B, gamma, K, K] (any real values; e.g. from
+// ubt_oracle_edge_scores), non-root budget, depth bonus zeta <= 0.
+// The path score is l(y_{1:d}) = sum_{i<=d} e_i(y_{i-1}, y_i) + zeta * d, with y_0 the
+// anchor (row 0 of the first slab).  Starting from the root, the tree grows one node at a
+// time: among the children of tree nodes that are not yet in the tree (the frontier), the
+// best one is added, under the order
+//   score desc, then depth asc, then the parent's slot asc, then candidate rank asc,
+// until `budget` nodes are in or the frontier is empty.  Slots are assigned in that
+// addition order (root = 0), so every parent precedes its children.  Outputs as for
+// ubt_oracle_build_tree (no supertree).
+int ubt_oracle_best_first(const int32_t* anchor, const int32_t* cand_ids, const double* edge,
+                          int B, int gamma, int K, int budget, double zeta,
+                          int32_t* n_nodes, int32_t* token, int32_t* parent, int32_t* depth,
+                          int32_t* cand_rank, double* score, uint32_t* mask, int n_threads) {
+  if (!anchor || !cand_ids || !edge || !n_nodes || !token || !parent || !depth || !cand_rank ||
+      !score || !mask)
+    return 1;
+  if (B < 0 || gamma < 1 || K < 1 || budget < 1 || !(zeta <= 0.0)) return 1;
+  const int N = budget + 1;
+  const int words = (N + 31) / 32;
+
+  parallel_for(B, n_threads, [&](int64_t b) {
+    struct Cand {
+      double score;  // l of the candidate node's prefix
+      int depth;     // its depth d >= 1
+      int pslot;     // slot of its parent in the tree
+      int c;         // its candidate rank in C_d
+    };
+    auto before = [](const Cand& x, const Cand& y) {
+      if (x.score != y.score) return x.score > y.score;
+      if (x.depth != y.depth) return x.depth < y.depth;
+      if (x.pslot != y.pslot) return x.pslot < y.pslot;
+      return x.c < y.c;
+    };
+    int32_t* tok = token + b * N;
+    int32_t* par = parent + b * N;
+    int32_t* dep = depth + b * N;
+    int32_t* cr = cand_rank + b * N;
+    double* sc = score + b * N;
+    for (int n = 0; n < N; ++n) {
+      tok[n] = par[n] = dep[n] = cr[n] = -1;
+      sc[n] = kNegInf;
+    }
+    tok[0] = anchor[b];
+    dep[0] = 0;
+    sc[0] = 0.0;
+
+    // The children of a tree node at slot `slot` (depth d, candidate rank c; the root has
+    // d = 0 and predecessor row 0): the K candidates of position d + 1.
+    std::vector<Cand> frontier;
+    auto push_children = [&](int slot, int d, int c, double s) {
+      if (d >= gamma) return;
+      const int row = (d == 0) ? 0 : c;
+      const double* e = edge + ((b * gamma + d) * static_cast<int64_t>(K) + row) * K;
+      for (int k = 0; k < K; ++k) frontier.push_back({s + e[k] + zeta, d + 1, slot, k});
+    };
+    push_children(0, 0, -1, 0.0);
+    int n = 1;
+    while (n <= budget && !frontier.empty()) {
+      size_t best = 0;
+      for (size_t j = 1; j < frontier.size(); ++j)
+        if (before(frontier[j], frontier[best])) best = j;
+      const Cand x = frontier[best];
+      frontier.erase(frontier.begin() + static_cast<std::ptrdiff_t>(best));
+      tok[n] = cand_ids[(b * gamma + (x.depth - 1)) * static_cast<int64_t>(K) + x.c];
+      par[n] = x.pslot;
+      dep[n] = x.depth;
+      cr[n] = x.c;
+      sc[n] = x.score;
+      push_children(n, x.depth, x.c, x.score);
+      ++n;
+    }
+    n_nodes[b] = n;
+
+    uint32_t* mrow = mask + b * static_cast<int64_t>(N) * words;
+    std::fill(mrow, mrow + static_cast<int64_t>(N) * words, 0u);
+    for (int m0 = 0; m0 < n; ++m0)
+      for (int m = m0; m >= 0; m = par[m]) mrow[m0 * words + m / 32] |= 1u << (m % 32);
+  });
   return 0;
 }
 

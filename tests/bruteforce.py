@@ -94,3 +94,27 @@ def frontier_as_paths(out: dict, b: int) -> list:
         res.append(cur)
         prev = cur
     return res
+
+
+def closure_best_first(edge: np.ndarray, budget: int, zeta: float = 0.0) -> list:
+    """Best-first growth under arbitrary (not necessarily monotone) edge scores, by brute
+    force: every lattice node is scored from scratch as a path sum; then, `budget` times,
+    the best node not yet taken whose parent is taken is added, under (score desc, depth
+    asc, parent's position in the taken list asc, candidate rank asc).  Returns the taken
+    nodes in order.  No frontier is kept: each round rescans the whole lattice."""
+    sc = lattice(edge, zeta)
+    taken = [()]
+    pos = {(): 0}
+    while len(taken) - 1 < budget:
+        best, best_key = None, None
+        for p in sc:
+            if p in pos or p[:-1] not in pos:
+                continue
+            key = (-sc[p], len(p), pos[p[:-1]], p[-1])
+            if best_key is None or key < best_key:
+                best, best_key = p, key
+        if best is None:
+            break
+        pos[best] = len(taken)
+        taken.append(best)
+    return taken[1:]
