@@ -148,7 +148,8 @@ def test_step_repeat_and_pool():
     for k in r0:
         assert np.array_equal(r0[k], r2[k]), f"{k} differs between identical calls"
     assert not np.array_equal(r0["cand_ids"], r1["cand_ids"])
-    ref1 = oracle.pipeline(d1["logits"], d1["phi"], d1["psi"], d1["gate"], d1["anchor"], d1["alpha"], d1["lam"], w.K,
+    # The step holds buffer 0's gate and anchor; only the logits come from buffer 1.
+    ref1 = oracle.pipeline(d1["logits"], d0["phi"], d0["psi"], d0["gate"], d0["anchor"], d0["alpha"], d0["lam"], w.K,
                            w.W, w.budget, w.zeta)
     parity.check_topk(r1, ref1)
     parity.check_selector({"logq": r1["logq"]}, ref1)
