@@ -22,9 +22,18 @@
 //     items run depth-major with a window of resident items (two workgroups per compute
 //     unit: at B = 32, C = 2 about eight positions in flight, the first rows ready after
 //     about 12 of 31 us of sweep).  An item runs the one-row sweep on its chunk, writes the
-//     chunk's LSE and top K (ids relative to the chunk) with device-coherent stores, and
-//     raises the row's counter with an agent-scope release; the helper that sees the count
-//     complete acquires at agent scope before it reads the chunks.
+//     chunk's LSE and top K (ids relative to the chunk) with device-coherent stores, waits for
+//     them to complete, and adds 1 to the row's counter.
+// The hand-over between workgroups (which may sit on different XCDs, each with its own
+// L2) uses agent-scope atomics only: the chunk results are written with relaxed
+// agent-scope atomic stores and read with relaxed agent-scope atomic loads, so they go to
+// and come from the device-coherent level and no L2 holds a stale copy.  The ordering is
+// the hardware's: the producer's wave waits for its stores to be acknowledged
+// (s_waitcnt 0) before it issues the counter increment, and a helper issues its loads of
+// the results only after its counter load has returned the final count.  A release on
+// the increment and an acquire after the wait express the same order in the language's
+// memory model, but at agent scope they compile to an L2 write-back per chunk and an L2
+// invalidation per row: measured 71.3 us per call against 45.2 us at B = 32, V = 151936.
 // The merge of the chunks is exact for the candidates (a selection on the same order
 // values) and sums the chunks' exponentials in chunk order, so the candidates, the slabs
 // and the tree are those of ubt_topk followed by ubt_draft_tree, and LSE and log-probs
@@ -54,6 +63,12 @@ __device__ __forceinline__ void store_agent32(uint32_t* p, uint32_t v) {
 }
 __device__ __forceinline__ uint32_t load_agent32(const uint32_t* p) {
   return __hip_atomic_load(const_cast<uint32_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// Waits until every memory operation issued so far by this wave has completed.
+__device__ __forceinline__ void wait_all_memory() {
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_waitcnt(0);
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
 struct PipeArgs {
@@ -88,22 +103,18 @@ __device__ __forceinline__ void pipe_worker(const PipeArgs& p, RowLdsT<kPipeWave
   const T* rp = static_cast<const T*>(p.logits) + b * p.stride_b + i * p.stride_i + c0;
   sweep_row<T, true, kPipeWaves>(lds, rp, len, p.K, row * p.chunks + c,
                                  RowOut{p.part_ids, p.part_logit, nullptr, p.part_lse, true});
-  // Wave 0 wrote the chunk's results.  After the workgroup barrier one thread raises the
-  // row's counter with release semantics at agent scope, which makes every store that
-  // happens before it (the barrier orders the other lanes' stores) visible to a wave that
-  // acquires the count.
-  __syncthreads();
-  if (w == 0 && lane == 0) __hip_atomic_fetch_add(&p.count[row], 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+  // Wave 0 wrote the chunk's results with agent-scope atomic stores; once they have
+  // completed, the row's counter goes up.
+  if (w == 0) {
+    wait_all_memory();
+    if (lane == 0) __hip_atomic_fetch_add(&p.count[row], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
 }
 
-// Spins until *f reaches n, then acquires at agent scope (pairing with the workers'
-// release of the count); false if the wait ran out of time.
+// Spins until *f reaches n; false if the wait ran out of time.
 __device__ __forceinline__ bool wait_count(const uint32_t* f, uint32_t n, uint64_t t0) {
   for (;;) {
-    if (__builtin_amdgcn_readfirstlane(load_agent32(f)) >= n) {
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-      return true;
-    }
+    if (__builtin_amdgcn_readfirstlane(load_agent32(f)) >= n) return true;
     if (__builtin_amdgcn_s_memrealtime() - t0 > kWaitTicks) return false;
     __builtin_amdgcn_s_sleep(2);
   }
