@@ -22,7 +22,9 @@
  *   ubt_tree_kl_loss   the renormalised-KL objective and its gradients
  *
  * ubt_draft_tree does ubt_bigram_scores + ubt_build_tree in one call (one launch for
- * the common shapes).
+ * the common shapes); ubt_draft_step the whole step.  ubt_edge_scores and
+ * ubt_build_tree_best_first replace the last two calls under the unigram-plus-bigram
+ * scoring (cumulative unnormalised scores, best-first growth).
  *
  * Conventions shared by every call:
  *   - Every pointer is device memory unless marked [host].  The caller owns every
@@ -223,8 +225,9 @@ ubt_status_t ubt_draft_tree(const void* phi_tab, const void* psi_tab, const void
  * chunk counter per row (from byte 256) and the chunks' partial results; each call
  * resets the counters it raised, so one workspace serves any number of consecutive calls
  * on one stream; calls that may overlap need separate workspaces.  A chunk's results are
- * published by an agent-scope release on its row counter and read after an agent-scope
- * acquire.  Every wait inside the launch is bounded (1 s).  If one runs out of time (a
+ * exchanged through agent-scope atomic stores and loads, and its row counter is raised
+ * only after those stores have completed.  Every wait inside the launch is bounded (1 s).
+ * If one runs out of time (a
  * stalled device; never in normal operation) the error word becomes nonzero, the
  * affected sequences are written with n_nodes = 0, the call's outputs are unspecified,
  * and the workspace must be zero-filled again before the next call (a late chunk may
@@ -243,6 +246,60 @@ ubt_status_t ubt_draft_step(const void* logits, ubt_dtype_t dt, int B, int gamma
                             int32_t* token, int32_t* parent, int32_t* depth, int32_t* cand_rank,
                             float* score, uint32_t* mask, void* workspace, size_t workspace_bytes,
                             hipStream_t stream);
+
+/* ====================================================================================
+ * Unigram-plus-bigram scoring with best-first growth.  Each edge scores its successor's
+ * unigram log-probability plus its raw selector score; a path ranks by the cumulative
+ * sum, and the tree grows best-first from the root.  Those sums are not monotone along a
+ * path (a selector score can exceed the log-probability it is added to), so the prefix
+ * closure that Appendix A / Global Pruning gets from normalised scores is enforced by
+ * the growth rule instead: a node is eligible only once its parent is in the tree.
+ * ==================================================================================== */
+
+/* ------------------------------------------------------------------------------------
+ * ubt_edge_scores -- edge scores of the unigram-plus-bigram scoring:
+ *   e_i(a, c) = alpha_i log q_i(C_i[c]) + lambda_i delta_i(a, c)
+ * with log q_i the unigram log-probability (Method / Unigram Proposer, Eq.
+ * ubtree-unigram), delta_i the selector score (Background, Eq. dflash2-selector; Method /
+ * Parallel Computation, Eq. ubtree-edge-matrix) and the depth weights of Method / Depth
+ * Calibration, Eq. (ubtree-depth); no normalisation over the successors.
+ *
+ * Arguments as for ubt_bigram_scores, with cand_logprob (ubt_topk's log-probabilities,
+ * [B, gamma, K]) in place of cand_logit and `edge` in place of logq: float
+ * [B, gamma, K, K] indexed [b][i][a][c], any sign.  At i = 0 row a = 0 (the anchor)
+ * holds the scores and rows 1..K-1 are written as 0.  delta may be NULL.  The same
+ * matrix-core tile as ubt_bigram_scores forms delta; e = fmaf(lambda, delta, alpha *
+ * logprob) in fp32.
+ * ------------------------------------------------------------------------------------ */
+ubt_status_t ubt_edge_scores(const void* phi_tab, const void* psi_tab, const void* gate,
+                             ubt_dtype_t feat_dt, int64_t V, int r, const int32_t* anchor,
+                             const int32_t* cand_ids, const float* cand_logprob, const float* alpha,
+                             const float* lambda, int B, int gamma, int K, float* delta, float* edge,
+                             hipStream_t stream);
+
+/* ------------------------------------------------------------------------------------
+ * ubt_build_tree_best_first -- best-first growth under cumulative edge scores
+ * (Background, "Tree Drafting": best-first search over accumulated scores) with the
+ * depth bonus of Appendix A, Eq. (ubtree-depth-bonus):
+ *   l(y_{1:d}) = sum_{i<=d} e_i(y_{i-1}, y_i) + zeta * d,  y_0 = the anchor (row 0).
+ * From the root (slot 0), `budget` times: among the children of the tree's nodes that
+ * are not yet in the tree, the best joins it, under the order score desc, then depth
+ * asc, then the parent's slot asc, then candidate rank asc.  Slots follow that growth
+ * order, so parent[n] < n; the tree stops early only when the whole lattice is in.
+ * Scores accumulate in fp32 as (l(parent) + e) + zeta.
+ *
+ * anchor, cand_ids : as for ubt_build_tree.  edge : [B, gamma, K, K] from ubt_edge_scores
+ *            (any finite values).  K <= UBT_MAX_K, gamma <= UBT_MAX_GAMMA, 1 <= budget <=
+ *            UBT_MAX_BUDGET, zeta finite and <= 0.
+ * Outputs exactly as ubt_build_tree's (n_nodes, token, parent, depth, cand_rank, score,
+ * mask; unused slots -1 / -inf; mask may be NULL), with slots in growth order.
+ * One wavefront per sequence; edge slabs of up to 32 KB per sequence are staged in LDS.
+ * ------------------------------------------------------------------------------------ */
+ubt_status_t ubt_build_tree_best_first(const int32_t* anchor, const int32_t* cand_ids,
+                                       const float* edge, int B, int gamma, int K, int budget,
+                                       float zeta, int32_t* n_nodes, int32_t* token,
+                                       int32_t* parent, int32_t* depth, int32_t* cand_rank,
+                                       float* score, uint32_t* mask, hipStream_t stream);
 
 /* ------------------------------------------------------------------------------------
  * ubt_tree_mask -- the ancestor ("tree attention") mask of a tree given by parent

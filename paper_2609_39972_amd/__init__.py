@@ -39,7 +39,7 @@ STATUS = {0: "UBT_OK", 1: "UBT_ERR_NULL", 2: "UBT_ERR_SHAPE", 3: "UBT_ERR_VALUE"
 # Every symbol include/ubt.h declares.
 EXPORTS = ("ubt_status_str", "ubt_abi_version", "ubt_last_hip_error", "ubt_topk",
            "ubt_bigram_scores", "ubt_build_tree", "ubt_draft_tree", "ubt_draft_step_workspace_bytes",
-           "ubt_draft_step", "ubt_tree_mask", "ubt_tree_attention", "ubt_verify_accept", "ubt_commit_kv",
+           "ubt_draft_step", "ubt_edge_scores", "ubt_build_tree_best_first", "ubt_tree_mask", "ubt_tree_attention", "ubt_verify_accept", "ubt_commit_kv",
            "ubt_tree_kl_loss")
 
 _p = ctypes.c_void_p
@@ -83,6 +83,9 @@ def lib() -> ctypes.CDLL:
         L.ubt_draft_step.argtypes = [_p, _i32, _i32, _i32, _i64, _i64, _i64, _i32, _p, _p, _p, _i32, _i32, _p, _p,
                                      _p, _i32, _i32, _f32, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p,
                                      ctypes.c_size_t, _p]
+        L.ubt_edge_scores.argtypes = [_p, _p, _p, _i32, _i64, _i32, _p, _p, _p, _p, _p, _i32, _i32, _i32, _p, _p, _p]
+        L.ubt_build_tree_best_first.argtypes = [_p, _p, _p, _i32, _i32, _i32, _i32, _f32, _p, _p, _p, _p, _p, _p, _p,
+                                                _p]
         L.ubt_tree_attention.argtypes = [_p, _p, _p, _p, _i64, _p, _p, _p, _p, _i32, _i32, _i32, _i32, _i32, _f32,
                                          _p, _i32, _p, _p]
         L.ubt_verify_accept.argtypes = [_p, _p, _p, _p, _i32, _i32, _p, _p, _p, _p]
@@ -90,7 +93,7 @@ def lib() -> ctypes.CDLL:
         L.ubt_tree_kl_loss.argtypes = [_p, _i32, _i32, _i32, _i64, _i64, _i64, _p, _p, _p, _i32, _p, _i64, _i64, _p,
                                        _p, _p, _p, _p, _i32, _i32, _p, _p, _f32, _f32, _p, _p, _p, _p, _p, _p]
         for f in (L.ubt_topk, L.ubt_bigram_scores, L.ubt_build_tree, L.ubt_draft_tree, L.ubt_tree_mask,
-                  L.ubt_draft_step, L.ubt_tree_attention, L.ubt_verify_accept, L.ubt_commit_kv, L.ubt_tree_kl_loss):
+                  L.ubt_draft_step, L.ubt_edge_scores, L.ubt_build_tree_best_first, L.ubt_tree_attention, L.ubt_verify_accept, L.ubt_commit_kv, L.ubt_tree_kl_loss):
             f.restype = _i32
         _lib = L
     return _lib
@@ -248,6 +251,48 @@ def draft_tree(phi: torch.Tensor, psi: torch.Tensor, gate: torch.Tensor, anchor:
                               _ptr(out["cand_rank"]), _ptr(out["score"]), _ptr(out.get("mask")), _stream(stream))
     _check("ubt_draft_tree", st)
     return {**out, "logq": logq}
+
+
+def edge_scores(phi: torch.Tensor, psi: torch.Tensor, gate: torch.Tensor, anchor: torch.Tensor,
+                cand_ids: torch.Tensor, cand_logprob: torch.Tensor, alpha, lam, out: dict | None = None,
+                with_delta: bool = False, stream=None) -> dict:
+    """``ubt_edge_scores``: unnormalised unigram-plus-bigram edge scores ``edge``
+    ``[B, gamma, K, K]`` (and ``delta`` if asked) from ``topk``'s log-probabilities."""
+    _need_gpu(phi, psi, gate, anchor, cand_ids, cand_logprob)
+    for n, t in (("phi", phi), ("psi", psi), ("gate", gate), ("anchor", anchor), ("cand_ids", cand_ids),
+                 ("cand_logprob", cand_logprob)):
+        _contig(t, n)
+    if not (phi.dtype == psi.dtype == gate.dtype):
+        raise TypeError("phi, psi and gate must share one dtype")
+    V, r = phi.shape
+    B, gamma, K = cand_ids.shape
+    dev = cand_ids.device
+    if out is None:
+        out = dict(delta=torch.empty(B, gamma, K, K, dtype=torch.float32, device=dev) if with_delta else None,
+                   edge=torch.empty(B, gamma, K, K, dtype=torch.float32, device=dev))
+    a, l = _host_f32(alpha, gamma), _host_f32(lam, gamma)
+    st = lib().ubt_edge_scores(_ptr(phi), _ptr(psi), _ptr(gate), _dtype_code(phi), V, r, _ptr(anchor), _ptr(cand_ids),
+                               _ptr(cand_logprob), a, l, B, gamma, K, _ptr(out.get("delta")), _ptr(out["edge"]),
+                               _stream(stream))
+    _check("ubt_edge_scores", st)
+    return out
+
+
+def build_tree_best_first(anchor: torch.Tensor, cand_ids: torch.Tensor, edge: torch.Tensor, budget: int,
+                          zeta: float = 0.0, out: dict | None = None, with_mask: bool = True, stream=None) -> dict:
+    """``ubt_build_tree_best_first``: the tree grown best-first under cumulative edge scores."""
+    _need_gpu(anchor, cand_ids, edge)
+    for n, t in (("anchor", anchor), ("cand_ids", cand_ids), ("edge", edge)):
+        _contig(t, n)
+    B, gamma, K = cand_ids.shape
+    if out is None:
+        out = tree_outputs(B, gamma, 1, budget, cand_ids.device, with_mask)
+    st = lib().ubt_build_tree_best_first(_ptr(anchor), _ptr(cand_ids), _ptr(edge), B, gamma, K, budget, float(zeta),
+                                         _ptr(out["n_nodes"]), _ptr(out["token"]), _ptr(out["parent"]),
+                                         _ptr(out["depth"]), _ptr(out["cand_rank"]), _ptr(out["score"]),
+                                         _ptr(out.get("mask")), _stream(stream))
+    _check("ubt_build_tree_best_first", st)
+    return out
 
 
 def tree_mask(parent: torch.Tensor, n_nodes: torch.Tensor, out: torch.Tensor | None = None,

@@ -252,6 +252,33 @@ ubt_status_t ubt_draft_step(const void* logits, ubt_dtype_t dt, int B, int gamma
                          token, parent, depth, cand_rank, score, mask, workspace, workspace_bytes, stream);
 }
 
+ubt_status_t ubt_edge_scores(const void* phi_tab, const void* psi_tab, const void* gate, ubt_dtype_t feat_dt,
+                             int64_t V, int r, const int32_t* anchor, const int32_t* cand_ids,
+                             const float* cand_logprob, const float* alpha, const float* lambda, int B, int gamma,
+                             int K, float* delta, float* edge, hipStream_t stream) {
+  if (!edge) return UBT_ERR_NULL;
+  ubt::Scales sc;
+  const ubt_status_t st = check_selector(phi_tab, psi_tab, gate, feat_dt, V, r, anchor, cand_ids, cand_logprob, alpha,
+                                         lambda, B, gamma, K, sc);
+  if (st != UBT_OK) return st;
+  return hip_status(ubt::launch_bigram(phi_tab, psi_tab, gate, static_cast<int>(feat_dt), V, r, anchor, cand_ids,
+                                       cand_logprob, sc, B, gamma, K, delta, edge, stream, false));
+}
+
+ubt_status_t ubt_build_tree_best_first(const int32_t* anchor, const int32_t* cand_ids, const float* edge, int B,
+                                       int gamma, int K, int budget, float zeta, int32_t* n_nodes, int32_t* token,
+                                       int32_t* parent, int32_t* depth, int32_t* cand_rank, float* score,
+                                       uint32_t* mask, hipStream_t stream) {
+  if (!edge) return UBT_ERR_NULL;
+  ubt::TreeArgs a;
+  // W does not apply to best-first growth; 1 passes the shared checks.
+  const ubt_status_t st = check_tree(anchor, cand_ids, B, gamma, K, 1, budget, zeta, n_nodes, token, parent, depth,
+                                     cand_rank, score, mask, a);
+  if (st != UBT_OK) return st;
+  a.logq = edge;
+  return hip_status(ubt::launch_best_first(a, stream));
+}
+
 ubt_status_t ubt_tree_mask(const int32_t* parent, const int32_t* n_nodes, int B, int N, uint32_t* mask,
                            hipStream_t stream) {
   if (!parent || !n_nodes || !mask) return UBT_ERR_NULL;

@@ -6,6 +6,9 @@
 // Delta_i = Phi_{i-1} diag(P(h_i)) Psi_i^T, with C_0 = {x_0} (one row at depth 1).
 // Method / Depth Calibration, Eq. (ubtree-depth): s_i = alpha_i u_i(b) + lambda_i delta_i.
 // Appendix A / Path Scores, Eq. (ubtree-path): log q^bi(b|a) = s_i(a,b) - log sum_v exp s_i(a,v).
+// Without the normalisation (normalise = false) the same kernels write s_i itself: the
+// edge scores of the unigram-plus-bigram scoring, given the candidates' log-probabilities
+// in place of their logits.
 //
 // One wavefront per (sequence, depth).  bf16 features: the rows of Phi and Psi are
 // gathered straight into MFMA operand registers (v_mfma_f32_16x16x32_bf16, 16x16 output
@@ -20,7 +23,7 @@
 namespace ubt {
 namespace {
 
-template <int KT>  // output tiles per side: K <= 16 * KT
+template <int KT, bool kNormalise>  // output tiles per side: K <= 16 * KT
 __global__ __launch_bounds__(kWave) void bigram_bf16_kernel(const uint16_t* __restrict__ phi,
                                                             const uint16_t* __restrict__ psi,
                                                             const uint16_t* __restrict__ gate, int64_t V, int r,
@@ -32,7 +35,7 @@ __global__ __launch_bounds__(kWave) void bigram_bf16_kernel(const uint16_t* __re
   const int64_t bi = blockIdx.x;  // b * gamma + i
   const int i = static_cast<int>(bi % gamma);
   const int64_t b = bi / gamma;
-  bigram_tile_bf16<KT>(phi, psi, gate + bi * r, V, r, i, K, anchor + b, i > 0 ? cand_ids + (bi - 1) * K : cand_ids, cand_ids + bi * K,
+  bigram_tile_bf16<KT, kNormalise>(phi, psi, gate + bi * r, V, r, i, K, anchor + b, i > 0 ? cand_ids + (bi - 1) * K : cand_ids, cand_ids + bi * K,
                        cand_logit + bi * K, sc.alpha[i], sc.lambda[i], delta ? delta + bi * K * K : nullptr,
                        logq + bi * K * K, nullptr, static_cast<int>(threadIdx.x));
 }
@@ -42,7 +45,8 @@ __global__ __launch_bounds__(kWave) void bigram_f32_kernel(const float* __restri
                                                            const int32_t* __restrict__ anchor,
                                                            const int32_t* __restrict__ cand_ids,
                                                            const float* __restrict__ cand_logit, Scales sc, int gamma,
-                                                           int K, float* __restrict__ delta, float* __restrict__ logq) {
+                                                           int K, float* __restrict__ delta, float* __restrict__ logq,
+                                                           int normalise) {
   __shared__ float s_delta[64 * 64];
   const int lane = threadIdx.x;
   const int64_t bi = blockIdx.x;
@@ -72,16 +76,19 @@ __global__ __launch_bounds__(kWave) void bigram_f32_kernel(const float* __restri
       }
       continue;
     }
-    float m = neg_inf();
-    for (int c = 0; c < K; ++c) m = fmaxf(m, fmaf(la, s_delta[a * K + c], al * cand_logit[bi * K + c]));
-    float e = 0.f;
-    for (int c = 0; c < K; ++c)
-      e += __builtin_amdgcn_exp2f((fmaf(la, s_delta[a * K + c], al * cand_logit[bi * K + c]) - m) * kLog2e);
-    const float norm = m + __builtin_amdgcn_logf(e) * kLn2;
+    float norm = 0.f;
+    if (normalise) {
+      float m = neg_inf();
+      for (int c = 0; c < K; ++c) m = fmaxf(m, fmaf(la, s_delta[a * K + c], al * cand_logit[bi * K + c]));
+      float e = 0.f;
+      for (int c = 0; c < K; ++c)
+        e += __builtin_amdgcn_exp2f((fmaf(la, s_delta[a * K + c], al * cand_logit[bi * K + c]) - m) * kLog2e);
+      norm = m + __builtin_amdgcn_logf(e) * kLn2;
+    }
     for (int c = 0; c < K; ++c) {
       const float s = fmaf(la, s_delta[a * K + c], al * cand_logit[bi * K + c]);
       if (dslab) dslab[a * K + c] = s_delta[a * K + c];
-      qslab[a * K + c] = fminf(s - norm, 0.f);
+      qslab[a * K + c] = normalise ? fminf(s - norm, 0.f) : s;
     }
   }
 }
@@ -90,26 +97,35 @@ __global__ __launch_bounds__(kWave) void bigram_f32_kernel(const float* __restri
 
 hipError_t launch_bigram(const void* phi, const void* psi, const void* gate, int feat_dtype, int64_t V, int r,
                          const int32_t* anchor, const int32_t* cand_ids, const float* cand_logit, const Scales& scales,
-                         int B, int gamma, int K, float* delta, float* logq, hipStream_t stream) {
+                         int B, int gamma, int K, float* delta, float* logq, hipStream_t stream, bool normalise) {
   const dim3 grid(static_cast<unsigned>(static_cast<int64_t>(B) * gamma));
   const dim3 block(kWave);
   if (feat_dtype == 1) {
     const uint16_t* p = static_cast<const uint16_t*>(phi);
     const uint16_t* s = static_cast<const uint16_t*>(psi);
     const uint16_t* g = static_cast<const uint16_t*>(gate);
-    if (K <= 16)
-      hipLaunchKernelGGL((bigram_bf16_kernel<1>), grid, block, 0, stream, p, s, g, V, r, anchor, cand_ids, cand_logit,
-                         scales, gamma, K, delta, logq);
-    else if (K <= 32)
-      hipLaunchKernelGGL((bigram_bf16_kernel<2>), grid, block, 0, stream, p, s, g, V, r, anchor, cand_ids, cand_logit,
-                         scales, gamma, K, delta, logq);
+#define UBT_BIGRAM_LAUNCH(KT, NORM)                                                                           \
+  hipLaunchKernelGGL((bigram_bf16_kernel<KT, NORM>), grid, block, 0, stream, p, s, g, V, r, anchor, cand_ids, \
+                     cand_logit, scales, gamma, K, delta, logq)
+#define UBT_BIGRAM_K(NORM)          \
+  do {                              \
+    if (K <= 16)                    \
+      UBT_BIGRAM_LAUNCH(1, NORM);   \
+    else if (K <= 32)               \
+      UBT_BIGRAM_LAUNCH(2, NORM);   \
+    else                            \
+      UBT_BIGRAM_LAUNCH(4, NORM);   \
+  } while (0)
+    if (normalise)
+      UBT_BIGRAM_K(true);
     else
-      hipLaunchKernelGGL((bigram_bf16_kernel<4>), grid, block, 0, stream, p, s, g, V, r, anchor, cand_ids, cand_logit,
-                         scales, gamma, K, delta, logq);
+      UBT_BIGRAM_K(false);
+#undef UBT_BIGRAM_K
+#undef UBT_BIGRAM_LAUNCH
   } else {
     hipLaunchKernelGGL(bigram_f32_kernel, grid, block, 0, stream, static_cast<const float*>(phi),
                        static_cast<const float*>(psi), static_cast<const float*>(gate), V, r, anchor, cand_ids,
-                       cand_logit, scales, gamma, K, delta, logq);
+                       cand_logit, scales, gamma, K, delta, logq, normalise ? 1 : 0);
   }
   return hipGetLastError();
 }

@@ -55,7 +55,10 @@ __device__ __forceinline__ void split_gated(u32x4 g, u32x4 p, u32x4& hi, u32x4& 
 // i = 0 only); pred_ids = C_{i-1} (read at i > 0 only); succ_ids / succ_logit = C_i and
 // its logits; g_row = P(h_i).  Writes delta (if dslab) and log q^bi to qslab and, if
 // given, qslab2, each [K][K] indexed [a][c].  All 64 lanes of the wave must call it.
-template <int KT>  // output tiles per side: K <= 16 * KT
+// kNormalise = false writes s_i(a, c) = al * succ_logit[c] + la * delta(a, c) itself,
+// with no normalisation over the successors (edge scores of the unigram-plus-bigram
+// scoring, where succ_logit holds the candidates' log-probabilities).
+template <int KT, bool kNormalise = true>  // output tiles per side: K <= 16 * KT
 __device__ __forceinline__ void bigram_tile_bf16(const uint16_t* __restrict__ phi, const uint16_t* __restrict__ psi,
                                                  const uint16_t* g_row, int64_t V, int r, int i, int K,
                                                  const int32_t* anchor, const int32_t* pred_ids,
@@ -134,19 +137,22 @@ __device__ __forceinline__ void bigram_tile_bf16(const uint16_t* __restrict__ ph
         s[nt] = c < K ? fmaf(la, acc[mt][nt][j], au[nt]) : neg_inf();
         m = fmaxf(m, s[nt]);
       }
-      m = group16_max(m);
-      float e = 0.f;
+      float norm = 0.f;
+      if (kNormalise) {
+        m = group16_max(m);
+        float e = 0.f;
 #pragma unroll
-      for (int nt = 0; nt < KT; ++nt) e += __builtin_amdgcn_exp2f((s[nt] - m) * kLog2e);
-      e = group16_sum(e);
-      const float norm = m + __builtin_amdgcn_logf(e) * kLn2;
+        for (int nt = 0; nt < KT; ++nt) e += __builtin_amdgcn_exp2f((s[nt] - m) * kLog2e);
+        e = group16_sum(e);
+        norm = m + __builtin_amdgcn_logf(e) * kLn2;
+      }
       const bool real = (i == 0) ? a == 0 : a < K;
       if (a < K) {
 #pragma unroll
         for (int nt = 0; nt < KT; ++nt) {
           const int c = 16 * nt + lr;
           if (c < K) {
-            const float q = real ? fminf(s[nt] - norm, 0.f) : 0.f;
+            const float q = real ? (kNormalise ? fminf(s[nt] - norm, 0.f) : s[nt]) : 0.f;
             if (dslab) dslab[a * K + c] = real ? acc[mt][nt][j] : 0.f;
             qslab[a * K + c] = q;
             if (qslab2) qslab2[a * K + c] = q;

@@ -316,6 +316,70 @@ __device__ __forceinline__ bool wait_slab(const FastSmem& sm, int i, uint64_t t0
   return wait_flag(&sm.ready[i], sm.fail, t0);
 }
 
+// Ancestor mask of a tree whose slots 0..n_nodes-1 are in `anc` (anc[n] = parent slot,
+// anc[0] = -1), by pointer jumping: after round k, a node's mask covers it and its
+// 2^k - 1 nearest ancestors and `up` points 2^k steps up; a chain of at most
+// max_depth + 1 nodes needs ceil(log2(max_depth + 1)) rounds.  Writes rows 0..N-1 of
+// mrow ([N, ceil(N/32)] words; rows >= n_nodes zero).  anc and mk (kMaxNodes rows of
+// kMaskWords words) are overwritten.  Run by one whole wavefront.
+__device__ __forceinline__ void ancestor_mask(int32_t* anc, uint32_t* mk, int n_nodes, int N, int max_depth,
+                                              uint32_t* mrow, int lane) {
+  const int words = (N + 31) / 32;
+  const int mrows = (N + kWave - 1) / kWave;  // <= 4
+  uint32_t m[4][kMaskWords];
+  int up[4];
+#pragma unroll
+  for (int rb = 0; rb < 4; ++rb) {
+    const int n = rb * kWave + lane;
+    const bool live = rb < mrows && n < n_nodes;
+    const int an = anc[n < n_nodes ? n : 0];
+    up[rb] = live ? an : -1;
+#pragma unroll
+    for (int w = 0; w < kMaskWords; ++w) m[rb][w] = (live && (n >> 5) == w) ? (1u << (n & 31)) : 0u;
+  }
+  int rounds = 0;
+  while ((1 << rounds) < max_depth + 1) ++rounds;
+  for (int it = 0; it < rounds; ++it) {
+#pragma unroll
+    for (int rb = 0; rb < 4; ++rb) {
+      const int n = rb * kWave + lane;
+      if (rb < mrows && n < n_nodes) {
+        uint4* dst = reinterpret_cast<uint4*>(mk + n * kMaskWords);
+        dst[0] = make_uint4(m[rb][0], m[rb][1], m[rb][2], m[rb][3]);
+        dst[1] = make_uint4(m[rb][4], m[rb][5], m[rb][6], m[rb][7]);
+        anc[n] = up[rb];
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+    for (int rb = 0; rb < 4; ++rb) {
+      if (rb < mrows && up[rb] >= 0) {
+        const uint4* src = reinterpret_cast<const uint4*>(mk + up[rb] * kMaskWords);
+        const uint4 lo = src[0], hi = src[1];
+        m[rb][0] |= lo.x;
+        m[rb][1] |= lo.y;
+        m[rb][2] |= lo.z;
+        m[rb][3] |= lo.w;
+        m[rb][4] |= hi.x;
+        m[rb][5] |= hi.y;
+        m[rb][6] |= hi.z;
+        m[rb][7] |= hi.w;
+        up[rb] = anc[up[rb]];
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+  }
+#pragma unroll
+  for (int rb = 0; rb < 4; ++rb) {
+    const int n = rb * kWave + lane;
+    if (rb < mrows && n < N) {
+#pragma unroll
+      for (int w = 0; w < kMaskWords; ++w)
+        if (w < words) mrow[n * words + w] = m[rb][w];
+    }
+  }
+}
+
 // Depth-wise expansion (Eq. ubtree-frontier): F_d = Top_W(E_d) for d = 1..gamma.  F_d is
 // ranked (score desc, parent position, candidate rank) as it is formed and stored in that
 // order to s_key / s_info (parent = its position in F_{d-1}), with the supertree outputs
@@ -518,64 +582,9 @@ __device__ __forceinline__ void fast_search(const TreeArgs& a, const FastSmem& s
   }
   __builtin_amdgcn_wave_barrier();
 
-  // ---- ancestor mask by pointer jumping ------------------------------------------------
-  // After round k, m covers the node and its 2^k - 1 nearest ancestors and `up` points
-  // 2^k steps up; a chain has at most gamma + 1 nodes.
   if (a.mask) {
-    const int mrows = (N + kWave - 1) / kWave;  // <= 4
-    uint32_t m[4][kMaskWords];
-    int up[4];
-#pragma unroll
-    for (int rb = 0; rb < 4; ++rb) {
-      const int n = rb * kWave + lane;
-      const bool live = rb < mrows && n < n_nodes;
-      const int an = sm.anc[n < n_nodes ? n : 0];
-      up[rb] = live ? an : -1;
-#pragma unroll
-      for (int w = 0; w < kMaskWords; ++w) m[rb][w] = (live && (n >> 5) == w) ? (1u << (n & 31)) : 0u;
-    }
-    int rounds = 0;
-    while ((1 << rounds) < gamma + 1) ++rounds;
-    for (int it = 0; it < rounds; ++it) {
-#pragma unroll
-      for (int rb = 0; rb < 4; ++rb) {
-        const int n = rb * kWave + lane;
-        if (rb < mrows && n < n_nodes) {
-          uint4* dst = reinterpret_cast<uint4*>(sm.mk + n * kMaskWords);
-          dst[0] = make_uint4(m[rb][0], m[rb][1], m[rb][2], m[rb][3]);
-          dst[1] = make_uint4(m[rb][4], m[rb][5], m[rb][6], m[rb][7]);
-          sm.anc[n] = up[rb];
-        }
-      }
-      __builtin_amdgcn_wave_barrier();
-#pragma unroll
-      for (int rb = 0; rb < 4; ++rb) {
-        if (rb < mrows && up[rb] >= 0) {
-          const uint4* src = reinterpret_cast<const uint4*>(sm.mk + up[rb] * kMaskWords);
-          const uint4 lo = src[0], hi = src[1];
-          m[rb][0] |= lo.x;
-          m[rb][1] |= lo.y;
-          m[rb][2] |= lo.z;
-          m[rb][3] |= lo.w;
-          m[rb][4] |= hi.x;
-          m[rb][5] |= hi.y;
-          m[rb][6] |= hi.z;
-          m[rb][7] |= hi.w;
-          up[rb] = sm.anc[up[rb]];
-        }
-      }
-      __builtin_amdgcn_wave_barrier();
-    }
     uint32_t* mrow = a.mask + b * static_cast<int64_t>(N) * words;
-#pragma unroll
-    for (int rb = 0; rb < 4; ++rb) {
-      const int n = rb * kWave + lane;
-      if (rb < mrows && n < N) {
-#pragma unroll
-        for (int w = 0; w < kMaskWords; ++w)
-          if (w < words) mrow[n * words + w] = m[rb][w];
-      }
-    }
+    ancestor_mask(sm.anc, sm.mk, n_nodes, N, gamma, mrow, lane);
   }
 }
 

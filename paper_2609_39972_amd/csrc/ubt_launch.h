@@ -21,7 +21,7 @@ struct Scales {
 hipError_t launch_bigram(const void* phi, const void* psi, const void* gate, int feat_dtype, int64_t V, int r,
                          const int32_t* anchor, const int32_t* cand_ids, const float* cand_logit,
                          const Scales& scales, int B, int gamma, int K, float* delta, float* logq,
-                         hipStream_t stream);
+                         hipStream_t stream, bool normalise = true);
 
 // ---- tree search --------------------------------------------------------------------
 struct TreeArgs {
@@ -44,6 +44,10 @@ struct TreeArgs {
   uint32_t* err;  // one-launch kernels: error word set when a wait inside the launch timed out (may be null)
 };
 hipError_t launch_build_tree(const TreeArgs& a, hipStream_t stream);
+
+// Best-first tree under cumulative edge scores (edge [B, gamma, K, K]); the tree outputs
+// of TreeArgs (logq = the edge scores; W and the supertree unused).
+hipError_t launch_best_first(const TreeArgs& a, hipStream_t stream);
 
 hipError_t launch_tree_mask(const int32_t* parent, const int32_t* n_nodes, int B, int N, uint32_t* mask,
                             hipStream_t stream);

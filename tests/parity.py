@@ -212,3 +212,82 @@ def record(label: str, counts: dict) -> None:
     if path:
         with open(path, "a") as fh:
             fh.write(json.dumps({"case": label, **counts, "failed": 0}) + "\n")
+
+
+def check_best_first(g: dict, ref: dict, edge: np.ndarray, cand_ids: np.ndarray, anchor: np.ndarray, budget: int,
+                     zeta: float = 0.0, seqs=None, allow_ties: bool = True) -> dict:
+    """Compares GPU trees grown best-first (all sequences in `g`, or `seqs` of them) with
+    the oracle's (`ref`, `edge` and `cand_ids` indexed like `seqs`).  Structure is exact:
+    parents precede children, depths, tokens and the mask match the parents.  A tree that
+    differs from the oracle's is validated step by step: each node the GPU added must be
+    a child of the nodes added before it and score within the tie gap of the best such
+    child (fp64 path sums).  Returns counts of exact and excused sequences."""
+    seqs = list(range(g["n_nodes"].shape[0])) if seqs is None else list(seqs)
+    counts = dict(exact=0, excused=0)
+    N = budget + 1
+    for j, b in enumerate(seqs):
+        n = int(g["n_nodes"][b])
+        assert n == int(ref["n_nodes"][j]), f"seq {b}: {n} nodes, oracle {int(ref['n_nodes'][j])}"
+        par, dep, cr, tok = g["parent"][b], g["depth"][b], g["cand_rank"][b], g["token"][b]
+        assert par[0] == -1 and dep[0] == 0 and tok[0] == anchor[j] and cr[0] == -1 and g["score"][b, 0] == 0
+        paths = [()]
+        for i in range(1, n):
+            p = int(par[i])
+            assert 0 <= p < i and dep[i] == dep[p] + 1 and 0 <= cr[i] < cand_ids.shape[-1]
+            assert tok[i] == cand_ids[j, dep[i] - 1, cr[i]], f"seq {b} slot {i}: token is not C_d[c]"
+            paths.append(paths[p] + (int(cr[i]),))
+        assert len(set(paths)) == n, f"seq {b}: a prefix appears twice"
+        assert (par[n:] == -1).all() and (tok[n:] == -1).all() and np.isneginf(g["score"][b, n:]).all()
+        if g.get("mask") is not None:
+            for i in range(N):
+                bits = _mask_bits(g["mask"][b, i], N)
+                anc, m = set(), i
+                while i < n and m >= 0:
+                    anc.add(m)
+                    m = int(par[m])
+                assert bits == anc, f"seq {b}: mask row {i} is not the ancestor set"
+        same = (np.array_equal(par, ref["parent"][j]) and np.array_equal(cr, ref["cand_rank"][j])
+                and np.array_equal(tok, ref["token"][j]))
+        if same:
+            for i in range(1, n):
+                sx, ax = _path_sum(edge[j], paths[i], zeta)
+                gs = float(g["score"][b, i])
+                assert abs(gs - float(ref["score"][j, i])) <= EPS * max(1.0, ax), \
+                    f"seq {b} slot {i}: GPU score {gs} vs {float(ref['score'][j, i])}"
+            counts["exact"] += 1
+            continue
+        if not allow_ties:
+            raise AssertionError(f"seq {b}: tree differs from the oracle and ties are not allowed here")
+        _guided_best_first(g, b, paths, edge[j], zeta)
+        counts["excused"] += 1
+    return counts
+
+
+def _path_sum(e: np.ndarray, path: tuple, zeta: float) -> tuple[float, float]:
+    """fp64 path score and the sum of its terms' magnitudes.  Edge scores can have either
+    sign, so a path sum may cancel; its fp32 rounding error is bounded relative to the sum
+    of magnitudes, which is what the best-first tolerance scales with (for edges <= 0 the
+    two coincide, as in the normalised scoring)."""
+    s, a, prev = 0.0, 0.0, 0
+    for i, c in enumerate(path):
+        t = float(e[i, prev, c])
+        s += t + zeta
+        a += abs(t) + abs(zeta)
+        prev = c
+    return s, a
+
+
+def _guided_best_first(g: dict, b: int, paths: list, e: np.ndarray, zeta: float) -> None:
+    gamma, K = e.shape[0], e.shape[2]
+    taken = {()}
+    for t, x in enumerate(paths[1:], start=1):
+        front = [p + (c,) for p in taken if len(p) < gamma for c in range(K) if p + (c,) not in taken]
+        scored = [_path_sum(e, f, zeta) for f in front]
+        bi = max(range(len(front)), key=lambda i: scored[i][0])
+        best, best_abs = scored[bi]
+        assert x in front, f"seq {b} slot {t}: {x} is not a child of the tree so far"
+        sx, ax = _path_sum(e, x, zeta)
+        assert sx >= best - EPS * max(1.0, best_abs, ax), f"seq {b} slot {t}: score {sx} below the best child {best}"
+        gs = float(g["score"][b, t])
+        assert abs(gs - sx) <= EPS * max(1.0, ax), f"seq {b} slot {t}: GPU score {gs} vs {sx}"
+        taken.add(x)
