@@ -247,6 +247,34 @@ ubt_status_t ubt_draft_step(const void* logits, ubt_dtype_t dt, int B, int gamma
                             float* score, uint32_t* mask, void* workspace, size_t workspace_bytes,
                             hipStream_t stream);
 
+/* ------------------------------------------------------------------------------------
+ * ubt_draft_step_noalloc -- ubt_draft_step for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same arguments without the workspace, the same checks, kernels and
+ * outputs.  It calls no hipMalloc, hipFree or allocating routine.
+ *
+ * The one-launch kernel's workspace is a static device array of the library
+ * (1,097,984 bytes, enough for every shape the one launch takes: B <= 64, gamma <= 64,
+ * K <= 16), one per device, held until the process ends; its address is looked up once
+ * per device on the first call there.  Each call first clears the error word and the row
+ * counters (a small fill kernel on `stream`), so a call never depends on what an earlier
+ * one left behind.  Calls that overlap on one device share that array and race: issue
+ * them on one stream (or otherwise order them).  A sequence whose bounded wait ran out
+ * of time (a stalled device) is written with n_nodes = 0.  A shape whose workspace would
+ * exceed the array returns UBT_ERR_WORKSPACE (the one-launch shapes never do); shapes the
+ * one launch does not take run the separate kernels, which need no workspace.
+ * ------------------------------------------------------------------------------------ */
+ubt_status_t ubt_draft_step_noalloc(const void* logits, ubt_dtype_t dt, int B, int gamma,
+                                    int64_t V, int64_t stride_b, int64_t stride_i, int K,
+                                    const void* phi_tab, const void* psi_tab, const void* gate,
+                                    ubt_dtype_t feat_dt, int r, const int32_t* anchor,
+                                    const float* alpha, const float* lambda, int W, int budget,
+                                    float zeta, int32_t* cand_ids, float* cand_logit,
+                                    float* cand_logprob, float* lse, float* logq, int32_t* n_nodes,
+                                    int32_t* token, int32_t* parent, int32_t* depth,
+                                    int32_t* cand_rank, float* score, uint32_t* mask,
+                                    hipStream_t stream);
+
 /* ====================================================================================
  * Unigram-plus-bigram scoring with best-first growth.  Each edge scores its successor's
  * unigram log-probability plus its raw selector score; a path ranks by the cumulative

@@ -39,7 +39,7 @@ STATUS = {0: "UBT_OK", 1: "UBT_ERR_NULL", 2: "UBT_ERR_SHAPE", 3: "UBT_ERR_VALUE"
 # Every symbol include/ubt.h declares.
 EXPORTS = ("ubt_status_str", "ubt_abi_version", "ubt_last_hip_error", "ubt_topk",
            "ubt_bigram_scores", "ubt_build_tree", "ubt_draft_tree", "ubt_draft_step_workspace_bytes",
-           "ubt_draft_step", "ubt_edge_scores", "ubt_build_tree_best_first", "ubt_tree_mask", "ubt_tree_attention", "ubt_verify_accept", "ubt_commit_kv",
+           "ubt_draft_step", "ubt_draft_step_noalloc", "ubt_edge_scores", "ubt_build_tree_best_first", "ubt_tree_mask", "ubt_tree_attention", "ubt_verify_accept", "ubt_commit_kv",
            "ubt_tree_kl_loss")
 
 _p = ctypes.c_void_p
@@ -83,6 +83,9 @@ def lib() -> ctypes.CDLL:
         L.ubt_draft_step.argtypes = [_p, _i32, _i32, _i32, _i64, _i64, _i64, _i32, _p, _p, _p, _i32, _i32, _p, _p,
                                      _p, _i32, _i32, _f32, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p,
                                      ctypes.c_size_t, _p]
+        L.ubt_draft_step_noalloc.argtypes = [_p, _i32, _i32, _i32, _i64, _i64, _i64, _i32, _p, _p, _p, _i32, _i32,
+                                             _p, _p, _p, _i32, _i32, _f32, _p, _p, _p, _p, _p, _p, _p, _p, _p, _p,
+                                             _p, _p, _p]
         L.ubt_edge_scores.argtypes = [_p, _p, _p, _i32, _i64, _i32, _p, _p, _p, _p, _p, _i32, _i32, _i32, _p, _p, _p]
         L.ubt_build_tree_best_first.argtypes = [_p, _p, _p, _i32, _i32, _i32, _i32, _f32, _p, _p, _p, _p, _p, _p, _p,
                                                 _p]
@@ -93,7 +96,7 @@ def lib() -> ctypes.CDLL:
         L.ubt_tree_kl_loss.argtypes = [_p, _i32, _i32, _i32, _i64, _i64, _i64, _p, _p, _p, _i32, _p, _i64, _i64, _p,
                                        _p, _p, _p, _p, _i32, _i32, _p, _p, _f32, _f32, _p, _p, _p, _p, _p, _p]
         for f in (L.ubt_topk, L.ubt_bigram_scores, L.ubt_build_tree, L.ubt_draft_tree, L.ubt_tree_mask,
-                  L.ubt_draft_step, L.ubt_edge_scores, L.ubt_build_tree_best_first, L.ubt_tree_attention, L.ubt_verify_accept, L.ubt_commit_kv, L.ubt_tree_kl_loss):
+                  L.ubt_draft_step, L.ubt_draft_step_noalloc, L.ubt_edge_scores, L.ubt_build_tree_best_first, L.ubt_tree_attention, L.ubt_verify_accept, L.ubt_commit_kv, L.ubt_tree_kl_loss):
             f.restype = _i32
         _lib = L
     return _lib
@@ -366,6 +369,42 @@ def draft_step(logits: torch.Tensor, phi: torch.Tensor, psi: torch.Tensor, gate:
                               _ptr(out["cand_rank"]), _ptr(out["score"]), _ptr(out.get("mask")), _ptr(workspace),
                               workspace.numel(), _stream(stream))
     _check("ubt_draft_step", st)
+    return {**cand, "logq": logq, **out}
+
+
+def draft_step_noalloc(logits: torch.Tensor, phi: torch.Tensor, psi: torch.Tensor, gate: torch.Tensor,
+                       anchor: torch.Tensor, alpha, lam, K: int, W: int, budget: int, zeta: float = 0.0,
+                       cand: dict | None = None, logq: torch.Tensor | None = None, out: dict | None = None,
+                       with_mask: bool = True, stream=None) -> dict:
+    """:func:`draft_step` through ``ubt_draft_step_noalloc``: no workspace argument; the
+    library's static per-device array serves the one-launch kernel.  Outputs are allocated
+    here unless given (pass them to allocate nothing)."""
+    _need_gpu(logits, phi, psi, gate, anchor)
+    if logits.dim() != 3 or logits.stride(2) != 1:
+        raise ValueError("logits must be [B, gamma, V] with unit stride along V")
+    for n, t in (("phi", phi), ("psi", psi), ("gate", gate), ("anchor", anchor)):
+        _contig(t, n)
+    B, gamma, V = logits.shape
+    r = phi.shape[1]
+    dev = logits.device
+    f32 = dict(dtype=torch.float32, device=dev)
+    if cand is None:
+        cand = dict(cand_ids=torch.empty(B, gamma, K, dtype=torch.int32, device=dev),
+                    cand_logit=torch.empty(B, gamma, K, **f32), cand_logprob=torch.empty(B, gamma, K, **f32),
+                    lse=torch.empty(B, gamma, **f32))
+    if logq is None:
+        logq = torch.empty(B, gamma, K, K, **f32)
+    if out is None:
+        out = tree_outputs(B, gamma, W, budget, dev, with_mask)
+    a, l = _host_f32(alpha, gamma), _host_f32(lam, gamma)
+    st = lib().ubt_draft_step_noalloc(_ptr(logits), _dtype_code(logits), B, gamma, V, logits.stride(0),
+                                      logits.stride(1), K, _ptr(phi), _ptr(psi), _ptr(gate), _dtype_code(phi), r,
+                                      _ptr(anchor), a, l, W, budget, float(zeta), _ptr(cand["cand_ids"]),
+                                      _ptr(cand["cand_logit"]), _ptr(cand.get("cand_logprob")), _ptr(cand.get("lse")),
+                                      _ptr(logq), _ptr(out["n_nodes"]), _ptr(out["token"]), _ptr(out["parent"]),
+                                      _ptr(out["depth"]), _ptr(out["cand_rank"]), _ptr(out["score"]),
+                                      _ptr(out.get("mask")), _stream(stream))
+    _check("ubt_draft_step_noalloc", st)
     return {**cand, "logq": logq, **out}
 
 

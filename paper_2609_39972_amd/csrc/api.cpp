@@ -185,15 +185,15 @@ size_t ubt_draft_step_workspace_bytes(int B, int gamma, int64_t V, int K, ubt_dt
 
 namespace {
 
-// ubt_draft_step: argument checks, then the one-launch kernel (with the caller's
-// workspace) or the separate kernels.
+// ubt_draft_step and ubt_draft_step_noalloc: the same checks and kernels; the one-launch
+// kernel's workspace is the caller's (use_static = false) or the library's static array.
 ubt_status_t draft_step_impl(const void* logits, ubt_dtype_t dt, int B, int gamma, int64_t V, int64_t stride_b,
                              int64_t stride_i, int K, const void* phi_tab, const void* psi_tab, const void* gate,
                              ubt_dtype_t feat_dt, int r, const int32_t* anchor, const float* alpha,
                              const float* lambda, int W, int budget, float zeta, int32_t* cand_ids, float* cand_logit,
                              float* cand_logprob, float* lse, float* logq, int32_t* n_nodes, int32_t* token,
                              int32_t* parent, int32_t* depth, int32_t* cand_rank, float* score, uint32_t* mask,
-                             void* workspace, size_t workspace_bytes, hipStream_t stream) {
+                             void* workspace, size_t workspace_bytes, bool use_static, hipStream_t stream) {
   if (!logits || !cand_ids || !cand_logit || !logq) return UBT_ERR_NULL;
   if (!valid_dtype(dt)) return UBT_ERR_VALUE;
   if (B < 1 || gamma < 1 || gamma > UBT_MAX_GAMMA || K < 1 || K > UBT_MAX_K || V < K || V >= (int64_t(1) << 31))
@@ -220,7 +220,15 @@ ubt_status_t draft_step_impl(const void* logits, ubt_dtype_t dt, int B, int gamm
                           stream);
   }
   const size_t need = ubt::step_workspace_bytes(B, gamma, V, K, static_cast<int>(dt));
-  if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0 || workspace_bytes < need) {
+  if (use_static) {
+    if (need > ubt::step_static_scratch_bytes()) return UBT_ERR_WORKSPACE;
+    st = hip_status(ubt::step_static_scratch(&workspace));
+    if (st != UBT_OK) return st;
+    // Every call starts from a clear error word and clear row counters, whatever an
+    // earlier call on this device left behind.
+    st = hip_status(ubt::clear_step_flags(workspace, B, gamma, stream));
+    if (st != UBT_OK) return st;
+  } else if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0 || workspace_bytes < need) {
     return UBT_ERR_WORKSPACE;
   }
   ubt::SelectorArgs s;
@@ -249,7 +257,20 @@ ubt_status_t ubt_draft_step(const void* logits, ubt_dtype_t dt, int B, int gamma
                             void* workspace, size_t workspace_bytes, hipStream_t stream) {
   return draft_step_impl(logits, dt, B, gamma, V, stride_b, stride_i, K, phi_tab, psi_tab, gate, feat_dt, r, anchor,
                          alpha, lambda, W, budget, zeta, cand_ids, cand_logit, cand_logprob, lse, logq, n_nodes,
-                         token, parent, depth, cand_rank, score, mask, workspace, workspace_bytes, stream);
+                         token, parent, depth, cand_rank, score, mask, workspace, workspace_bytes, false, stream);
+}
+
+ubt_status_t ubt_draft_step_noalloc(const void* logits, ubt_dtype_t dt, int B, int gamma, int64_t V,
+                                    int64_t stride_b, int64_t stride_i, int K, const void* phi_tab,
+                                    const void* psi_tab, const void* gate, ubt_dtype_t feat_dt, int r,
+                                    const int32_t* anchor, const float* alpha, const float* lambda, int W,
+                                    int budget, float zeta, int32_t* cand_ids, float* cand_logit,
+                                    float* cand_logprob, float* lse, float* logq, int32_t* n_nodes, int32_t* token,
+                                    int32_t* parent, int32_t* depth, int32_t* cand_rank, float* score,
+                                    uint32_t* mask, hipStream_t stream) {
+  return draft_step_impl(logits, dt, B, gamma, V, stride_b, stride_i, K, phi_tab, psi_tab, gate, feat_dt, r, anchor,
+                         alpha, lambda, W, budget, zeta, cand_ids, cand_logit, cand_logprob, lse, logq, n_nodes,
+                         token, parent, depth, cand_rank, score, mask, nullptr, 0, true, stream);
 }
 
 ubt_status_t ubt_edge_scores(const void* phi_tab, const void* psi_tab, const void* gate, ubt_dtype_t feat_dt,

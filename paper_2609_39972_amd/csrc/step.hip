@@ -42,6 +42,8 @@
 // Sweep workgroups never wait.  Searcher waves wait only on counters that sweep
 // workgroups of the same launch raise unconditionally, each wait bounded in time; the
 // searcher that read a counter resets it, leaving the workspace ready for the next call.
+#include <mutex>
+
 #include "bigram_tile.h"
 #include "search.h"
 #include "sweep.h"
@@ -288,9 +290,58 @@ PipeWorkspace pipe_workspace(int B, int gamma, int64_t V, int K, int dtype) {
   return w;
 }
 
+// Largest workspace of the one-launch shapes: B <= kMaxStepSequences, gamma <= 64 and
+// K <= 16 with at most kPipeMaxChunks chunks per row (V and the dtype do not change it).
+constexpr size_t kStaticRows = static_cast<size_t>(kMaxStepSequences) * 64;
+constexpr size_t kStaticScratchBytes = kCountBase + ((kStaticRows * 4 + 255) & ~size_t(255)) +
+                                       2 * ((kStaticRows * kPipeMaxChunks * 16 * 4 + 255) & ~size_t(255)) +
+                                       ((kStaticRows * kPipeMaxChunks * 4 + 255) & ~size_t(255));
+
+// The allocation-free variant's workspace: one array per device, held until the process
+// ends.  Host code never passes this name to a kernel (on the host it is only a stand-in
+// for the symbol); it uses the device address hipGetSymbolAddress returns for the device.
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Zero-fills n 32-bit words (a fill kernel rather than a memset, so graph capture records
+// a kernel node).
+__global__ void zero_words_kernel(uint32_t* __restrict__ p, int n) {
+  const int i = static_cast<int>(blockIdx.x * blockDim.x + threadIdx.x);
+  if (i < n) p[i] = 0u;
+}
+
 }  // namespace
 
 // ---- host side ------------------------------------------------------------------------------
+size_t step_static_scratch_bytes() { return kStaticScratchBytes; }
+
+hipError_t step_static_scratch(void** ptr) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return hipSuccess;
+}
+
+hipError_t clear_step_flags(void* workspace, int B, int gamma, hipStream_t stream) {
+  // The error word (and the rest of the first 256 bytes) and one counter per row.
+  const int words = static_cast<int>(kCountBase / 4) + B * gamma;
+  hipLaunchKernelGGL(zero_words_kernel, dim3(static_cast<unsigned>((words + 255) / 256)), dim3(256), 0, stream,
+                     static_cast<uint32_t*>(workspace), words);
+  return hipGetLastError();
+}
+
 size_t step_workspace_bytes(int B, int gamma, int64_t V, int K, int dtype) {
   return pipe_workspace(B, gamma, V, K, dtype).total;
 }

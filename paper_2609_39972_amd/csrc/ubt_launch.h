@@ -81,6 +81,13 @@ hipError_t launch_draft_step(const void* logits, int dtype, int B, int gamma, in
                              int64_t stride_i, int K, int32_t* cand_ids, float* cand_logit, float* cand_logprob,
                              float* lse, const SelectorArgs& s, const TreeArgs& a, void* workspace,
                              hipStream_t stream);
+// The allocation-free variant's workspace: a static device array of
+// step_static_scratch_bytes() bytes per device; *ptr receives its address on the current
+// device (looked up once per device).
+size_t step_static_scratch_bytes();
+hipError_t step_static_scratch(void** ptr);
+// Zero-fills the error word and the B * gamma row counters of a step workspace.
+hipError_t clear_step_flags(void* workspace, int B, int gamma, hipStream_t stream);
 
 // ---- verification: tree attention, acceptance walk, KV commit -------------------------
 struct TreeAttnArgs {
