@@ -494,17 +494,15 @@ __device__ __forceinline__ void expand_depths(const TreeArgs& a, const FastSmem&
   }
 }
 
-// Algorithm 1 for sequence b, run by one wavefront once the sequence's candidate ids are
-// in LDS and, unless kWait, all its score slabs; with kWait the slab of position i is
-// awaited before depth i + 1 first reads it.
-template <int KT, int R, bool kWait>
-__device__ __forceinline__ void fast_search(const TreeArgs& a, const FastSmem& sm, int64_t b, int lane,
-                                            uint64_t magic_w) {
+// Global pruning (Eq. ubtree-pruning), emission and the mask, once the supertree's keys
+// and infos are in s_key / s_info (F_d in rank order at (d - 1) * W + rank) and `total`
+// counts its nodes.  With kCheckFail, a wait of the workgroup that ran out of time marks
+// the sequence with n_nodes = 0 and sets the launch's error word.
+template <int KT, bool kCheckFail>
+__device__ __forceinline__ void finish_tree(const TreeArgs& a, const FastSmem& sm, int64_t b, int lane,
+                                            uint64_t magic_w, int total) {
   const int gamma = a.gamma, W = a.W;
   const int GW = gamma * W;
-
-  int total = 0;
-  expand_depths<KT, R, kWait>(a, sm, b, lane, total);
 
   // ---- global pruning: Top_budget over the supertree --------------------------------
   const int n_sel = total < a.budget ? total : a.budget;
@@ -543,8 +541,8 @@ __device__ __forceinline__ void fast_search(const TreeArgs& a, const FastSmem& s
   // that were never published behind the tree: the sequence is then marked with
   // n_nodes = 0, and the launch's error word is set if it has one.
   const bool failed =
-      kWait && __builtin_amdgcn_readfirstlane(__hip_atomic_load(sm.fail, __ATOMIC_RELAXED,
-                                                                __HIP_MEMORY_SCOPE_WORKGROUP)) != 0u;
+      kCheckFail && __builtin_amdgcn_readfirstlane(__hip_atomic_load(sm.fail, __ATOMIC_RELAXED,
+                                                                     __HIP_MEMORY_SCOPE_WORKGROUP)) != 0u;
   if (lane == 0) {
     a.n_nodes[b] = failed ? 0 : n_nodes;
     if (failed && a.err) __hip_atomic_store(a.err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -586,6 +584,17 @@ __device__ __forceinline__ void fast_search(const TreeArgs& a, const FastSmem& s
     uint32_t* mrow = a.mask + b * static_cast<int64_t>(N) * words;
     ancestor_mask(sm.anc, sm.mk, n_nodes, N, gamma, mrow, lane);
   }
+}
+
+// Algorithm 1 for sequence b, run by one wavefront once the sequence's candidate ids are
+// in LDS and, unless kWait, all its score slabs; with kWait the slab of position i is
+// awaited before depth i + 1 first reads it.
+template <int KT, int R, bool kWait>
+__device__ __forceinline__ void fast_search(const TreeArgs& a, const FastSmem& sm, int64_t b, int lane,
+                                            uint64_t magic_w) {
+  int total = 0;
+  expand_depths<KT, R, kWait>(a, sm, b, lane, total);
+  finish_tree<KT, kWait>(a, sm, b, lane, magic_w, total);
 }
 
 }  // namespace

@@ -45,6 +45,7 @@
 #include <mutex>
 
 #include "bigram_tile.h"
+#include "pipe_search.h"
 #include "search.h"
 #include "sweep.h"
 #include "ubt_launch.h"
@@ -124,6 +125,7 @@ __device__ __forceinline__ bool wait_count(const uint32_t* f, uint32_t n, uint64
 
 struct SearcherLayout {
   FastLayout fast;
+  PipeSearchLayout pipe;
   uint32_t clogit, rready, mstage, total;
 };
 
@@ -137,7 +139,8 @@ __host__ __device__ inline SearcherLayout searcher_layout(int gamma, int K, int 
   q += static_cast<uint32_t>((gamma * sizeof(uint32_t) + 15) & ~static_cast<size_t>(15));
   L.mstage = q;  // one 64-entry order-value stage per wave
   q += static_cast<uint32_t>(kPipeWaves * kWave * sizeof(uint64_t));
-  L.total = q;
+  L.pipe = pipe_search_layout(q, gamma);
+  L.total = L.pipe.total;
   return L;
 }
 
@@ -188,33 +191,21 @@ __device__ __forceinline__ void merge_chunks(const PipeArgs& p, int64_t row, int
   if (lane == 0 && p.lse) p.lse[row] = lse;
 }
 
-// One sequence's merges, selector slabs and tree search.  Wave 0 searches; waves 1..
-// take the positions round-robin: they wait for the position's chunks, merge them,
-// compute the slab once the predecessor position's candidates are in, and publish it to
-// the search wave.
-template <typename T, int KT, int R>
-__device__ __forceinline__ void searcher(const PipeArgs& p, const TreeArgs& a, const SelectorArgs& s,
-                                         uint64_t magic_w, unsigned char* smem, int w, int nw, int lane) {
+// A helper wave's positions, w - 1, w - 1 + (nw - 2), ...: it waits for the position's
+// chunks, merges them, computes the slab once the predecessor position's candidates are
+// in, and publishes it to the search wave.
+template <typename T, int KT>
+__device__ __forceinline__ void helper_slabs(const PipeArgs& p, const TreeArgs& a, const SelectorArgs& s,
+                                             const FastSmem& sm, unsigned char* smem, const SearcherLayout& L, int w,
+                                             int nw, int lane) {
   const int b = static_cast<int>(blockIdx.x);
   const int gamma = a.gamma;
-  const SearcherLayout L = searcher_layout(gamma, KT, a.W);
-  const FastSmem sm = fast_smem(smem, L.fast);
   float* clogit = reinterpret_cast<float*>(smem + L.clogit);
   uint32_t* rready = reinterpret_cast<uint32_t*>(smem + L.rready);
   uint64_t* stage = reinterpret_cast<uint64_t*>(smem + L.mstage) + w * kWave;
-  for (int e = static_cast<int>(threadIdx.x); e < gamma; e += static_cast<int>(blockDim.x)) {
-    sm.ready[e] = 0u;
-    rready[e] = 0u;
-  }
-  if (threadIdx.x == 0) *sm.fail = 0u;
-  __syncthreads();
-  __builtin_amdgcn_s_setprio(3);
-  if (w == 0) {
-    fast_search<KT, R, true>(a, sm, b, lane, magic_w);
-    return;
-  }
+  const int helpers = nw - 2;
   const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
-  for (int i = w - 1; i < gamma; i += nw - 1) {
+  for (int i = w - 1; i < gamma; i += helpers) {
     const int64_t bi = static_cast<int64_t>(b) * gamma + i;
     if (!wait_count(&p.count[bi], static_cast<uint32_t>(p.chunks), t0) && lane == 0) {
       store_agent32(p.err, 1u);
@@ -234,6 +225,37 @@ __device__ __forceinline__ void searcher(const PipeArgs& p, const TreeArgs& a, c
 #pragma unroll
     for (int e = lane; e < KT * KT; e += kWave) gq[e] = slab[e];
   }
+}
+
+// One sequence's merges, selector slabs and tree search.  Wave 0 runs the depth-wise
+// expansion, the last wave ranks each frontier and stores it, and the waves between take
+// the positions round-robin (helper_slabs).  Then all waves prune, emit and build the mask
+// together.
+template <typename T, int KT, int R>
+__device__ __forceinline__ void searcher(const PipeArgs& p, const TreeArgs& a, const SelectorArgs& s,
+                                         uint64_t magic_w, unsigned char* smem, int w, int nw, int lane) {
+  const int b = static_cast<int>(blockIdx.x);
+  const int gamma = a.gamma;
+  const SearcherLayout L = searcher_layout(gamma, KT, a.W);
+  const FastSmem sm = fast_smem(smem, L.fast);
+  const PipeSearchSmem ps = pipe_search_smem(smem, L.pipe);
+  uint32_t* rready = reinterpret_cast<uint32_t*>(smem + L.rready);
+  for (int e = static_cast<int>(threadIdx.x); e < gamma; e += static_cast<int>(blockDim.x)) {
+    sm.ready[e] = 0u;
+    rready[e] = 0u;
+    ps.stage_ready[e] = 0u;
+    ps.rank_ready[e] = 0u;
+  }
+  if (threadIdx.x == 0) *sm.fail = 0u;
+  __syncthreads();
+  __builtin_amdgcn_s_setprio(3);
+  if (w == 0)
+    pipe_search_wave<KT, R>(a, sm, ps, lane);
+  else if (w == nw - 1)
+    pipe_prune_wave<KT>(a, sm, ps, lane);
+  else
+    helper_slabs<T, KT>(p, a, s, sm, smem, L, w, nw, lane);
+  finish_tree_coop<KT>(a, sm, ps, b, w, nw, lane, magic_w);
 }
 
 // Workgroups 0..B-1 search; workgroup B + t sweeps work item t.
