@@ -287,3 +287,22 @@ def loss_inputs(w: Workload, buf: int = 0, invalid_frac: float = 0.05) -> dict:
             y[row] = int(rng.integers(0, w.V))
     y[rng.random(w.rows) < invalid_frac] = -1
     return dict(target_logits=z.reshape(w.B, w.gamma, w.V), y_star=y.reshape(w.B, w.gamma))
+
+
+# ---- LM-head inputs ---------------------------------------------------------------------
+F_LMH, F_LMW = 40, 41
+
+
+def lm_head_inputs(seed: int, M: int, d: int, V: int, logit_std: float = 3.0) -> dict:
+    """Synthetic operands of the LM-head projection as bf16 bit patterns (uint16): hidden
+    states ``h [M, d]`` i.i.d. N(0, 1) (unit scale, as after the proposer's final
+    normalisation) and a head ``W [V, d]`` i.i.d. N(0, logit_std^2 / d), so each logit is
+    roughly N(0, logit_std^2).  W is drawn in blocks of rows to bound memory."""
+    h = round_bf16_bits(_rng(seed, F_LMH).normal(0.0, 1.0, size=(M, d)))
+    w = np.empty((V, d), np.uint16)
+    sd = logit_std / math.sqrt(d)
+    block = 8192
+    for i, v0 in enumerate(range(0, V, block)):
+        n = min(block, V - v0)
+        w[v0:v0 + n] = round_bf16_bits(_rng(seed, F_LMW, i).normal(0.0, sd, size=(n, d)))
+    return dict(h=h, w=w)
