@@ -47,6 +47,8 @@ VERIFY_PROFILE = os.path.join(ROOT, "profiles", "tree_attention_verify-b32-n65-p
 VERIFY_SOURCES = ("verify.hip", "ubt_device.h")
 LOSS_PROFILE = os.path.join(ROOT, "profiles", "kl_loss_zipf-v151936-b32.md")
 LOSS_SOURCES = ("loss.hip", "ubt_device.h")
+LMHEAD_PROFILE = os.path.join(ROOT, "profiles", "lm_head_topk_m15-d2560-v151936-k64.md")
+LMHEAD_SOURCES = ("lmhead.hip", "search.h", "bigram_tile.h", "ubt_device.h")
 
 
 def source_hash(files=SWEEP_SOURCES) -> str:
@@ -392,6 +394,129 @@ def bench_loss(args, dev) -> int:
     return 0
 
 
+def bench_lmhead(args, dev) -> int:
+    """The LM-head projection fused with the candidate sets (ubt_lm_head_topk) at the
+    drafting block of the paper's latency breakdown: 15 draft positions of one sequence,
+    hidden size 2560 (Qwen3-4B), V = 151936, K = 64, bf16.  Timed beside the library path
+    (hipBLASLt GEMM writing bf16 logits, then ubt_topk) and inside the whole batch-1
+    post-processing (ubt_lm_head_topk then ubt_draft_tree with W = 12, budget 64, rank
+    256).  The head (778 MB) exceeds the 256 MB last-level cache, so every call streams
+    it from HBM."""
+    import numpy as np
+    import torch
+
+    import paper_2609_39972_amd as ubt
+    import synth
+
+    M, d, V, K = args.lm_rows, args.lm_hidden, 151936, 64
+    t0 = time.perf_counter()
+    x = synth.lm_head_inputs(0, M, d, V)
+    log(f"inputs M={M} d={d} V={V}: {time.perf_counter() - t0:.1f} s")
+    h = ubt.bf16_tensor_from_bits(x["h"], dev)
+    wt = ubt.bf16_tensor_from_bits(x["w"], dev)
+    ws = ubt.lm_head_workspace(M, d, V, K, dev)
+    stream = torch.cuda.Stream(device=dev)
+    out = ubt.lm_head_topk(h, wt, K, workspace=ws)
+    torch.cuda.synchronize()
+
+    def timed(fn, n=50, replays=4):
+        with torch.cuda.stream(stream):
+            fn()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=stream):
+            for _ in range(n):
+                fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        with torch.cuda.stream(stream):
+            g.replay()
+            a.record(stream)
+            for _ in range(replays):
+                g.replay()
+            b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) * 1e3 / (n * replays)
+
+    fused_us = timed(lambda: ubt.lm_head_topk(h, wt, K, out=out, workspace=ws, stream=stream))
+    logits = torch.empty(1, M, V, dtype=torch.bfloat16, device=dev)
+    lib_out = ubt.topk(logits, K)
+
+    def library():
+        torch.matmul(h, wt.t(), out=logits[0])
+        ubt.topk(logits, K, out=lib_out, stream=stream)
+
+    gemm_us = timed(lambda: torch.matmul(h, wt.t(), out=logits[0]))
+    lib_us = timed(library)
+    # The whole batch-1 post-processing: candidates, selector scores and the tree.
+    w6 = synth.WORKLOADS[6]
+    gate = ubt.bf16_tensor_from_bits(synth.gate(w6, 0)[:1, :M], dev).contiguous()
+    anchor = torch.from_numpy(synth.anchor(w6, 0)[:1].copy()).to(dev)
+    phi_b, psi_b = synth.tables(w6)
+    phi, psi = ubt.bf16_tensor_from_bits(phi_b, dev), ubt.bf16_tensor_from_bits(psi_b, dev)
+    alpha, lam = synth.calibration(w6)
+    alpha, lam = alpha[:M], lam[:M]
+    cand3 = {k: v.view(1, M, *v.shape[1:]) for k, v in out.items() if v is not None}
+    tree = ubt.tree_outputs(1, M, w6.W, w6.budget, dev)
+    logq = torch.empty(1, M, K, K, dtype=torch.float32, device=dev)
+
+    def chain():
+        ubt.lm_head_topk(h, wt, K, out=out, workspace=ws, stream=stream)
+        ubt.draft_tree(phi, psi, gate, anchor, cand3["cand_ids"], cand3["cand_logit"], alpha, lam, w6.W, w6.budget,
+                       logq=logq, out=tree, stream=stream)
+
+    chain_us = timed(chain) if M <= w6.gamma else None
+    alg_bytes = V * d * 2 + M * d * 2 + M * K * 12 + M * 4
+    gbps = alg_bytes / (fused_us * 1e-6) / 1e9
+    tflops = 2.0 * M * V * d / (fused_us * 1e-6) / 1e12
+    log(f"fused {fused_us:.2f} us ({gbps:.0f} GB/s of the head, {tflops:.1f} TFLOP/s); library GEMM {gemm_us:.2f} "
+        f"us, GEMM + ubt_topk {lib_us:.2f} us; batch-1 post-processing {chain_us} us")
+    # Parity of the timed outputs against the oracle, and the oracle on the host.
+    parity_counts, cpu = None, None
+    if not args.no_cpu_baseline:
+        sys.path.insert(0, os.path.join(ROOT, "tests"))
+        import parity as par
+        from oracle import lm_head as LH
+
+        torch.cuda.synchronize()
+        g = {k: v.cpu().numpy() for k, v in out.items() if v is not None}
+        c = par.check_lm_head(g, x["h"], x["w"], K)
+        parity_counts = {"rows": M, "exact": c["exact"], "excused": c["excused"], "failed": 0}
+        t0, reps = time.perf_counter(), 0
+        while True:
+            LH.lm_head_topk(x["h"], x["w"], K)
+            reps += 1
+            if time.perf_counter() - t0 >= args.cpu_seconds:
+                break
+        el = time.perf_counter() - t0
+        cpu = {"value": round(reps / el, 4), "unit": "blocks/s", "cores": torch.get_num_threads(),
+               "kind": "oracle", "cpu_model": cpu_model(), "host_cpus": os.cpu_count(),
+               "sample": f"{reps} whole calls (M={M}, d={d}, V={V}, K={K}): fp64 numpy matmul in blocks of "
+                         f"8192 head rows, then the candidate sets; {el:.1f} s"}
+    res = {
+        "metric": f"LM head + candidate sets us/call at M={M}, d={d}, V={V}, K={K} (bf16)",
+        "value": round(1e6 / fused_us, 1), "unit": "blocks/s", "n_gpus": 1, "steps": 200, "warmup": 50,
+        "ms_per_step": round(fused_us / 1e3, 6), "us_per_step": round(fused_us, 3), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"lm-head-m{M}-d{d}-v{V}-k{K}", "M": M, "d": d, "V": V, "K": K},
+        "kernels_us": {"ubt_lm_head_topk": round(fused_us, 3), "library_gemm_bf16_logits": round(gemm_us, 3),
+                       "library_gemm_plus_ubt_topk": round(lib_us, 3),
+                       "post_processing_batch1 (lm_head_topk + draft_tree W=12 budget=64 r=256)":
+                           None if chain_us is None else round(chain_us, 3)},
+        "speedup_vs_library": round(lib_us / fused_us, 3),
+        "roofline": {"bound": "hbm", "kernel": "lm_head_stream_kernel + lm_head_merge_kernel (whole call)",
+                     "achieved": round(gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(gbps / HBM_PEAK_GBPS, 4),
+                     "traffic": (measured_traffic(LMHEAD_PROFILE, LMHEAD_SOURCES) or {}).get("bytes"),
+                     "algorithmic_bytes_per_launch": alg_bytes, "mfma_tflops": round(tflops, 2),
+                     "mfma_frac_bf16": round(tflops / 2500.0, 5)},
+        "parity": parity_counts,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(res), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -400,10 +525,12 @@ def main() -> int:
     ap.add_argument("--workload", type=int, default=3, help="synthetic workload id (3 = B=32, V=151936 headline)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="minimum oracle time for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--mode", choices=("step", "tree", "separate", "verify", "loss"), default="step",
+    ap.add_argument("--mode", choices=("step", "tree", "separate", "verify", "loss", "lmhead"), default="step",
                     help="step: one ubt_draft_step call; tree: ubt_topk + ubt_draft_tree; separate: ubt_topk + "
                          "ubt_bigram_scores + ubt_build_tree; verify: tree verification; loss: the training "
-                         "objective (each its own JSON line)")
+                         "objective; lmhead: the LM head fused with the candidate sets (each its own JSON line)")
+    ap.add_argument("--lm-rows", type=int, default=15, help="lmhead mode: rows of h (draft positions)")
+    ap.add_argument("--lm-hidden", type=int, default=2560, help="lmhead mode: hidden size d")
     ap.add_argument("--sweep-launches", type=int, default=200, help="launches per kernel in the per-kernel timing")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run a plain device copy of known size (counter calibration) and exit")
@@ -436,6 +563,8 @@ def main() -> int:
         return bench_verify(args, dev)
     if args.mode == "loss":
         return bench_loss(args, dev)
+    if args.mode == "lmhead":
+        return bench_lmhead(args, dev)
 
     w = synth.WORKLOADS[args.workload]
     pool = max(1, -(-POOL_BYTES // w.logit_bytes))

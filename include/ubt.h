@@ -7,6 +7,7 @@
  * of L positions includes the anchor x_0).  The calls run in this order:
  *
  *   ubt_topk           per row: softmax statistics and the top-K candidate set C_i
+ *   ubt_lm_head_topk   the same from hidden states and the LM head, logits kept on chip
  *   ubt_bigram_scores  per (b, depth): selector scores Delta_i and normalised log q^bi
  *   ubt_build_tree     per sequence: beam search + global pruning -> tree and mask
  *   ubt_tree_mask      (optional) the ancestor mask of any parent-pointer tree
@@ -106,6 +107,37 @@ int ubt_last_hip_error(void);
 ubt_status_t ubt_topk(const void* logits, ubt_dtype_t dt, int B, int gamma, int64_t V,
                       int64_t stride_b, int64_t stride_i, int K, int32_t* cand_ids,
                       float* cand_logit, float* cand_logprob, float* lse, hipStream_t stream);
+
+/* ------------------------------------------------------------------------------------
+ * ubt_lm_head_topk -- the LM-head projection followed by ubt_topk's outputs, without
+ * writing the logits.  Background, "DFlash & DFlash 2": the proposer's hidden state h_i
+ * is mapped to its logits by the frozen target LM head, u_i = W_lm h_i.  Method /
+ * Unigram Proposer, Eq. (ubtree-unigram) and "Candidate Sets": LSE_i and C_i as for
+ * ubt_topk.
+ *
+ * h        : bf16 [M, d] row-major, the hidden states (M = rows over all sequences and
+ *            positions, e.g. B * gamma), 16-byte aligned.
+ * w_lm     : bf16 [V, d] row-major, the LM head (one row per token), 16-byte aligned.
+ * M, d, V  : M >= 1; d % 32 == 0, 32 <= d <= 65536; K <= V < 2^31.
+ * K        : candidates per row, 1 <= K <= UBT_MAX_K.
+ * cand_ids : int32 [M, K]  token ids ordered by (logit desc, id asc).
+ * cand_logit : float [M, K] the candidates' logits, fp32 sums of the exact bf16
+ *            products (accumulation order unspecified).
+ * cand_logprob : float [M, K] logit - lse; may be NULL.   lse : float [M]; may be NULL.
+ * workspace, ws_bytes : device scratch of at least ubt_lm_head_topk_workspace_bytes(M, d,
+ *            V, K) bytes, 256-byte aligned, owned by the caller; no state is kept in it
+ *            between calls, and calls that share it must not overlap.
+ * The head is read once per 16 rows of h (rows are taken 16 at a time); each pass is
+ * bound by the bandwidth of reading w_lm.  Inputs must be finite; non-finite logits
+ * give unspecified candidates.  Returns UBT_ERR_WORKSPACE for a missing, small or
+ * misaligned workspace, UBT_ERR_UNSUPPORTED for shapes the workspace query rejects
+ * (it returns 0 for them: very large V at large K).
+ * ------------------------------------------------------------------------------------ */
+size_t ubt_lm_head_topk_workspace_bytes(int M, int d, int64_t V, int K);
+ubt_status_t ubt_lm_head_topk(const void* h, const void* w_lm, int M, int d, int64_t V, int K,
+                              int32_t* cand_ids, float* cand_logit, float* cand_logprob,
+                              float* lse, void* workspace, size_t ws_bytes,
+                              hipStream_t stream);
 
 /* ------------------------------------------------------------------------------------
  * ubt_bigram_scores -- selector scores and normalised transition log-probabilities.

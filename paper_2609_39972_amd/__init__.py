@@ -38,7 +38,7 @@ STATUS = {0: "UBT_OK", 1: "UBT_ERR_NULL", 2: "UBT_ERR_SHAPE", 3: "UBT_ERR_VALUE"
 
 # Every symbol include/ubt.h declares.
 EXPORTS = ("ubt_status_str", "ubt_abi_version", "ubt_last_hip_error", "ubt_topk",
-           "ubt_bigram_scores", "ubt_build_tree", "ubt_draft_tree", "ubt_draft_step_workspace_bytes",
+           "ubt_lm_head_topk_workspace_bytes", "ubt_lm_head_topk", "ubt_bigram_scores", "ubt_build_tree", "ubt_draft_tree", "ubt_draft_step_workspace_bytes",
            "ubt_draft_step", "ubt_draft_step_noalloc", "ubt_edge_scores", "ubt_build_tree_best_first", "ubt_tree_mask", "ubt_tree_attention", "ubt_verify_accept", "ubt_commit_kv",
            "ubt_tree_kl_loss")
 
@@ -71,6 +71,9 @@ def lib() -> ctypes.CDLL:
         L.ubt_abi_version.restype = _i32
         L.ubt_last_hip_error.restype = _i32
         L.ubt_topk.argtypes = [_p, _i32, _i32, _i32, _i64, _i64, _i64, _i32, _p, _p, _p, _p, _p]
+        L.ubt_lm_head_topk_workspace_bytes.argtypes = [_i32, _i32, _i64, _i32]
+        L.ubt_lm_head_topk_workspace_bytes.restype = ctypes.c_size_t
+        L.ubt_lm_head_topk.argtypes = [_p, _p, _i32, _i32, _i64, _i32, _p, _p, _p, _p, _p, ctypes.c_size_t, _p]
         L.ubt_bigram_scores.argtypes = [_p, _p, _p, _i32, _i64, _i32, _p, _p, _p, _p, _p, _i32, _i32, _i32, _p, _p,
                                         _p]
         L.ubt_build_tree.argtypes = [_p, _p, _p, _i32, _i32, _i32, _i32, _i32, _f32, _p, _p, _p, _p, _p, _p, _p,
@@ -95,7 +98,7 @@ def lib() -> ctypes.CDLL:
         L.ubt_commit_kv.argtypes = [_p, _p, _p, _p, _p, _p, _p, _i32, _i32, _i32, _i32, _i64, _p]
         L.ubt_tree_kl_loss.argtypes = [_p, _i32, _i32, _i32, _i64, _i64, _i64, _p, _p, _p, _i32, _p, _i64, _i64, _p,
                                        _p, _p, _p, _p, _i32, _i32, _p, _p, _f32, _f32, _p, _p, _p, _p, _p, _p]
-        for f in (L.ubt_topk, L.ubt_bigram_scores, L.ubt_build_tree, L.ubt_draft_tree, L.ubt_tree_mask,
+        for f in (L.ubt_topk, L.ubt_lm_head_topk, L.ubt_bigram_scores, L.ubt_build_tree, L.ubt_draft_tree, L.ubt_tree_mask,
                   L.ubt_draft_step, L.ubt_draft_step_noalloc, L.ubt_edge_scores, L.ubt_build_tree_best_first, L.ubt_tree_attention, L.ubt_verify_accept, L.ubt_commit_kv, L.ubt_tree_kl_loss):
             f.restype = _i32
         _lib = L
@@ -154,6 +157,50 @@ def topk(logits: torch.Tensor, K: int, out: dict | None = None, with_logprob: bo
                         _ptr(out["cand_ids"]), _ptr(out["cand_logit"]), _ptr(out.get("cand_logprob")),
                         _ptr(out.get("lse")), _stream(stream))
     _check("ubt_topk", st)
+    return out
+
+
+def lm_head_workspace(M: int, d: int, V: int, K: int, device="cuda") -> torch.Tensor:
+    """A workspace for :func:`lm_head_topk` (uint8, 256-byte aligned; its contents are
+    never read before they are written)."""
+    n = lib().ubt_lm_head_topk_workspace_bytes(M, d, V, K)
+    if n == 0:
+        raise ValueError("invalid shape for ubt_lm_head_topk")
+    ws = torch.empty(n, dtype=torch.uint8, device=device)
+    if ws.data_ptr() % 256:
+        raise RuntimeError("workspace is not 256-byte aligned")
+    return ws
+
+
+def lm_head_topk(h: torch.Tensor, w_lm: torch.Tensor, K: int, out: dict | None = None,
+                 workspace: torch.Tensor | None = None, with_logprob: bool = True, stream=None) -> dict:
+    """Candidates and softmax statistics of the logits ``h @ w_lm.T`` without forming them:
+    ``h [..., d]`` and ``w_lm [V, d]``, both contiguous bf16.  Outputs have h's leading
+    shape: ``cand_ids``/``cand_logit``/``cand_logprob`` [..., K] and ``lse`` [...]."""
+    _need_gpu(h, w_lm)
+    _contig(h, "h")
+    _contig(w_lm, "w_lm")
+    if h.dtype != torch.bfloat16 or w_lm.dtype != torch.bfloat16:
+        raise TypeError("h and w_lm must be bfloat16")
+    if w_lm.dim() != 2 or h.shape[-1] != w_lm.shape[1]:
+        raise ValueError("h must be [..., d] and w_lm [V, d]")
+    lead = tuple(h.shape[:-1])
+    M = 1
+    for n in lead:
+        M *= n
+    V, d = w_lm.shape
+    dev = h.device
+    if out is None:
+        out = dict(cand_ids=torch.empty(*lead, K, dtype=torch.int32, device=dev),
+                   cand_logit=torch.empty(*lead, K, dtype=torch.float32, device=dev),
+                   cand_logprob=torch.empty(*lead, K, dtype=torch.float32, device=dev) if with_logprob else None,
+                   lse=torch.empty(*lead, dtype=torch.float32, device=dev))
+    if workspace is None:
+        workspace = lm_head_workspace(M, d, V, K, dev)
+    st = lib().ubt_lm_head_topk(_ptr(h), _ptr(w_lm), M, d, V, K, _ptr(out["cand_ids"]), _ptr(out["cand_logit"]),
+                                _ptr(out.get("cand_logprob")), _ptr(out.get("lse")), _ptr(workspace),
+                                workspace.numel(), _stream(stream))
+    _check("ubt_lm_head_topk", st)
     return out
 
 

@@ -9,7 +9,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libubt.so")
-SOURCES = ["api.cpp", "topk.hip", "bigram.hip", "tree.hip", "step.hip", "bestfirst.hip", "verify.hip", "loss.hip"]
+SOURCES = ["api.cpp", "topk.hip", "bigram.hip", "tree.hip", "step.hip", "bestfirst.hip", "lmhead.hip", "verify.hip", "loss.hip"]
 ARCH = "gfx950"
 
 FLAGS_COMPILE = [

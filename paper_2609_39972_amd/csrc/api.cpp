@@ -108,6 +108,26 @@ ubt_status_t ubt_topk(const void* logits, ubt_dtype_t dt, int B, int gamma, int6
                                      cand_ids, cand_logit, cand_logprob, lse, stream));
 }
 
+size_t ubt_lm_head_topk_workspace_bytes(int M, int d, int64_t V, int K) {
+  if (M < 1 || d < 32 || d > 65536 || d % 32 != 0 || K < 1 || K > UBT_MAX_K || V < K || V >= (int64_t(1) << 31))
+    return 0;
+  return ubt::lm_head_workspace_bytes(M, d, V, K);
+}
+
+ubt_status_t ubt_lm_head_topk(const void* h, const void* w_lm, int M, int d, int64_t V, int K, int32_t* cand_ids,
+                              float* cand_logit, float* cand_logprob, float* lse, void* workspace, size_t ws_bytes,
+                              hipStream_t stream) {
+  if (!h || !w_lm || !cand_ids || !cand_logit) return UBT_ERR_NULL;
+  if (M < 1 || d < 32 || d > 65536 || d % 32 != 0 || K < 1 || K > UBT_MAX_K || V < K || V >= (int64_t(1) << 31))
+    return UBT_ERR_SHAPE;
+  if (!aligned16(h) || !aligned16(w_lm)) return UBT_ERR_UNSUPPORTED;
+  const size_t need = ubt::lm_head_workspace_bytes(M, d, V, K);
+  if (need == 0) return UBT_ERR_UNSUPPORTED;
+  if (!workspace || ws_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0) return UBT_ERR_WORKSPACE;
+  return hip_status(ubt::launch_lm_head_topk(h, w_lm, M, d, V, K, cand_ids, cand_logit, cand_logprob, lse, workspace,
+                                             stream));
+}
+
 ubt_status_t ubt_bigram_scores(const void* phi_tab, const void* psi_tab, const void* gate, ubt_dtype_t feat_dt,
                                int64_t V, int r, const int32_t* anchor, const int32_t* cand_ids,
                                const float* cand_logit, const float* alpha, const float* lambda, int B, int gamma,

@@ -18,6 +18,10 @@ struct Scales {
   float alpha[64];
   float lambda[64];
 };
+size_t lm_head_workspace_bytes(int M, int d, int64_t V, int K);
+hipError_t launch_lm_head_topk(const void* h, const void* w_lm, int M, int d, int64_t V, int K, int32_t* cand_ids,
+                               float* cand_logit, float* cand_logprob, float* lse, void* workspace,
+                               hipStream_t stream);
 hipError_t launch_bigram(const void* phi, const void* psi, const void* gate, int feat_dtype, int64_t V, int r,
                          const int32_t* anchor, const int32_t* cand_ids, const float* cand_logit,
                          const Scales& scales, int B, int gamma, int K, float* delta, float* logq,

@@ -291,3 +291,62 @@ def _guided_best_first(g: dict, b: int, paths: list, e: np.ndarray, zeta: float)
         gs = float(g["score"][b, t])
         assert abs(gs - sx) <= EPS * max(1.0, ax), f"seq {b} slot {t}: GPU score {gs} vs {sx}"
         taken.add(x)
+
+
+def lm_head_tol(abs_sum: np.ndarray, d: int) -> np.ndarray:
+    """Bound on the fp32 rounding of a logit formed from exact bf16 products: at most
+    d/32 accumulating matrix-core steps, each of which may round up to 32 times, so
+    (d/32 + 32) unit roundoffs (2^-24) of the sum of the terms' magnitudes."""
+    return (d / 32 + 32) * 2.0 ** -24 * abs_sum
+
+
+def check_lm_head(g: dict, h_bits: np.ndarray, w_bits: np.ndarray, K: int, exact: bool = False) -> dict:
+    """GPU candidates of the LM head (numpy outputs, rows flattened) against the fp64
+    oracle.  exact: logits exact in fp32 (integer-valued inputs), so ids and logits must
+    match bit for bit, ties included.  Otherwise every reported logit must be its id's
+    fp64 logit within lm_head_tol, the order (logit desc, id asc) must hold on the
+    reported values, and no excluded id may beat an included one by more than both
+    tolerances; rows whose ids differ from the oracle's only that way are 'excused'."""
+    from oracle import lm_head as LH
+
+    M, d = h_bits.shape
+    u = LH.logits(h_bits, w_bits)
+    ref = LH.topk_of_logits(u, K)
+    gid = np.asarray(g["cand_ids"]).reshape(M, K).astype(np.int64)
+    gval = np.asarray(g["cand_logit"]).reshape(M, K).astype(np.float64)
+    glse = np.asarray(g["lse"]).reshape(M).astype(np.float64)
+    glp = None if g.get("cand_logprob") is None else np.asarray(g["cand_logprob"]).reshape(M, K).astype(np.float64)
+    if exact:
+        if not np.array_equal(gid, ref["cand_ids"]):
+            r = int(np.argwhere((gid != ref["cand_ids"]).any(-1))[0][0])
+            raise AssertionError(f"ids differ in row {r}: gpu={gid[r].tolist()} ref={ref['cand_ids'][r].tolist()}")
+        np.testing.assert_array_equal(gval, ref["cand_logit"], "candidate logits")
+        close(glse, ref["lse"], "lse")
+        if glp is not None:
+            close(glp, ref["cand_logprob"], "cand_logprob")
+        return {"exact": M, "excused": 0}
+    # Sum of |h_k W_vk| for every (row, id): the oracle's logits of the magnitudes.
+    tolu = lm_head_tol(LH.logits(h_bits & np.uint16(0x7FFF), w_bits & np.uint16(0x7FFF)), d)
+    V = u.shape[1]
+    counts = {"exact": 0, "excused": 0}
+    for m in range(M):
+        ids = gid[m]
+        assert ((ids >= 0) & (ids < V)).all() and len(set(ids.tolist())) == K, f"row {m}: invalid ids {ids.tolist()}"
+        uv, tv = u[m, ids], tolu[m, ids]
+        err = np.abs(gval[m] - uv)
+        assert (err <= tv).all(), f"row {m}: logit of id {ids[np.argmax(err - tv)]} off by {err.max()} (tol {tv.max()})"
+        dv = np.diff(gval[m])
+        assert (dv <= 0).all(), f"row {m}: reported logits not descending"
+        assert ((dv < 0) | (np.diff(ids) > 0)).all(), f"row {m}: equal logits not in id order"
+        out = np.ones(V, bool)
+        out[ids] = False
+        if out.any():
+            worst_out = np.max(u[m, out] - tolu[m, out])
+            assert worst_out <= np.min(uv + tv), f"row {m}: an excluded id beats the selection beyond the tolerance"
+        lse_tol = tolu[m].max() + EPS * max(1.0, abs(ref["lse"][m]))
+        assert abs(glse[m] - ref["lse"][m]) <= lse_tol, f"row {m}: lse {glse[m]} vs {ref['lse'][m]}"
+        if glp is not None:
+            lp_err = np.abs(glp[m] - (uv - ref["lse"][m]))
+            assert (lp_err <= tv + lse_tol).all(), f"row {m}: cand_logprob off by {lp_err.max()}"
+        counts["exact" if np.array_equal(ids, ref["cand_ids"][m]) else "excused"] += 1
+    return counts

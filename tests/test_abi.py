@@ -242,3 +242,41 @@ def test_draft_step_workspace_bytes(B, gamma, V, K, dt):
     assert got >= 256 + 4 * B * gamma
     assert L.ubt_draft_step_workspace_bytes(0, gamma, V, K, dt) == 0
     assert L.ubt_draft_step_workspace_bytes(B, gamma, K - 1, K, dt) == 0
+
+
+def _lmh(**kw):
+    a = dict(h=FAKE, w=FAKE, M=15, d=2560, V=151936, K=64, ids=FAKE, val=FAKE, lp=None, lse=None, ws=FAKE,
+             wsb=1 << 30)
+    a.update(kw)
+    return ubt.lib().ubt_lm_head_topk(a["h"], a["w"], a["M"], a["d"], a["V"], a["K"], a["ids"], a["val"], a["lp"],
+                                      a["lse"], a["ws"], a["wsb"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(h=None), 1), (dict(w=None), 1), (dict(ids=None), 1), (dict(val=None), 1),
+    (dict(M=0), 2), (dict(d=48), 2), (dict(d=0), 2), (dict(d=65568), 2), (dict(K=0), 2), (dict(K=65), 2),
+    (dict(V=63), 2), (dict(V=2 ** 31), 2),
+    (dict(h=ctypes.c_void_p(0x10008)), 4), (dict(w=ctypes.c_void_p(0x10002)), 4),
+    (dict(ws=None), 5), (dict(wsb=1000), 5), (dict(ws=ctypes.c_void_p(0x10010)), 5),
+])
+def test_lm_head_validation(kw, code):
+    assert _lmh(**kw) == code
+
+
+def test_lm_head_workspace_bytes():
+    """One (max, sum) and K sorted (key, id) pairs per (row slot, workgroup),
+    for 16 row slots per group of rows.  Workgroups: one per compute unit (256 on this GPU
+    and when none is visible), at most one per 16-row tile when d is a multiple of 512
+    (the k-split kernel), else at most one per 8 tiles."""
+    L = ubt.lib()
+    al = lambda n: (n + 255) // 256 * 256
+    for M, d, V, K in ((15, 2560, 151936, 64), (17, 4096, 151936, 8), (1, 2560, 1000, 1), (3, 96, 1000, 4),
+                       (2, 2560, 600, 8)):
+        tiles = (V + 15) // 16
+        G = min(256, tiles) if d % 512 == 0 else min(256, (tiles + 7) // 8)
+        parts = (M + 15) // 16 * G * 16
+        assert L.ubt_lm_head_topk_workspace_bytes(M, d, V, K) == al(parts * 8) + al(parts * K * 8)
+    assert L.ubt_lm_head_topk_workspace_bytes(0, 2560, 1000, 8) == 0
+    assert L.ubt_lm_head_topk_workspace_bytes(4, 2560, 7, 8) == 0
+    assert L.ubt_lm_head_topk_workspace_bytes(4, 48, 1000, 8) == 0
+    assert L.ubt_lm_head_topk_workspace_bytes(4, 2560, 2 ** 31 - 1, 64) == 0  # the merge's candidates would not fit
