@@ -37,6 +37,7 @@ constexpr int kLmRows = 16;       // rows of h per group (one MFMA tile)
 constexpr int kLmMaxRounds = 16;  // tiles per wave: LDS holds 16 x (rounds * 128) logits
 constexpr int kLmRowPad = 4;      // LDS row padding (floats): spreads a tile's 4 row groups over the banks
 constexpr int kLmMergeThreads = 256;
+constexpr int kLmStageWords = 2 * (64 + 2);  // per-wave selection stage: two rows of K + 2 (K <= 64)
 
 struct LmArgs {
   const uint16_t* h;  // [M, d] bf16
@@ -58,71 +59,184 @@ __device__ __forceinline__ uint64_t lm_order(uint32_t key, uint32_t id) {
   return (static_cast<uint64_t>(key) << 32) | static_cast<uint32_t>(~id);
 }
 
-// Per row m < Mg of the group (waves take rows w, w + 8): the maximum and sum of
-// exp(u - max) of the workgroup's logits vals[m][0..nslot), and their exact top K under
-// (logit desc, id asc), written as (order key, id) pairs in that order.  slot_id(s) is
-// the vocabulary id of slot s and must increase with s, so the selection's (key desc,
-// index asc) order is (logit desc, id asc).  Empty slots hold -inf.  stage: this wave's
-// LDS scratch of K 64-bit words.
+// One row of a workgroup's logits during the per-row selection (registers of one wave).
+template <int NR>
+struct RowSel {
+  float x[NR];
+  uint32_t key[NR];  // order key, 0 for an empty slot
+  float mx, se;      // maximum and sum of exp(u - max)
+  int need;          // entries to take: min(K, live entries)
+  uint32_t thr;      // threshold key
+  bool exact;        // exactly `need` live keys are >= thr (else ties at thr by slot)
+};
+
+template <int NR>
+__device__ __forceinline__ void row_load(RowSel<NR>& R, const float* row, int nslot, int lane, bool live, int K) {
+#pragma unroll
+  for (int r = 0; r < NR; ++r) {
+    const int s = r * kWave + lane;
+    R.x[r] = live && s < nslot ? row[s] : neg_inf();
+    R.key[r] = R.x[r] == neg_inf() ? 0u : f32_key(R.x[r]);
+  }
+  float mx = neg_inf();
+#pragma unroll
+  for (int r = 0; r < NR; ++r) mx = fmaxf(mx, R.x[r]);
+  R.mx = wave_max(mx);
+  float se = 0.f;
+#pragma unroll
+  for (int r = 0; r < NR; ++r) se += R.key[r] != 0u ? __builtin_amdgcn_exp2f((R.x[r] - R.mx) * kLog2e) : 0.f;
+  R.se = wave_sum(se);
+  int n_live = 0;
+#pragma unroll
+  for (int r = 0; r < NR; ++r) n_live += popc(ballot(R.key[r] != 0u));
+  R.need = n_live < K ? n_live : K;
+  R.thr = 1u;  // every live key is >= 1
+  R.exact = true;
+}
+
+// Search state of the need-th largest key of a row: a ballot radix search over the bits
+// below the common prefix of the largest key and a lower bound of the answer, stopping at
+// the first exact split.  The lower bound is the smallest per-lane maximum when at least
+// `need` lanes hold a key (each of those lanes has a key at or above it), else the
+// smallest key.
+struct RadixState {
+  uint32_t m, t, cand;
+  int cnt;
+};
+
+template <int NR>
+__device__ __forceinline__ RadixState radix_begin(RowSel<NR>& R) {
+  RadixState S{0u, 0u, 0u, 0};
+  uint32_t hi = 0u, lo = ~0u;
+#pragma unroll
+  for (int r = 0; r < NR; ++r) {
+    hi = max(hi, R.key[r]);
+    lo = min(lo, R.key[r] != 0u ? R.key[r] : ~0u);
+  }
+  int n_live = 0;
+#pragma unroll
+  for (int r = 0; r < NR; ++r) n_live += popc(ballot(R.key[r] != 0u));
+  if (n_live <= R.need) return S;  // every live key is taken
+  const uint32_t kmax = wave_umax(hi);
+  uint32_t kmin = wave_umin(lo);
+  const int lanes = popc(ballot(hi != 0u));
+  if (lanes >= R.need) kmin = max(kmin, wave_umin(hi != 0u ? hi : ~0u));
+  R.exact = false;
+  if (kmax == kmin) {
+    R.thr = kmax;
+    return S;
+  }
+  S.m = 0x80000000u >> __clz(kmax ^ kmin);
+  S.t = kmax & ~(S.m | (S.m - 1u));
+  return S;
+}
+
+template <int NR>
+__device__ __forceinline__ void radix_step(const RowSel<NR>& R, RadixState& S) {
+  S.cand = S.t | S.m;
+  int cnt = 0;
+#pragma unroll
+  for (int r = 0; r < NR; ++r) cnt += popc(ballot(R.key[r] >= S.cand));  // empty slots (0) never count
+  S.cnt = cnt;
+  S.t = cnt > R.need ? S.cand : S.t;
+  S.m = radix_next(S.m, cnt, R.need, 0u);
+}
+
+template <int NR>
+__device__ __forceinline__ void radix_end(RowSel<NR>& R, const RadixState& S) {
+  if (R.exact || R.thr != 1u) return;  // no search ran (everything taken, or all keys equal)
+  if (S.cnt == R.need) {
+    R.thr = S.cand;
+    R.exact = true;
+  } else {
+    R.thr = S.t;
+  }
+}
+
+// The selected entries' order values to stage[0..need) in slot order, then stage[need] =
+// stage[need + 1] = 0 (below every entry).
+template <int NR, class SlotId>
+__device__ __forceinline__ void row_compact(const RowSel<NR>& R, uint64_t* stage, int lane, SlotId slot_id) {
+  int left = 0;
+  if (!R.exact) {
+    int above = 0;
+#pragma unroll
+    for (int r = 0; r < NR; ++r) above += popc(ballot(R.key[r] > R.thr));
+    left = R.need - above;
+  }
+  int pos = 0;
+#pragma unroll
+  for (int r = 0; r < NR; ++r) {
+    uint64_t msk = ballot(R.key[r] >= R.thr);
+    if (!R.exact) {
+      const uint64_t eq = ballot(R.key[r] == R.thr);
+      msk = ballot(R.key[r] > R.thr) | ballot(lane_in(eq) && static_cast<int>(lanes_below(eq)) < left);
+      const int te = popc(eq);
+      left -= te < left ? te : left;
+    }
+    if (lane_in(msk)) stage[pos + static_cast<int>(lanes_below(msk))] = lm_order(R.key[r], slot_id(r * kWave + lane));
+    pos += popc(msk);
+  }
+  if (lane < 2) stage[R.need + lane] = 0ull;
+}
+
+// Lane < need: its staged entry and its rank (entries above it), read two at a time.
+__device__ __forceinline__ int stage_rank(const uint64_t* stage, int need, uint64_t mine) {
+  const ulonglong2* p = reinterpret_cast<const ulonglong2*>(stage);
+  int rank = 0;
+  for (int j = 0; j < (need + 1) / 2; ++j) {
+    const ulonglong2 o = p[j];
+    rank += (o.x > mine ? 1 : 0) + (o.y > mine ? 1 : 0);
+  }
+  return rank;
+}
+
+// Per row m < Mg of the group (wave w takes rows w and w + 8, interleaved so that their
+// dependent steps overlap): the maximum and sum of exp(u - max) of the workgroup's logits
+// vals[m][0..nslot), and their exact top K under (logit desc, id asc), written as (order
+// key, id) pairs in that order.  slot_id(s) is the vocabulary id of slot s and must
+// increase with s, so (key desc, slot asc) is (logit desc, id asc).  Empty slots hold
+// -inf.  stage: this wave's LDS scratch of 2 (K + 2) 64-bit words, 16-byte aligned.  NR:
+// registers per lane for a row (nslot <= 64 NR).
 template <int NR, class SlotId>
 __device__ __forceinline__ void emit_rows(const LmArgs& a, const float* vals, int rstride, int nslot, int Mg, int w,
                                           int lane, int64_t pbase, uint64_t* stage, SlotId slot_id) {
+  static_assert(kLmRows <= 2 * kLmWaves, "two rows per wave");
   const int K = a.K;
-  for (int m = w; m < Mg; m += kLmWaves) {
-    const float* row = vals + m * rstride;
-    float x[NR];
-    uint32_t key[NR], ids[NR];
-#pragma unroll
-    for (int r = 0; r < NR; ++r) {
-      const int s = r * kWave + lane;
-      x[r] = s < nslot ? row[s] : neg_inf();
-      key[r] = x[r] == neg_inf() ? 0u : f32_key(x[r]);
-      ids[r] = slot_id(s);
-    }
-    float mx = neg_inf();
-#pragma unroll
-    for (int r = 0; r < NR; ++r) mx = fmaxf(mx, x[r]);
-    mx = wave_max(mx);
-    float se = 0.f;
-#pragma unroll
-    for (int r = 0; r < NR; ++r)
-      if (key[r] != 0u) se += __builtin_amdgcn_exp2f((x[r] - mx) * kLog2e);
-    se = wave_sum(se);
-    int n_live = 0;
-#pragma unroll
-    for (int r = 0; r < NR; ++r) n_live += popc(ballot(key[r] != 0u));
-    const int need = n_live < K ? n_live : K;
-    uint64_t sel[NR];
-    if (need > 0) {
-      select_best<NR>(key, n_live, need, sel);
-    } else {
-#pragma unroll
-      for (int r = 0; r < NR; ++r) sel[r] = 0ull;
-    }
-    // The selected entries' order values to the stage, then each ranked by counting.
-    int pos = 0;
-#pragma unroll
-    for (int r = 0; r < NR; ++r) {
-      if (lane_in(sel[r])) stage[pos + static_cast<int>(lanes_below(sel[r]))] = lm_order(key[r], ids[r]);
-      pos += popc(sel[r]);
-    }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
+  const int m0 = w, m1 = w + kLmWaves;
+  if (m0 >= Mg) return;
+  const bool has1 = m1 < Mg;
+  RowSel<NR> R0, R1;
+  row_load<NR>(R0, vals + m0 * rstride, nslot, lane, true, K);
+  row_load<NR>(R1, vals + (has1 ? m1 : m0) * rstride, nslot, lane, has1, K);
+  RadixState S0 = radix_begin<NR>(R0), S1 = radix_begin<NR>(R1);
+  while (S0.m != 0u || S1.m != 0u) {
+    if (S0.m != 0u) radix_step<NR>(R0, S0);
+    if (S1.m != 0u) radix_step<NR>(R1, S1);
+  }
+  radix_end<NR>(R0, S0);
+  radix_end<NR>(R1, S1);
+  const int st1 = (K + 3) & ~1;  // even, so the second stage stays 16-byte aligned
+  uint64_t* stage0 = stage;
+  uint64_t* stage1 = stage + st1;
+  row_compact<NR>(R0, stage0, lane, slot_id);
+  row_compact<NR>(R1, stage1, lane, slot_id);
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
+  const uint64_t mine0 = lane < R0.need ? stage0[lane] : 0ull;
+  const uint64_t mine1 = lane < R1.need ? stage1[lane] : 0ull;
+  const int rank0 = lane < R0.need ? stage_rank(stage0, R0.need, mine0) : 0;
+  const int rank1 = lane < R1.need ? stage_rank(stage1, R1.need, mine1) : 0;
+  auto store = [&](int m, const RowSel<NR>& R, uint64_t mine, int rank) {
     const int64_t pidx = pbase + m;
     uint2* out = a.part_cand + pidx * K;
-    if (lane < need) {
-      const uint64_t mine = stage[lane];
-      int rank = 0;
-      for (int j = 0; j < need; ++j) rank += stage[j] > mine ? 1 : 0;
-      out[rank] = make_uint2(static_cast<uint32_t>(mine >> 32), ~static_cast<uint32_t>(mine));
-    }
-    for (int e = need + lane; e < K; e += kWave) out[e] = make_uint2(0u, 0u);
-    if (lane == 0) a.part_ms[pidx] = make_float2(mx, se);
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
-    __builtin_amdgcn_wave_barrier();  // the stage is reused by the next row
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
-  }
+    if (lane < R.need) out[rank] = make_uint2(static_cast<uint32_t>(mine >> 32), ~static_cast<uint32_t>(mine));
+    for (int e = R.need + lane; e < K; e += kWave) out[e] = make_uint2(0u, 0u);
+    if (lane == 0) a.part_ms[pidx] = make_float2(R.mx, R.se);
+  };
+  store(m0, R0, mine0, rank0);
+  if (has1) store(m1, R1, mine1, rank1);
 }
 
 // P: k-steps per chunk of loads in flight (divides d / 32); NR: registers per lane holding
@@ -200,7 +314,7 @@ __global__ __launch_bounds__(kLmWaves* kWave) void lm_head_stream_kernel(LmArgs 
   __syncthreads();
   // Slot s = (round * 8 + wave) * 16 + column holds vocabulary id
   // ((g * 8 + wave) + round * T) * 16 + column.
-  uint64_t* stage = reinterpret_cast<uint64_t*>(smem_raw + kLmRows * rstride * sizeof(float)) + w * kWave;
+  uint64_t* stage = reinterpret_cast<uint64_t*>(smem_raw + kLmRows * rstride * sizeof(float)) + w * kLmStageWords;
   emit_rows<NR>(a, vals, rstride, nslot, Mg, w, lane, (static_cast<int64_t>(grp) * G + g) * kLmRows, stage, [&](int s) {
     const int col = s & 15, wv = (s >> 4) & (kLmWaves - 1), round = s >> 7;
     return static_cast<uint32_t>((static_cast<int64_t>(g) * kLmWaves + wv + static_cast<int64_t>(round) * stride) * 16 +
@@ -618,10 +732,12 @@ hipError_t launch_lm_head_topk(const void* h, const void* w_lm, int M, int d, in
   do {                            \
     if (nslot <= 4 * kWave)       \
       UBT_LM_SPLIT(SWV, 4);       \
+    else if (nslot <= 10 * kWave) \
+      UBT_LM_SPLIT(SWV, 10);      \
     else if (nslot <= 16 * kWave) \
       UBT_LM_SPLIT(SWV, 16);      \
     else                          \
-      UBT_LM_SPLIT(SWV, 32);      \
+      UBT_LM_SPLIT(SWV, 24);      \
   } while (0)
     switch (sw) {
       case 4: UBT_LM_SPLIT_NR(4); break;
@@ -637,7 +753,7 @@ hipError_t launch_lm_head_topk(const void* h, const void* w_lm, int M, int d, in
 #undef UBT_LM_SPLIT
   } else {
     const size_t smem = static_cast<size_t>(kLmRows) * (a.rounds * kLmWaves * 16 + kLmRowPad) * sizeof(float) +
-                        kLmWaves * kWave * sizeof(uint64_t);  // + the per-wave stages
+                        kLmWaves * kLmStageWords * sizeof(uint64_t);  // + the per-wave stages
     const int nr = 2 * a.rounds;  // slots per lane: rounds * 128 / 64
     const bool p8 = (d / 32) % 8 == 0;
 #define UBT_LM_LAUNCH(PP, NRV)                                                                     \
