@@ -162,7 +162,7 @@ def topk(logits: torch.Tensor, K: int, out: dict | None = None, with_logprob: bo
 
 def lm_head_workspace(M: int, d: int, V: int, K: int, device="cuda") -> torch.Tensor:
     """A workspace for :func:`lm_head_topk` (uint8, 256-byte aligned; its contents are
-    never read before they are written)."""
+    never read before they are written, so it serves calls of any shape in turn)."""
     n = lib().ubt_lm_head_topk_workspace_bytes(M, d, V, K)
     if n == 0:
         raise ValueError("invalid shape for ubt_lm_head_topk")

@@ -493,9 +493,11 @@ __global__ __launch_bounds__(kLmMergeThreads) void lm_head_merge_kernel(LmArgs a
   const int64_t base = static_cast<int64_t>(grp) * G * kLmRows + mr;  // workgroup g's partial: base + 16 g
   if (tid < kWave) {
     constexpr int R = 2 * GL;
+    constexpr int kHead = 4;  // entries of every list read with the first loads
     float pm[GL], ps[GL];
     uint32_t key[R];
     const uint2* lst[GL];
+    uint2 hd[GL][kHead];
 #pragma unroll
     for (int i = 0; i < GL; ++i) {
       const int g = lane + kWave * i;
@@ -504,8 +506,10 @@ __global__ __launch_bounds__(kLmMergeThreads) void lm_head_merge_kernel(LmArgs a
       const float2 p = live ? a.part_ms[base + static_cast<int64_t>(g) * kLmRows] : make_float2(neg_inf(), 0.f);
       pm[i] = p.x;
       ps[i] = p.y;
-      key[2 * i] = live ? lst[i][0].x : 0u;
-      key[2 * i + 1] = live && K > 1 ? lst[i][1].x : 0u;
+#pragma unroll
+      for (int e = 0; e < kHead; ++e) hd[i][e] = live && e < K ? lst[i][e] : make_uint2(0u, 0u);
+      key[2 * i] = hd[i][0].x;
+      key[2 * i + 1] = hd[i][1].x;
     }
     float mx = neg_inf();
 #pragma unroll
@@ -530,17 +534,14 @@ __global__ __launch_bounds__(kLmMergeThreads) void lm_head_merge_kernel(LmArgs a
       for (int r = 0; r < R; ++r) lo = min(lo, lane_in(sl[r]) ? key[r] : ~0u);
       kb = wave_umin(lo);
     }
-    // Survivors, one entry of every open list per round.
+    // Survivors: entry e of every list still above the bound, the first kHead entries
+    // from the registers, later ones (rare) one round of loads each.
     int ns = 0;
     uint32_t open = 0u;  // bit i: list i still above the bound
 #pragma unroll
     for (int i = 0; i < GL; ++i)
       if (lane + kWave * i < G) open |= 1u << i;
-    for (int e = 0; e < K; ++e) {
-      if (ballot(open != 0u) == 0ull) break;
-      uint2 c[GL];
-#pragma unroll
-      for (int i = 0; i < GL; ++i) c[i] = (open >> i) & 1u ? lst[i][e] : make_uint2(0u, 0u);
+    auto take = [&](const uint2 (&c)[GL]) {
 #pragma unroll
       for (int i = 0; i < GL; ++i) {
         const bool keep = ((open >> i) & 1u) && c[i].x != 0u && c[i].x >= kb;
@@ -549,6 +550,20 @@ __global__ __launch_bounds__(kLmMergeThreads) void lm_head_merge_kernel(LmArgs a
         if (keep) surv[ns + static_cast<int>(lanes_below(mk))] = lm_order(c[i].x, c[i].y);
         ns += popc(mk);
       }
+    };
+#pragma unroll
+    for (int e = 0; e < kHead; ++e) {
+      uint2 c[GL];
+#pragma unroll
+      for (int i = 0; i < GL; ++i) c[i] = hd[i][e];
+      take(c);
+    }
+    for (int e = kHead; e < K; ++e) {
+      if (ballot(open != 0u) == 0ull) break;
+      uint2 c[GL];
+#pragma unroll
+      for (int i = 0; i < GL; ++i) c[i] = (open >> i) & 1u ? lst[i][e] : make_uint2(0u, 0u);
+      take(c);
     }
     if (lane == 0) {
       misc[0] = static_cast<uint32_t>(ns);

@@ -11,7 +11,7 @@ against the fp64 oracle, through the C ABI.
   ragged shapes (M not a multiple of 16, V not a multiple of 16, d/32 odd): logits within
   the derived fp32 accumulation bound, the candidate order valid under it.
 * Degenerate cases: h = 0 (every logit 0), K = V, K = 1, one row; reuse of a workspace
-  across calls of different shapes."""
+  across calls of different shapes and kernels."""
 from __future__ import annotations
 
 import math
@@ -114,4 +114,19 @@ def test_lm_head_workspace_reuse():
     a = synth.lm_head_inputs(10, 40, 128, 50000)
     b = synth.lm_head_inputs(11, 7, 128, 3001)
     for x, K in ((a, 64), (b, 8), (a, 64)):
+        parity.check_lm_head(_run(x["h"], x["w"], K, workspace=ws), x["h"], x["w"], K)
+
+
+def test_lm_head_workspace_reuse_across_shapes():
+    """One workspace serves calls with different numbers of row groups, hidden sizes and
+    kernels in any order: nothing in it is read before the call writes it."""
+    import paper_2609_39972_amd as ubt
+
+    print("lm_head workspace reuse across shapes", flush=True)
+    cases = [(40, 2560, 30011, 64), (5, 2560, 9000, 8), (17, 1024, 20000, 16), (3, 96, 3000, 4), (40, 2560, 30011, 64)]
+    n = max(ubt.lib().ubt_lm_head_topk_workspace_bytes(M, d, V, K) for M, d, V, K in cases)
+    import torch
+    ws = torch.full((n,), 0xA5, dtype=torch.uint8, device="cuda")  # stale bytes must not matter
+    for i, (M, d, V, K) in enumerate(cases):
+        x = synth.lm_head_inputs(20 + i, M, d, V)
         parity.check_lm_head(_run(x["h"], x["w"], K, workspace=ws), x["h"], x["w"], K)
