@@ -36,7 +36,7 @@ TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "topk_sweep_zipf-v151936-b32_co
 SWEEP_SOURCES = ("topk.hip", "sweep.h", "ubt_device.h")
 STEP_KERNEL = "draft_pipe_kernel"
 STEP_PROFILE = os.path.join(ROOT, "profiles", "draft_step_pipe_zipf-v151936-b32_counters.md")
-STEP_SOURCES = ("step.hip", "sweep.h", "search.h", "bigram_tile.h", "ubt_device.h")
+STEP_SOURCES = ("step.hip", "sweep.h", "search.h", "pipe_search.h", "bigram_tile.h", "ubt_device.h")
 
 
 def log(msg: str) -> None:
@@ -419,7 +419,7 @@ def bench_lmhead(args, dev) -> int:
     out = ubt.lm_head_topk(h, wt, K, workspace=ws)
     torch.cuda.synchronize()
 
-    def timed(fn, n=50, replays=4):
+    def timed(fn, n=args.lm_calls, replays=4):
         with torch.cuda.stream(stream):
             fn()
         torch.cuda.synchronize()
@@ -495,7 +495,8 @@ def bench_lmhead(args, dev) -> int:
                          f"8192 head rows, then the candidate sets; {el:.1f} s"}
     res = {
         "metric": f"LM head + candidate sets us/call at M={M}, d={d}, V={V}, K={K} (bf16)",
-        "value": round(1e6 / fused_us, 1), "unit": "blocks/s", "n_gpus": 1, "steps": 200, "warmup": 50,
+        "value": round(1e6 / fused_us, 1), "unit": "blocks/s", "n_gpus": 1, "steps": 4 * args.lm_calls,
+        "warmup": args.lm_calls,
         "ms_per_step": round(fused_us / 1e3, 6), "us_per_step": round(fused_us, 3), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": f"lm-head-m{M}-d{d}-v{V}-k{K}", "M": M, "d": d, "V": V, "K": K},
@@ -531,6 +532,7 @@ def main() -> int:
                          "objective; lmhead: the LM head fused with the candidate sets (each its own JSON line)")
     ap.add_argument("--lm-rows", type=int, default=15, help="lmhead mode: rows of h (draft positions)")
     ap.add_argument("--lm-hidden", type=int, default=2560, help="lmhead mode: hidden size d")
+    ap.add_argument("--lm-calls", type=int, default=50, help="lmhead mode: calls per timing graph (4 replays)")
     ap.add_argument("--sweep-launches", type=int, default=200, help="launches per kernel in the per-kernel timing")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run a plain device copy of known size (counter calibration) and exit")

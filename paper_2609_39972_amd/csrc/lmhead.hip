@@ -26,6 +26,8 @@
 // row's top K is in its own workgroup's top K, so the entries at or above the largest of
 // these bounds hold the row's top K.  An 8-bit radix selection over their 64-bit order
 // values finds the K-th, and the K entries at or above it are ranked by counting.
+#include <type_traits>
+
 #include "bigram_tile.h"
 #include "search.h"
 
@@ -350,7 +352,8 @@ __host__ __device__ inline SplitLayout split_layout(int rstride) {
 // Each load instruction reads 128 contiguous bytes of 8 head rows (8 lanes per row, whole
 // cache lines); the wave's LDS buffer turns two such loads (16 rows x 64 k) into the B
 // operands of two MFMA steps.  The loads of the next tile are issued as the current one's
-// registers are freed, so a whole tile slice (SW loads) stays in flight per wave.  After
+// registers are freed, so a whole tile slice (SW loads) stays in flight per wave (the last tile
+// issues none).  After
 // each tile the 8 partial 16 x 16 products are summed in wave order through LDS.
 template <int SW, int NR>
 __global__ __launch_bounds__(kLmWaves* kWave) void lm_head_split_kernel(LmArgs a) {
@@ -410,23 +413,30 @@ __global__ __launch_bounds__(kLmWaves* kWave) void lm_head_split_kernel(LmArgs a
   unsigned char* tw1 = tw0 + 8 * kLmTRow;
   const unsigned char* trd = tb + lr * kLmTRow + 16 * kg;
   lds_barrier();  // vals initialised
-  for (int j = 0; j < ntw; ++j) {
-    const int jn = j + 1 < ntw ? j + 1 : j;  // the tile to prefetch (the last one again at the end)
-    const unsigned char* p0 = row_ptr(jn, 0);
-    const unsigned char* p1 = row_ptr(jn, 1);
+  // One tile through this wave's slice: R holds its loads; with kNext they are replaced by
+  // the next tile's (p0, p1) as they are consumed (the last tile loads nothing more).
+  auto pass = [&](auto next_tag, const unsigned char* p0, const unsigned char* p1) {
+    constexpr bool kNext = decltype(next_tag)::value;
     f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int c = 0; c < kSeg; ++c) {
       *reinterpret_cast<u32x4*>(tw0) = R[2 * c];
       *reinterpret_cast<u32x4*>(tw1) = R[2 * c + 1];
-      R[2 * c] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p0 + 128 * c));
-      R[2 * c + 1] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p1 + 128 * c));
+      if (kNext) {
+        R[2 * c] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p0 + 128 * c));
+        R[2 * c + 1] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p1 + 128 * c));
+      }
       const u32x4 b0 = *reinterpret_cast<const u32x4*>(trd);
       const u32x4 b1 = *reinterpret_cast<const u32x4*>(trd + 64);
       acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(A[2 * c]), as_bf16x8(b0), acc, 0, 0, 0);
       acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(A[2 * c + 1]), as_bf16x8(b1), acc, 0, 0, 0);
       __builtin_amdgcn_sched_barrier(0);
     }
+    return acc;
+  };
+  for (int j = 0; j < ntw; ++j) {
+    const f32x4 acc = j + 1 < ntw ? pass(std::true_type{}, row_ptr(j + 1, 0), row_ptr(j + 1, 1))
+                                  : pass(std::false_type{}, nullptr, nullptr);
     // This wave's partial: acc[jj] = sum over its slice for (row 4 kg + jj, column lr).
     float* rw = red + ((j & 1) * kLmWaves + w) * 256;
 #pragma unroll
