@@ -50,9 +50,9 @@ __host__ __device__ inline FastLayout fast_layout(int gamma, int K, int W) {
     p += static_cast<uint32_t>((bytes + 15) & ~static_cast<size_t>(15));
     return at;
   };
-  // K = 64: the slabs (gamma K^2 floats) do not fit; slab rows are read from memory.
+  // K = 64: the slabs (gamma K^2 floats) do not fit; one depth's slab at a time is staged.
   const bool in_lds = K <= 16;
-  L.slab = take(in_lds ? static_cast<size_t>(gamma) * K * K * sizeof(float) : 0);
+  L.slab = take((in_lds ? static_cast<size_t>(gamma) : 1) * K * K * sizeof(float));
   L.rmax = take(in_lds ? static_cast<size_t>(gamma) * K * sizeof(float) : 0);
   L.cids = take(static_cast<size_t>(gamma) * K * sizeof(int32_t));
   L.xpose = take(kFastMaxWK * sizeof(float));
@@ -188,28 +188,6 @@ __device__ __forceinline__ int rank_in_stage(const uint2* stage, int n, uint64_t
     for (int i = 0; i < 8; ++i) cur[i] = nxt[i];
   }
   return (acc[0] + acc[1]) + (acc[2] + acc[3]);
-}
-
-// A slab row from memory (K = 64: the slabs stay in memory), with its maximum.
-template <int KT>
-__device__ __forceinline__ float load_row_global(const float* row, bool vec, float (&v)[KT]) {
-  if (vec) {
-#pragma unroll
-    for (int i = 0; i < KT / 4; ++i) {
-      const float4 t = reinterpret_cast<const float4*>(row)[i];
-      v[4 * i] = t.x;
-      v[4 * i + 1] = t.y;
-      v[4 * i + 2] = t.z;
-      v[4 * i + 3] = t.w;
-    }
-  } else {
-#pragma unroll
-    for (int i = 0; i < KT; ++i) v[i] = row[i];
-  }
-  float m = v[0];
-#pragma unroll
-  for (int i = 1; i < KT; ++i) m = fmaxf(m, v[i]);
-  return m;
 }
 
 template <int KT>
@@ -380,32 +358,72 @@ __device__ __forceinline__ void ancestor_mask(int32_t* anc, uint32_t* mk, int n_
   }
 }
 
-// Depth-wise expansion (Eq. ubtree-frontier): F_d = Top_W(E_d) for d = 1..gamma.  F_d is
-// ranked (score desc, parent position, candidate rank) as it is formed and stored in that
-// order to s_key / s_info (parent = its position in F_{d-1}), with the supertree outputs
-// if asked.  total = the number of supertree nodes.
+// F_d, once selected: the w_d entries of `key` marked in `sel` (entry index e = parent
+// position in F_{d-1} * K + candidate rank), compacted to the stage in index order.
+// Returns this lane's entry (lane < w_d): its key, parent position p and candidate c.
+template <int R, int kLogK>
+__device__ __forceinline__ bool frontier_entry(const FastSmem& sm, const uint32_t (&key)[R], const uint64_t (&sel)[R],
+                                               int w_d, int lane, uint32_t& mx, uint32_t& my, int& p, int& c) {
+  compact_selected<R>(sm.stage, key, sel, w_d, lane);
+  const uint2 st = sm.stage[lane];
+  const bool have = lane < w_d;
+  mx = have ? st.x : 0u;
+  my = have ? st.y : 0u;
+  const int e = have ? static_cast<int>(~mx) : 0;
+  p = e >> kLogK;
+  c = e & ((1 << kLogK) - 1);
+  return have;
+}
+
+// Stores F_d in rank order (score desc, then index) to s_key / s_info (parent = its
+// position in F_{d-1}, candidate rank), with the supertree outputs if asked: the lanes
+// with `have` hold the w_d entries, each with its rank, and slots w_d..W-1 are cleared.
+__device__ __forceinline__ void frontier_store(const TreeArgs& a, const FastSmem& sm, int64_t b, int lane, int d,
+                                               int w_d, bool have, int rank, uint32_t my, int p, int c) {
+  const int gamma = a.gamma, W = a.W;
+  const int fb = (d - 1) * W;
+  const bool clear = lane >= w_d && lane < W;
+  if (have) {
+    sm.s_key[fb + rank] = my;
+    sm.s_info[fb + rank] = static_cast<uint32_t>(p) | (static_cast<uint32_t>(c) << 16);
+  } else if (clear) {
+    sm.s_key[fb + lane] = 0u;
+  }
+  if (a.f_count) {
+    if (lane == 0) a.f_count[b * gamma + d - 1] = w_d;
+    const int64_t o = (b * gamma + d - 1) * W;
+    if (have) {
+      a.f_parent[o + rank] = p;
+      a.f_cand[o + rank] = c;
+      a.f_score[o + rank] = f32_key_value(my);
+    } else if (clear) {
+      a.f_parent[o + lane] = -1;
+      a.f_cand[o + lane] = -1;
+      a.f_score[o + lane] = neg_inf();
+    }
+  }
+}
+
+// Depth-wise expansion (Eq. ubtree-frontier): F_d = Top_W(E_d) for d = 1..gamma, with the
+// slabs in LDS (K <= 16).  F_d is ranked (score desc, parent position, candidate rank) as
+// it is formed and stored in that order to s_key / s_info (parent = its position in
+// F_{d-1}), with the supertree outputs if asked.  total = the number of supertree nodes.
 template <int KT, int R, bool kWait>
 __device__ __forceinline__ void expand_depths(const TreeArgs& a, const FastSmem& sm, int64_t b, int lane,
                                               int& total) {
-  constexpr int kLogK = KT == 4 ? 2 : (KT == 8 ? 3 : (KT == 16 ? 4 : 6));
-  constexpr bool kMemSlab = KT > 16;  // slab rows come from logq in memory
+  static_assert(KT <= 16, "K = 64 stages its slabs (expand_depths64)");
+  constexpr int kLogK = KT == 4 ? 2 : (KT == 8 ? 3 : 4);
   const int gamma = a.gamma, W = a.W;
-  const float* gq = a.logq + b * gamma * KT * KT;
-  const bool vec = (reinterpret_cast<uintptr_t>(a.logq) & 15u) == 0;
   // Frontier entry on lane j < np: score key, position in F, and its slab row for the
-  // next depth (prefetched as soon as the entry's candidate rank is known).
+  // next depth (loaded as soon as the entry's candidate rank is known).
   uint32_t fkey = f32_key(0.f);
   int fpos = 0;
   float nq[KT];
   float rm;
   const uint64_t t0 = kWait ? __builtin_amdgcn_s_memrealtime() : 0ull;
-  if (kMemSlab) {
-    rm = load_row_global<KT>(gq, vec, nq);  // depth 1 extends the root through row 0
-  } else {
-    if (kWait) wait_slab(sm, 0, t0);
-    load_row<KT>(sm.slab, nq);  // depth 1 extends the root through row 0
-    rm = sm.rmax[0];
-  }
+  if (kWait) wait_slab(sm, 0, t0);
+  load_row<KT>(sm.slab, nq);  // depth 1 extends the root through row 0
+  rm = sm.rmax[0];
   int np = 1;
   total = 0;
   const float zeta = a.zeta;
@@ -449,48 +467,147 @@ __device__ __forceinline__ void expand_depths(const TreeArgs& a, const FastSmem&
     } else {
       select_best<R>(key, n, w_d, sel);
     }
-    compact_selected<R>(sm.stage, key, sel, w_d, lane);
-    const uint2 st = sm.stage[lane];
-    const bool have = lane < w_d;
-    const uint32_t mx = have ? st.x : 0u, my = have ? st.y : 0u;
-    const int e = have ? static_cast<int>(~mx) : 0;
-    const int p = e >> kLogK;
-    const int c = e & (KT - 1);
+    uint32_t mx, my;
+    int p, c;
+    const bool have = frontier_entry<R, kLogK>(sm, key, sel, w_d, lane, mx, my, p, c);
     if (d < gamma) {
-      if (kMemSlab) {
-        rm = load_row_global<KT>(gq + (d * KT + c) * KT, vec, nq);
-      } else {
-        if (kWait) wait_slab(sm, d, t0);
-        load_row<KT>(sm.slab + (d * KT + c) * KT, nq);
-        rm = sm.rmax[d * KT + c];
-      }
+      if (kWait) wait_slab(sm, d, t0);
+      load_row<KT>(sm.slab + (d * KT + c) * KT, nq);
+      rm = sm.rmax[d * KT + c];
     }
     const int rank = rank_in_stage(sm.stage, w_d, order_value(mx, my));
-    const int fb = (d - 1) * W;
-    if (have) {
-      sm.s_key[fb + rank] = my;
-      sm.s_info[fb + rank] = static_cast<uint32_t>(p) | (static_cast<uint32_t>(c) << 16);
-    } else if (lane < W) {
-      sm.s_key[fb + lane] = 0u;
-    }
-    if (a.f_count) {
-      if (lane == 0) a.f_count[b * gamma + d - 1] = w_d;
-      const int64_t o = (b * gamma + d - 1) * W;
-      if (have) {
-        a.f_parent[o + rank] = p;
-        a.f_cand[o + rank] = c;
-        a.f_score[o + rank] = f32_key_value(my);
-      } else if (lane < W) {
-        a.f_parent[o + lane] = -1;
-        a.f_cand[o + lane] = -1;
-        a.f_score[o + lane] = neg_inf();
-      }
-    }
+    frontier_store(a, sm, b, lane, d, w_d, have, rank, my, p, c);
     fkey = my;
     fpos = rank;
     np = w_d;
     total += w_d;
     __builtin_amdgcn_wave_barrier();
+  }
+}
+
+// The same expansion for K = 64, whose slabs (gamma K^2 floats) do not fit in LDS: the
+// slab of depth d is staged in LDS (16 KB) while the slab of depth d + 1 is already on its
+// way into registers, so every depth finds its slab in LDS without a memory round trip.
+// Entry (r, lane) of depth d is child `lane` of the frontier entry of rank r in F_{d-1}
+// (index r * 64 + lane: index order is (parent rank, candidate rank)); its score is the
+// parent's plus row c_r of the slab.
+//
+// Selection: each parent's best child is a wave maximum over its register, and the
+// smallest of these W maxima is a lower bound of the W-th best entry (they are W distinct
+// entries).  The entries at or above that bound (the survivors) hold F_d; when there are
+// at most 64 of them, each survivor's rank among them (score desc, then index) is counted
+// directly and the survivors of rank < W are F_d, already ranked.  Otherwise the radix
+// selection over all entries takes F_d, which is then ranked.
+template <int R, bool vec>
+__device__ __forceinline__ void expand_depths64(const TreeArgs& a, const FastSmem& sm, int64_t b, int lane,
+                                                int& total) {
+  constexpr int KT = 64;
+  const int gamma = a.gamma, W = a.W;
+  const float* gq = a.logq + b * gamma * KT * KT;
+  float* slab = sm.slab;  // [64][64], the slab of the current depth
+  float P[KT];            // this lane's share of the next slab, in flight
+  auto load_slab = [&](const float* src) {
+    if constexpr (vec) {
+#pragma unroll
+      for (int i = 0; i < KT / 4; ++i) {
+        const float4 t = reinterpret_cast<const float4*>(src)[i * kWave + lane];
+        P[4 * i] = t.x;
+        P[4 * i + 1] = t.y;
+        P[4 * i + 2] = t.z;
+        P[4 * i + 3] = t.w;
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < KT; ++i) P[i] = src[i * kWave + lane];
+    }
+  };
+  auto store_slab = [&]() {
+    if constexpr (vec) {
+#pragma unroll
+      for (int i = 0; i < KT / 4; ++i)
+        reinterpret_cast<float4*>(slab)[i * kWave + lane] = make_float4(P[4 * i], P[4 * i + 1], P[4 * i + 2], P[4 * i + 3]);
+    } else {
+#pragma unroll
+      for (int i = 0; i < KT; ++i) slab[i * kWave + lane] = P[i];
+    }
+  };
+  load_slab(gq);  // depth 1
+  int np = 1;
+  total = 0;
+  const float zeta = a.zeta;
+  const bool with_zeta = zeta != 0.f;
+  for (int d = 1; d <= gamma; ++d) {
+    // Slab d to LDS (the reads of slab d - 1 are done: a wave's LDS operations run in
+    // order), then slab d + 1 on its way.
+    store_slab();
+    if (d < gamma) load_slab(gq + static_cast<int64_t>(d) * KT * KT);
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
+    // F_{d-1}: entry r on lane r (depth 1: the root, score 0, extends through row 0).
+    uint32_t pkey = f32_key(0.f), pinfo = 0u;
+    if (d > 1 && lane < W) {
+      pkey = sm.s_key[(d - 2) * W + lane];
+      pinfo = sm.s_info[(d - 2) * W + lane];
+    }
+    uint32_t key[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const float base = f32_key_value(__builtin_amdgcn_readlane(pkey, r));
+      const int row = static_cast<int>(__builtin_amdgcn_readlane(pinfo, r) >> 16);
+      float v = base + slab[row * KT + lane];
+      if (with_zeta) v += zeta;
+      key[r] = r < np ? f32_key(v) : 0u;
+    }
+    const int n = np * KT;
+    const int w_d = n < W ? n : W;
+    uint32_t kmax = 0u, kbound = 1u;  // keys of live entries are nonzero
+    if (np >= W) {
+      kbound = ~0u;
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        if (r < np) {
+          const uint32_t m = wave_umax(key[r]);
+          kmax = max(kmax, m);
+          kbound = min(kbound, m);
+        }
+      }
+    }
+    uint64_t sel[R];
+    int ns = 0;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      sel[r] = ballot(key[r] >= kbound);
+      ns += popc(sel[r]);
+    }
+    uint32_t mx, my;
+    int p, c, rank;
+    bool have;
+    if (ns <= kWave) {
+      compact_selected<R>(sm.stage, key, sel, ns, lane);
+      const uint2 st = sm.stage[lane];
+      const bool live = lane < ns;
+      mx = live ? st.x : 0u;
+      my = live ? st.y : 0u;
+      rank = rank_in_stage(sm.stage, ns, order_value(mx, my));
+      have = live && rank < w_d;
+      const int e = have ? static_cast<int>(~mx) : 0;
+      p = e >> 6;
+      c = e & (KT - 1);
+    } else {
+      if (np >= W)
+        select_best<R>(key, n, w_d, sel, kmax, kbound);
+      else
+        select_best<R>(key, n, w_d, sel);
+      have = frontier_entry<R, 6>(sm, key, sel, w_d, lane, mx, my, p, c);
+      rank = rank_in_stage(sm.stage, w_d, order_value(mx, my));
+    }
+    frontier_store(a, sm, b, lane, d, w_d, have, rank, my, p, c);
+    np = w_d;
+    total += w_d;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
   }
 }
 
@@ -593,7 +710,14 @@ template <int KT, int R, bool kWait>
 __device__ __forceinline__ void fast_search(const TreeArgs& a, const FastSmem& sm, int64_t b, int lane,
                                             uint64_t magic_w) {
   int total = 0;
-  expand_depths<KT, R, kWait>(a, sm, b, lane, total);
+  if constexpr (KT == 64) {
+    // Two copies of the loop, so that neither merges the other's loads of the next slab.
+    if ((reinterpret_cast<uintptr_t>(a.logq) & 15u) == 0)
+      expand_depths64<R, true>(a, sm, b, lane, total);
+    else
+      expand_depths64<R, false>(a, sm, b, lane, total);
+  } else
+    expand_depths<KT, R, kWait>(a, sm, b, lane, total);
   finish_tree<KT, kWait>(a, sm, b, lane, magic_w, total);
 }
 
