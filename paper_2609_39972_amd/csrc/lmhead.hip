@@ -324,13 +324,6 @@ __global__ __launch_bounds__(kLmWaves* kWave) void lm_head_stream_kernel(LmArgs 
   });
 }
 
-// A workgroup barrier ordering LDS only: loads from global memory stay in flight.
-__device__ __forceinline__ void lds_barrier() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-  __builtin_amdgcn_s_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-}
-
 constexpr int kLmTRow = 144;  // bytes per row of a wave's transpose buffer: 128 + 16 (bank spread)
 
 struct SplitLayout {

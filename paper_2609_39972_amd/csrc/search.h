@@ -37,9 +37,10 @@ constexpr int kFastMaxW = 64;
 constexpr int kStageLive = 272;                // up to 255 selected entries + 16 zero entries
 constexpr int kStageCap = kStageLive + kWave;  // + one dummy slot per lane
 constexpr int kMaskWords = 8;                  // ceil(256 / 32)
+constexpr int kBoundWords = 32;                // K = 64: per-parent best keys (16), per-wave counts
 
 struct FastLayout {
-  uint32_t slab, rmax, cids, xpose, stage, s_key, s_info, f_slot, anc, mk, ready, fail, total;
+  uint32_t slab, rmax, cids, xpose, stage, s_key, s_info, f_slot, anc, mk, ready, fail, bound, total;
 };
 
 __host__ __device__ inline FastLayout fast_layout(int gamma, int K, int W) {
@@ -50,12 +51,13 @@ __host__ __device__ inline FastLayout fast_layout(int gamma, int K, int W) {
     p += static_cast<uint32_t>((bytes + 15) & ~static_cast<size_t>(15));
     return at;
   };
-  // K = 64: the slabs (gamma K^2 floats) do not fit; one depth's slab at a time is staged.
+  // K = 64: the slabs (gamma K^2 floats) do not fit; two depths' slabs at a time are staged.
   const bool in_lds = K <= 16;
-  L.slab = take((in_lds ? static_cast<size_t>(gamma) : 1) * K * K * sizeof(float));
+  L.slab = take((in_lds ? static_cast<size_t>(gamma) : 2) * K * K * sizeof(float));
   L.rmax = take(in_lds ? static_cast<size_t>(gamma) * K * sizeof(float) : 0);
   L.cids = take(static_cast<size_t>(gamma) * K * sizeof(int32_t));
-  L.xpose = take(kFastMaxWK * sizeof(float));
+  // K = 64: the survivors' stage (up to W K entries, 16 zero entries, a dummy per lane).
+  L.xpose = take(K <= 16 ? kFastMaxWK * sizeof(float) : (kFastMaxWK + 16 + kWave) * sizeof(uint2));
   L.stage = take(kStageCap * sizeof(uint2));
   L.s_key = take(static_cast<size_t>(gamma) * W * sizeof(uint32_t));
   L.s_info = take(static_cast<size_t>(gamma) * W * sizeof(uint32_t));
@@ -64,6 +66,7 @@ __host__ __device__ inline FastLayout fast_layout(int gamma, int K, int W) {
   L.mk = take(kMaxNodes * kMaskWords * sizeof(uint32_t));
   L.ready = take(static_cast<size_t>(gamma) * sizeof(uint32_t));
   L.fail = take(sizeof(uint32_t));
+  L.bound = take(kBoundWords * sizeof(uint32_t));
   L.total = p;
   return L;
 }
@@ -215,6 +218,7 @@ struct FastSmem {
   uint32_t* mk;
   uint32_t* ready;  // per position: its slab is in LDS (one-launch kernels only)
   uint32_t* fail;   // nonzero once a wait of this workgroup ran out of time (one-launch kernels only)
+  uint32_t* bound;  // K = 64: [0, 16) best child key per parent, [16, 20) survivors per wave
 };
 
 // Top_budget over the supertree: stages the selected entries (as compact_selected does).
@@ -246,6 +250,7 @@ __device__ __forceinline__ FastSmem fast_smem(unsigned char* raw, const FastLayo
   sm.mk = reinterpret_cast<uint32_t*>(raw + L.mk);
   sm.ready = reinterpret_cast<uint32_t*>(raw + L.ready);
   sm.fail = reinterpret_cast<uint32_t*>(raw + L.fail);
+  sm.bound = reinterpret_cast<uint32_t*>(raw + L.bound);
   return sm;
 }
 
@@ -485,31 +490,34 @@ __device__ __forceinline__ void expand_depths(const TreeArgs& a, const FastSmem&
   }
 }
 
-// The same expansion for K = 64, whose slabs (gamma K^2 floats) do not fit in LDS: the
-// slab of depth d is staged in LDS (16 KB) while the slab of depth d + 1 is already on its
-// way into registers, so every depth finds its slab in LDS without a memory round trip.
-// Entry (r, lane) of depth d is child `lane` of the frontier entry of rank r in F_{d-1}
-// (index r * 64 + lane: index order is (parent rank, candidate rank)); its score is the
-// parent's plus row c_r of the slab.
+// The same expansion for K = 64 on kK64Waves waves of one workgroup (a lone wave issues
+// too slowly for the 64 W entries of a depth).  The slabs (gamma K^2 floats) do not fit
+// in LDS: two are staged at a time, each wave loading a quarter of the slab two depths
+// ahead into registers while the current one is searched.  Entry (r, lane) of depth d is
+// child `lane` of the frontier entry of rank r in F_{d-1} (index r * 64 + lane: index
+// order is (parent rank, candidate rank)); wave w holds the parents r = w, w + 4, ...
 //
 // Selection: each parent's best child is a wave maximum over its register, and the
 // smallest of these W maxima is a lower bound of the W-th best entry (they are W distinct
-// entries).  The entries at or above that bound (the survivors) hold F_d; when there are
-// at most 64 of them, each survivor's rank among them (score desc, then index) is counted
-// directly and the survivors of rank < W are F_d, already ranked.  Otherwise the radix
-// selection over all entries takes F_d, which is then ranked.
-template <int R, bool vec>
-__device__ __forceinline__ void expand_depths64(const TreeArgs& a, const FastSmem& sm, int64_t b, int lane,
+// entries).  The entries at or above that bound (the survivors, typically a few dozen)
+// hold F_d; they are compacted to the survivors' stage and each survivor's rank among
+// them (score desc, then index) is counted, so the survivors of rank < W are F_d, already
+// ranked.  All waves return with the same `total`.
+constexpr int kK64Waves = 4;
+
+template <int RW, bool vec>
+__device__ __forceinline__ void expand_depths64(const TreeArgs& a, const FastSmem& sm, int64_t b, int w, int lane,
                                                 int& total) {
   constexpr int KT = 64;
+  constexpr int kQuarter = KT * KT / kK64Waves;  // floats of a slab staged by one wave
   const int gamma = a.gamma, W = a.W;
-  const float* gq = a.logq + b * gamma * KT * KT;
-  float* slab = sm.slab;  // [64][64], the slab of the current depth
-  float P[KT];            // this lane's share of the next slab, in flight
-  auto load_slab = [&](const float* src) {
+  const float* gq = a.logq + b * gamma * KT * KT + w * kQuarter;
+  float P[kQuarter / kWave];  // this wave's quarter of a slab, in flight
+  auto load_slab = [&](int d) {  // slab of depth d (1-based)
+    const float* src = gq + static_cast<int64_t>(d - 1) * KT * KT;
     if constexpr (vec) {
 #pragma unroll
-      for (int i = 0; i < KT / 4; ++i) {
+      for (int i = 0; i < kQuarter / (4 * kWave); ++i) {
         const float4 t = reinterpret_cast<const float4*>(src)[i * kWave + lane];
         P[4 * i] = t.x;
         P[4 * i + 1] = t.y;
@@ -518,96 +526,113 @@ __device__ __forceinline__ void expand_depths64(const TreeArgs& a, const FastSme
       }
     } else {
 #pragma unroll
-      for (int i = 0; i < KT; ++i) P[i] = src[i * kWave + lane];
+      for (int i = 0; i < kQuarter / kWave; ++i) P[i] = src[i * kWave + lane];
     }
   };
-  auto store_slab = [&]() {
+  auto store_slab = [&](int d) {
+    float* dst = sm.slab + ((d - 1) & 1) * KT * KT + w * kQuarter;
     if constexpr (vec) {
 #pragma unroll
-      for (int i = 0; i < KT / 4; ++i)
-        reinterpret_cast<float4*>(slab)[i * kWave + lane] = make_float4(P[4 * i], P[4 * i + 1], P[4 * i + 2], P[4 * i + 3]);
+      for (int i = 0; i < kQuarter / (4 * kWave); ++i)
+        reinterpret_cast<float4*>(dst)[i * kWave + lane] = make_float4(P[4 * i], P[4 * i + 1], P[4 * i + 2], P[4 * i + 3]);
     } else {
 #pragma unroll
-      for (int i = 0; i < KT; ++i) slab[i * kWave + lane] = P[i];
+      for (int i = 0; i < kQuarter / kWave; ++i) dst[i * kWave + lane] = P[i];
     }
   };
-  load_slab(gq);  // depth 1
+  uint32_t* s_best = sm.bound;
+  uint32_t* s_cnt = sm.bound + 16;
+  uint2* surv = reinterpret_cast<uint2*>(sm.xpose);  // [0, ns) survivors, then 16 zeros
+  const int dummy = kFastMaxWK + 16 + lane;
+  load_slab(1);
+  store_slab(1);
+  if (gamma > 1) load_slab(2);
+  lds_barrier();
   int np = 1;
   total = 0;
   const float zeta = a.zeta;
   const bool with_zeta = zeta != 0.f;
   for (int d = 1; d <= gamma; ++d) {
-    // Slab d to LDS (the reads of slab d - 1 are done: a wave's LDS operations run in
-    // order), then slab d + 1 on its way.
-    store_slab();
-    if (d < gamma) load_slab(gq + static_cast<int64_t>(d) * KT * KT);
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
+    // Slab d + 1 to LDS (its buffer held slab d - 1, whose reads ended before the last
+    // barrier of depth d - 1), then slab d + 2 on its way; the barriers of this depth
+    // publish slab d + 1 before depth d + 1 reads it.
+    if (d + 1 <= gamma) {
+      store_slab(d + 1);
+      if (d + 2 <= gamma) load_slab(d + 2);
+    }
+    const float* slab = sm.slab + ((d - 1) & 1) * KT * KT;
     // F_{d-1}: entry r on lane r (depth 1: the root, score 0, extends through row 0).
     uint32_t pkey = f32_key(0.f), pinfo = 0u;
     if (d > 1 && lane < W) {
       pkey = sm.s_key[(d - 2) * W + lane];
       pinfo = sm.s_info[(d - 2) * W + lane];
     }
-    uint32_t key[R];
+    uint32_t key[RW];
 #pragma unroll
-    for (int r = 0; r < R; ++r) {
+    for (int i = 0; i < RW; ++i) {
+      const int r = i * kK64Waves + w;
       const float base = f32_key_value(__builtin_amdgcn_readlane(pkey, r));
       const int row = static_cast<int>(__builtin_amdgcn_readlane(pinfo, r) >> 16);
       float v = base + slab[row * KT + lane];
       if (with_zeta) v += zeta;
-      key[r] = r < np ? f32_key(v) : 0u;
+      key[i] = r < np ? f32_key(v) : 0u;
     }
     const int n = np * KT;
     const int w_d = n < W ? n : W;
-    uint32_t kmax = 0u, kbound = 1u;  // keys of live entries are nonzero
+    // The bound: the smallest best child over the W parents (np = W from depth 2 on).
+    uint32_t kbound = 1u;  // keys of live entries are nonzero
     if (np >= W) {
-      kbound = ~0u;
 #pragma unroll
-      for (int r = 0; r < R; ++r) {
-        if (r < np) {
-          const uint32_t m = wave_umax(key[r]);
-          kmax = max(kmax, m);
-          kbound = min(kbound, m);
-        }
+      for (int i = 0; i < RW; ++i) {
+        const int r = i * kK64Waves + w;
+        const uint32_t m = wave_umax(key[i]);
+        if (r < np && lane == 0) s_best[r] = m;
       }
+      lds_barrier();
+      kbound = wave_umin(lane < W ? s_best[lane < W ? lane : 0] : ~0u);
     }
-    uint64_t sel[R];
-    int ns = 0;
+    uint64_t sel[RW];
+    int cnt = 0;
 #pragma unroll
-    for (int r = 0; r < R; ++r) {
-      sel[r] = ballot(key[r] >= kbound);
-      ns += popc(sel[r]);
+    for (int i = 0; i < RW; ++i) {
+      sel[i] = ballot(key[i] >= kbound);
+      cnt += popc(sel[i]);
     }
-    uint32_t mx, my;
-    int p, c, rank;
-    bool have;
-    if (ns <= kWave) {
-      compact_selected<R>(sm.stage, key, sel, ns, lane);
-      const uint2 st = sm.stage[lane];
-      const bool live = lane < ns;
-      mx = live ? st.x : 0u;
-      my = live ? st.y : 0u;
-      rank = rank_in_stage(sm.stage, ns, order_value(mx, my));
-      have = live && rank < w_d;
+    if (lane == 0) s_cnt[w] = static_cast<uint32_t>(cnt);
+    lds_barrier();
+    const uint32_t c4 = lane < kK64Waves ? s_cnt[lane < kK64Waves ? lane : 0] : 0u;
+    int ns = 0, off = 0;
+#pragma unroll
+    for (int v = 0; v < kK64Waves; ++v) {
+      const int cv = static_cast<int>(__builtin_amdgcn_readlane(c4, v));
+      off += v < w ? cv : 0;
+      ns += cv;
+    }
+    // Survivors to surv[0, ns) (each wave at its offset, in any order), then 16 zeros.
+    int pos = off;
+#pragma unroll
+    for (int i = 0; i < RW; ++i) {
+      const int r = i * kK64Waves + w;
+      const int at = lane_in(sel[i]) ? pos + static_cast<int>(lanes_below(sel[i])) : dummy;
+      surv[at] = make_uint2(~static_cast<uint32_t>(r * KT + lane), key[i]);
+      pos += popc(sel[i]);
+    }
+    if (w == 0) surv[lane < 16 ? ns + lane : dummy] = make_uint2(0u, 0u);
+    lds_barrier();
+    // Survivor j is ranked by lane j % 64 of wave (j / 64) % kK64Waves.
+    for (int j0 = w * kWave; j0 < ns; j0 += kK64Waves * kWave) {
+      const int j = j0 + lane;
+      const bool live = j < ns;
+      const uint2 st = surv[live ? j : 0];
+      const uint32_t mx = live ? st.x : 0u, my = live ? st.y : 0u;
+      const int rank = rank_in_stage(surv, ns, order_value(mx, my));
+      const bool have = live && rank < w_d;
       const int e = have ? static_cast<int>(~mx) : 0;
-      p = e >> 6;
-      c = e & (KT - 1);
-    } else {
-      if (np >= W)
-        select_best<R>(key, n, w_d, sel, kmax, kbound);
-      else
-        select_best<R>(key, n, w_d, sel);
-      have = frontier_entry<R, 6>(sm, key, sel, w_d, lane, mx, my, p, c);
-      rank = rank_in_stage(sm.stage, w_d, order_value(mx, my));
+      frontier_store(a, sm, b, w == 0 && j0 == 0 ? lane : kWave, d, w_d, have, rank, my, e >> 6, e & (KT - 1));
     }
-    frontier_store(a, sm, b, lane, d, w_d, have, rank, my, p, c);
     np = w_d;
     total += w_d;
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
+    lds_barrier();  // F_d and slab d + 1 published; the survivors and bound words free
   }
 }
 
@@ -710,14 +735,7 @@ template <int KT, int R, bool kWait>
 __device__ __forceinline__ void fast_search(const TreeArgs& a, const FastSmem& sm, int64_t b, int lane,
                                             uint64_t magic_w) {
   int total = 0;
-  if constexpr (KT == 64) {
-    // Two copies of the loop, so that neither merges the other's loads of the next slab.
-    if ((reinterpret_cast<uintptr_t>(a.logq) & 15u) == 0)
-      expand_depths64<R, true>(a, sm, b, lane, total);
-    else
-      expand_depths64<R, false>(a, sm, b, lane, total);
-  } else
-    expand_depths<KT, R, kWait>(a, sm, b, lane, total);
+  expand_depths<KT, R, kWait>(a, sm, b, lane, total);
   finish_tree<KT, kWait>(a, sm, b, lane, magic_w, total);
 }
 

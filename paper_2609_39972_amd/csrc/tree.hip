@@ -327,14 +327,14 @@ __global__ __launch_bounds__(kWave) void build_tree_kernel(TreeArgs a, int stage
 
 template <int KT, int R>
 __global__ __launch_bounds__(kWave) void build_tree_fast_kernel(TreeArgs a, uint64_t magic_w) {
+  static_assert(KT <= 16, "K = 64 runs build_tree_k64_kernel");
   extern __shared__ __align__(16) unsigned char smem_raw[];
   const int lane = threadIdx.x;
   const int64_t b = blockIdx.x;
   const int gamma = a.gamma;
   const FastSmem sm = fast_smem(smem_raw, fast_layout(gamma, KT, a.W));
-  // Stage this sequence's score slabs (K <= 16; at K = 64 the search reads the rows it
-  // needs from memory) and candidate ids.
-  if (KT <= 16) {
+  // Stage this sequence's score slabs and candidate ids.
+  {
     const int ns = gamma * KT * KT;
     const float* gslab = a.logq + b * ns;
     if ((reinterpret_cast<uintptr_t>(gslab) & 15u) == 0) {
@@ -350,9 +350,32 @@ __global__ __launch_bounds__(kWave) void build_tree_fast_kernel(TreeArgs a, uint
   const int32_t* gids = a.cand_ids + b * gamma * KT;
   for (int e = lane; e < gamma * KT; e += kWave) sm.cids[e] = gids[e];
   __syncthreads();
-  if (KT <= 16) slab_row_max<KT>(sm.slab, sm.rmax, lane, gamma * KT, kWave);
+  slab_row_max<KT>(sm.slab, sm.rmax, lane, gamma * KT, kWave);
   __syncthreads();
   fast_search<KT, R, false>(a, sm, b, lane, magic_w);
+}
+
+// K = 64: kK64Waves waves search one sequence together, staging its slabs two depths at a
+// time; wave 0 then prunes, emits the tree and builds the mask.  RW = registers of
+// 64 entries per wave (W <= 4 RW).
+template <int RW>
+__global__ __launch_bounds__(kK64Waves* kWave) void build_tree_k64_kernel(TreeArgs a, uint64_t magic_w) {
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  const int w = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) / kWave);
+  const int lane = static_cast<int>(threadIdx.x) % kWave;
+  const int64_t b = blockIdx.x;
+  const int gamma = a.gamma;
+  const FastSmem sm = fast_smem(smem_raw, fast_layout(gamma, 64, a.W));
+  const int32_t* gids = a.cand_ids + b * gamma * 64;
+  for (int e = static_cast<int>(threadIdx.x); e < gamma * 64; e += static_cast<int>(blockDim.x)) sm.cids[e] = gids[e];
+  // (the first barrier of the expansion publishes the ids)
+  int total = 0;
+  if ((reinterpret_cast<uintptr_t>(a.logq) & 15u) == 0)
+    expand_depths64<RW, true>(a, sm, b, w, lane, total);
+  else
+    expand_depths64<RW, false>(a, sm, b, w, lane, total);
+  if (w != 0) return;
+  finish_tree<64, false>(a, sm, b, lane, magic_w, total);
 }
 
 // Selector scores and tree search in one launch, one workgroup per sequence.  Wave 0
@@ -454,19 +477,28 @@ hipError_t launch_build_tree(const TreeArgs& a, hipStream_t stream) {
     else                        \
       UBT_FAST_LAUNCH(KK, 8);   \
   } while (0)
+#define UBT_K64_LAUNCH(RW)                                                                                   \
+  do {                                                                                                       \
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&build_tree_k64_kernel<RW>),                     \
+                              hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(smem));           \
+    hipLaunchKernelGGL((build_tree_k64_kernel<RW>), grid, dim3(kK64Waves * kWave), smem, stream, a, magic_w); \
+  } while (0)
     if (a.K == 4) {
       UBT_FAST_ROWS(4);
     } else if (a.K == 8) {
       UBT_FAST_ROWS(8);
     } else if (a.K == 16) {
       UBT_FAST_ROWS(16);
-    } else if (wk <= 512) {
-      UBT_FAST_ROWS(64);
-    } else if (wk <= 768) {
-      UBT_FAST_LAUNCH(64, 12);
+    } else if (a.W <= 4) {
+      UBT_K64_LAUNCH(1);
+    } else if (a.W <= 8) {
+      UBT_K64_LAUNCH(2);
+    } else if (a.W <= 12) {
+      UBT_K64_LAUNCH(3);
     } else {
-      UBT_FAST_LAUNCH(64, 16);
+      UBT_K64_LAUNCH(4);
     }
+#undef UBT_K64_LAUNCH
 #undef UBT_FAST_ROWS
 #undef UBT_FAST_LAUNCH
     return hipGetLastError();

@@ -52,6 +52,13 @@ __device__ __forceinline__ uint32_t lanes_below(uint64_t mask) {
 }
 
 __device__ __forceinline__ uint64_t ballot(bool p) { return __ballot(p); }
+
+// A workgroup barrier ordering LDS only: loads from global memory stay in flight.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
 __device__ __forceinline__ int popc(uint64_t m) { return __popcll(m); }
 
 // Float reductions.  DPP patterns inside a row of 16 lanes: xor 1 and xor 2 within a
