@@ -76,12 +76,15 @@ struct Traits<float> {
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
 
-struct WaveLds {
-  u32x4 data[kCapGroups];     // buffered candidate groups
-  uint32_t base[kCapGroups];  // row index of each group's first element
+template <int CAP>
+struct WaveLdsT {
+  static constexpr int kCap = CAP;
+  u32x4 data[CAP];     // buffered candidate groups
+  uint32_t base[CAP];  // row index of each group's first element
   uint2 stage[kWave];         // compaction staging (key, id)
   uint64_t cand[kWave];       // live candidates as 64-bit order values
 };
+using WaveLds = WaveLdsT<kCapGroups>;
 
 // Shared memory of one row's workgroup of up to MW waves.
 template <int MW>
@@ -151,9 +154,10 @@ __device__ __forceinline__ void load_checked(u32x4 (&buf)[kSubGroups], __amdgpu_
 template <typename T>
 __device__ __forceinline__ void mask_tail(u32x4 (&buf)[kSubGroups], int64_t c0, int64_t V, int lane) {
   constexpr int EPG = Traits<T>::kPer;
+  const int64_t lane_e = c0 + lane * EPG;
 #pragma unroll
   for (int g = 0; g < kSubGroups; ++g)
-    if (c0 + (g * kWave + lane) * EPG >= V) Traits<T>::set_neg_inf(buf[g]);
+    if (lane_e >= V - g * kWave * EPG) Traits<T>::set_neg_inf(buf[g]);
 }
 
 // Wave priority from the number of tiles this wave still has to stream: waves that are
@@ -166,8 +170,8 @@ __device__ __forceinline__ void set_prio(int rem) {
 }
 
 // Compacts the selected entries (at most 64) into lanes 0.. of (out_key, out_id).
-template <int R>
-__device__ __forceinline__ void compact(WaveLds& s, const uint32_t (&key)[R], const uint32_t (&sub)[R],
+template <int R, class WL>
+__device__ __forceinline__ void compact(WL& s, const uint32_t (&key)[R], const uint32_t (&sub)[R],
                                         const uint64_t (&sel)[R], int lane, uint32_t& out_key, uint32_t& out_id) {
   int n = 0;
 #pragma unroll
@@ -186,8 +190,8 @@ __device__ __forceinline__ void compact(WaveLds& s, const uint32_t (&key)[R], co
 // kCarry false, selects the top K of the groups alone (the running top-K is empty).
 // Elements whose key does not pass the threshold (key >= thr, or key > thr when strict)
 // are dropped: they cannot be in the top K.
-template <typename T, int RB, bool kCarry>
-__device__ __forceinline__ void flush_buffer(WaveLds& s, int g0, int nbuf, int64_t V, uint32_t thr, bool strict, int K,
+template <typename T, int RB, bool kCarry, class WL>
+__device__ __forceinline__ void flush_buffer(WL& s, int g0, int nbuf, int64_t V, uint32_t thr, bool strict, int K,
                                              int lane, uint32_t& cur_key, uint32_t& cur_id) {
   constexpr int EPG = Traits<T>::kPer;
   constexpr int C = kCarry ? 1 : 0;
@@ -223,8 +227,8 @@ __device__ __forceinline__ void flush_buffer(WaveLds& s, int g0, int nbuf, int64
 
 // Merges nbuf buffered groups into the running top-K; returns the new (key, id) pair of
 // this lane (lanes 0..K-1 hold the top K).  kFresh: the running top-K is empty.
-template <typename T, bool kFresh>
-__device__ __forceinline__ uint2 flush(WaveLds& s, int nbuf, int64_t V, uint32_t thr, bool strict, int K, int lane,
+template <typename T, bool kFresh, class WL>
+__device__ __forceinline__ uint2 flush(WL& s, int nbuf, int64_t V, uint32_t thr, bool strict, int K, int lane,
                                        uint32_t cur_key, uint32_t cur_id) {
   constexpr int EPG = Traits<T>::kPer;
   constexpr int kSlice = 4 * kWave / EPG;  // groups per selection pass (four register rows)
@@ -250,8 +254,8 @@ __device__ __forceinline__ uint2 flush(WaveLds& s, int nbuf, int64_t V, uint32_t
 }
 
 // The top K of the waves' candidates part[0..total), total <= 64 R, into lanes 0..K-1.
-template <typename T, int R>
-__device__ __forceinline__ void merge_parts(const uint2* part, int total, int K, int lane, WaveLds& s,
+template <typename T, int R, class WL>
+__device__ __forceinline__ void merge_parts(const uint2* part, int total, int K, int lane, WL& s,
                                             uint32_t& cur_key, uint32_t& cur_id) {
   uint32_t key[R], sub[R];
   uint64_t live[R], sel[R];
@@ -289,8 +293,8 @@ __device__ __forceinline__ int count_above(const uint64_t* v, int n, uint64_t mi
 }
 // Stages the buffered elements with key >= thr to s.cand (in buffer order); returns how
 // many there are (only the first 64 are staged).
-template <typename T>
-__device__ __forceinline__ int stage_live(WaveLds& s, int nbuf, int64_t V, uint32_t thr, int lane) {
+template <typename T, class WL>
+__device__ __forceinline__ int stage_live(WL& s, int nbuf, int64_t V, uint32_t thr, int lane) {
   constexpr int EPG = Traits<T>::kPer;
   const int total = nbuf * EPG;
   int n = 0;
@@ -341,9 +345,9 @@ struct WaveState {
 // the running top K, the threshold tightened, and the rest re-filtered, until every
 // passing group is held.  Otherwise a group that does not fit sets `overflow` (exact
 // re-scan at the end).
-template <typename T, bool kBig>
+template <typename T, bool kBig, class WL>
 __device__ __forceinline__ void push_groups(const u32x4 (&buf)[kSubGroups], const float (&gmax)[kSubGroups],
-                                            uint32_t pending, int64_t c0, int64_t V, int K, int lane, WaveLds& s,
+                                            uint32_t pending, int64_t c0, int64_t V, int K, int lane, WL& s,
                                             WaveState& st);
 
 // Max and exp-sum of one tile, folded into the lane's running (lm, ls): ls is the
@@ -423,10 +427,12 @@ __device__ __forceinline__ uint32_t passing_groups(const float (&gmax)[kSubGroup
   const float thr_v = Traits<T>::from_key(thr);
   const bool full = c0 + SUB <= V;
   const int lim = full ? static_cast<int>(SUB) : static_cast<int>(V - c0);
+  // One register for the lane's offset; the group's part of it is folded into the limit.
+  const int lane_e = lane * EPG;
   uint32_t pending = 0;
 #pragma unroll
   for (int g = 0; g < kSubGroups; ++g) {
-    const bool valid = full || (g * kWave + lane) * EPG < lim;
+    const bool valid = full || lane_e < lim - g * kWave * EPG;
     const bool pass = thr == 0 || (strict ? gmax[g] > thr_v : gmax[g] >= thr_v);
     if (valid && pass) pending |= 1u << g;
   }
@@ -435,9 +441,9 @@ __device__ __forceinline__ uint32_t passing_groups(const float (&gmax)[kSubGroup
 
 // Appends this lane's pending groups to the wave's LDS buffer; returns the groups that
 // did not fit.
-template <typename T>
+template <typename T, class WL>
 __device__ __forceinline__ uint32_t buffer_groups(const u32x4 (&buf)[kSubGroups], uint32_t pending, int64_t c0,
-                                                  int lane, WaveLds& s, int& nbuf) {
+                                                  int lane, WL& s, int& nbuf) {
   constexpr int EPG = Traits<T>::kPer;
 #pragma unroll
   for (int g = 0; g < kSubGroups; ++g) {
@@ -445,12 +451,12 @@ __device__ __forceinline__ uint32_t buffer_groups(const u32x4 (&buf)[kSubGroups]
     const uint64_t m = ballot(hit);
     if (m) {
       const int pos = nbuf + static_cast<int>(lanes_below(m));
-      if (hit && pos < kCapGroups) {
+      if (hit && pos < WL::kCap) {
         s.data[pos] = buf[g];
         s.base[pos] = static_cast<uint32_t>(c0) + static_cast<uint32_t>((g * kWave + lane) * EPG);
         pending &= ~(1u << g);
       }
-      nbuf = nbuf + popc(m) < kCapGroups ? nbuf + popc(m) : kCapGroups;
+      nbuf = nbuf + popc(m) < WL::kCap ? nbuf + popc(m) : WL::kCap;
     }
   }
   return pending;
@@ -460,9 +466,9 @@ __device__ __forceinline__ uint32_t buffer_groups(const u32x4 (&buf)[kSubGroups]
 // values): re-reads its tiles and keeps a running top-K, merging the buffer each
 // time it fills and tightening the threshold once K candidates are held (later groups
 // carry larger ids, so they must beat the K-th candidate strictly).
-template <typename T, bool kAligned>
+template <typename T, bool kAligned, class WL>
 __device__ uint2 rescan(__amdgpu_buffer_rsrc_t rsrc, const T* rp, int64_t first, int64_t nsub, int nw, int64_t V,
-                        uint32_t thr, int K, int lane, WaveLds& s) {
+                        uint32_t thr, int K, int lane, WL& s) {
   constexpr int64_t SUB = static_cast<int64_t>(kSubGroups) * kWave * Traits<T>::kPer;
   uint32_t cur_key = 0, cur_id = 0;
   bool strict = false;
@@ -501,9 +507,9 @@ __device__ uint2 rescan(__amdgpu_buffer_rsrc_t rsrc, const T* rp, int64_t first,
   return make_uint2(cur_key, cur_id);
 }
 
-template <typename T, bool kBig>
+template <typename T, bool kBig, class WL>
 __device__ __forceinline__ void push_groups(const u32x4 (&buf)[kSubGroups], const float (&gmax)[kSubGroups],
-                                            uint32_t pending, int64_t c0, int64_t V, int K, int lane, WaveLds& s,
+                                            uint32_t pending, int64_t c0, int64_t V, int K, int lane, WL& s,
                                             WaveState& st) {
   pending = buffer_groups<T>(buf, pending, c0, lane, s, st.nbuf);
   if (!ballot(pending != 0)) return;
@@ -550,24 +556,19 @@ struct RowOut {
   }
 };
 
-// The row at rp (V elements) of global row index `row`; the workgroup has up to MW waves
-// and `lds` is its shared memory.  Writes cand_*[row * K, row * K + K) and lse[row].
-template <typename T, bool kAligned, int MW = kWaves, bool kBig = false>
-__device__ __forceinline__ void sweep_row(RowLdsT<MW>& lds, const T* __restrict__ rp, int64_t V, int K, int64_t row,
-                                          const RowOut& out) {
+// The streaming pass over the row at rp (V elements) by wave w of nw: the running
+// (max, exp-sum) of each lane and the groups that reach the candidate threshold, in the
+// wave's buffer s (with kBig, also a running top K).  lane_max (nw * 64 words of LDS)
+// receives the lane maxima of the first tiles; the threshold is agreed on after one
+// __syncthreads of the workgroup.
+template <typename T, bool kAligned, int MW, bool kBig, class WL>
+__device__ __forceinline__ void stream_row(WL& s, uint32_t* lane_max, const T* __restrict__ rp, int64_t V, int K,
+                                           int nw, int w, int lane, __amdgpu_buffer_rsrc_t rsrc, WaveState& st) {
   constexpr int EPG = Traits<T>::kPer;
   constexpr int64_t SUB = static_cast<int64_t>(kSubGroups) * kWave * EPG;
-  const int nw = blockDim.x / kWave;
-  // Wave-uniform, and known to be: the tile indices and offsets derived from it
-  // then live in scalar registers.
-  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-  const int lane = threadIdx.x % kWave;
-  const __amdgpu_buffer_rsrc_t rsrc = row_resource(rp, static_cast<uint32_t>(V * static_cast<int64_t>(sizeof(T))));
   const int64_t nsub = (V + SUB - 1) / SUB;
   const uint32_t lane_off = static_cast<uint32_t>(lane * EPG * sizeof(T));
-  WaveLds& s = lds.wave[w];
-
-  WaveState st{neg_inf(), 0.f, 0u, 0, false, false, false, 0u, 0u};
+  st = WaveState{neg_inf(), 0.f, 0u, 0, false, false, false, 0u, 0u};
   u32x4 bufA[kSubGroups], bufB[kSubGroups];
   float gmax[kSubGroups];
   // Tiles [0, nfull) stream through the pipeline (aligned rows only, with the ragged last
@@ -592,8 +593,7 @@ __device__ __forceinline__ void sweep_row(RowLdsT<MW>& lds, const T* __restrict_
     uint32_t lkey = 0;
     if (sc * SUB == last_c0) mask_tail<T>(bufA, sc * SUB, V, lane);
     if (sc < nfull) lkey = Traits<T>::key_value(reduce_sub<T>(bufA, gmax, st.lm, st.ls));
-    lds.lane_max[w * kWave + lane] = lkey;
-    if (threadIdx.x == 0) lds.thr2 = 0;
+    lane_max[w * kWave + lane] = lkey;
   }
   __syncthreads();
   if (kBig) {
@@ -604,7 +604,7 @@ __device__ __forceinline__ void sweep_row(RowLdsT<MW>& lds, const T* __restrict_
     uint64_t lv[MW];
 #pragma unroll
     for (int j = 0; j < MW; ++j) {
-      lk[j] = j < nw ? lds.lane_max[j * kWave + lane] : 0u;
+      lk[j] = j < nw ? lane_max[j * kWave + lane] : 0u;
       lv[j] = ballot(lk[j] != 0u);
     }
     st.thr = wave_threshold<MW>(lk, lv, K, K + K / 4);
@@ -613,7 +613,7 @@ __device__ __forceinline__ void sweep_row(RowLdsT<MW>& lds, const T* __restrict_
     // waves): K distinct groups reach it, so it is a lower bound of the row's K-th largest
     // element.  Each lane counts the column maxima above its own.
     uint32_t cm = 0;
-    for (int j = 0; j < nw; ++j) cm = max(cm, lds.lane_max[j * kWave + lane]);
+    for (int j = 0; j < nw; ++j) cm = max(cm, lane_max[j * kWave + lane]);
     uint32_t* sv = reinterpret_cast<uint32_t*>(s.stage);
     sv[lane] = cm;
     __builtin_amdgcn_wave_barrier();
@@ -675,6 +675,27 @@ __device__ __forceinline__ void sweep_row(RowLdsT<MW>& lds, const T* __restrict_
       if (ballot(p != 0)) push_groups<T, kBig>(bufA, gmax, p, sr * SUB, V, K, lane, s, st);
     }
   }
+
+}
+
+// The row at rp (V elements) of global row index `row`; the workgroup has up to MW waves
+// and `lds` is its shared memory.  Writes cand_*[row * K, row * K + K) and lse[row].
+template <typename T, bool kAligned, int MW = kWaves, bool kBig = false>
+__device__ __forceinline__ void sweep_row(RowLdsT<MW>& lds, const T* __restrict__ rp, int64_t V, int K, int64_t row,
+                                          const RowOut& out) {
+  constexpr int EPG = Traits<T>::kPer;
+  constexpr int64_t SUB = static_cast<int64_t>(kSubGroups) * kWave * EPG;
+  const int nw = blockDim.x / kWave;
+  // Wave-uniform, and known to be: the tile indices and offsets derived from it
+  // then live in scalar registers.
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const int lane = threadIdx.x % kWave;
+  const __amdgpu_buffer_rsrc_t rsrc = row_resource(rp, static_cast<uint32_t>(V * static_cast<int64_t>(sizeof(T))));
+  const int64_t nsub = (V + SUB - 1) / SUB;
+  WaveLds& s = lds.wave[w];
+  if (threadIdx.x == 0) lds.thr2 = 0;  // published by the barrier inside the pass
+  WaveState st;
+  stream_row<T, kAligned, MW, kBig>(s, lds.lane_max, rp, V, K, nw, w, lane, rsrc, st);
 
   // This wave's live candidates (key >= the threshold) in s.cand: staged straight from
   // the buffer, or, when there are more than 64 of them or the buffer overflowed, the top

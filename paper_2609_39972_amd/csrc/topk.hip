@@ -5,12 +5,14 @@
 // Sets": C_i = the K tokens of largest q_i, ranked on the logits with ties to the lower
 // token id.
 #include "sweep.h"
+#include "sweep_big.h"
 #include "ubt_launch.h"
 
 namespace ubt {
 namespace {
 
-// kBig: K > 16 (a tighter first threshold and a running top K instead of the re-scan).
+// kBig: K > 16 (a tighter first threshold, a larger buffer with a running top K instead
+// of the re-scan, and the workgroup-wide selection of sweep_big.h).
 template <typename T, bool kAligned, bool kBig>
 __global__ __launch_bounds__(kWave* kWaves, 4) void topk_row_kernel(const T* __restrict__ logits, int gamma,
                                                                     int64_t V, int64_t stride_b, int64_t stride_i,
@@ -18,11 +20,16 @@ __global__ __launch_bounds__(kWave* kWaves, 4) void topk_row_kernel(const T* __r
                                                                     float* __restrict__ cand_logit,
                                                                     float* __restrict__ cand_logprob,
                                                                     float* __restrict__ lse) {
-  __shared__ RowLds lds;
   const int64_t row = blockIdx.x;
   const int64_t b = row / gamma, i = row - b * gamma;
-  sweep_row<T, kAligned, kWaves, kBig>(lds, logits + b * stride_b + i * stride_i, V, K, row,
-                         RowOut{cand_ids, cand_logit, cand_logprob, lse, false});
+  const RowOut out{cand_ids, cand_logit, cand_logprob, lse, false};
+  if constexpr (kBig) {
+    __shared__ BigRowLds lds;
+    sweep_row_big<T, kAligned>(lds, logits + b * stride_b + i * stride_i, V, K, row, out);
+  } else {
+    __shared__ RowLds lds;
+    sweep_row<T, kAligned, kWaves, false>(lds, logits + b * stride_b + i * stride_i, V, K, row, out);
+  }
 }
 
 template <typename T, bool kAligned>

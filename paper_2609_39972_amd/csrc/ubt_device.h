@@ -119,6 +119,27 @@ __device__ __forceinline__ uint32_t dpp_row_umin(uint32_t v) {
   v = min(v, static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x140, 0xF, 0xF, false)));
   return v;
 }
+// Inclusive prefix sum over the lanes of the wave (lanes 0..l for lane l), by DPP: sums of
+// 4, 8 and 16 lanes inside each row of 16, then the rows' totals broadcast into the rows
+// after them.  Every lane must be active.
+__device__ __forceinline__ uint32_t wave_prefix_sum(uint32_t v) {
+  const int x = static_cast<int>(v);
+  int s = x + __builtin_amdgcn_update_dpp(0, x, 0x111, 0xF, 0xF, true);  // row_shr:1
+  s += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xF, 0xF, true);         // row_shr:2
+  s += __builtin_amdgcn_update_dpp(0, x, 0x113, 0xF, 0xF, true);         // row_shr:3
+  s += __builtin_amdgcn_update_dpp(0, s, 0x114, 0xF, 0xE, false);        // row_shr:4, lanes 4..15
+  s += __builtin_amdgcn_update_dpp(0, s, 0x118, 0xF, 0xC, false);        // row_shr:8, lanes 8..15
+  s += __builtin_amdgcn_update_dpp(0, s, 0x142, 0xA, 0xF, false);        // row_bcast:15, rows 1, 3
+  s += __builtin_amdgcn_update_dpp(0, s, 0x143, 0xC, 0xF, false);        // row_bcast:31, rows 2, 3
+  return static_cast<uint32_t>(s);
+}
+
+// Sum over each quad of lanes (every lane of the quad gets it).
+__device__ __forceinline__ int quad_sum(int v) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false);
+  return v;
+}
 __device__ __forceinline__ uint32_t wave_umax(uint32_t v) {
   v = dpp_row_umax(v);
   const uint32_t a = __builtin_amdgcn_readlane(v, 0), b = __builtin_amdgcn_readlane(v, 16);

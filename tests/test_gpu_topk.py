@@ -89,6 +89,34 @@ def test_zipf_rows_full_vocab():
     _check(x, 16)
 
 
+@pytest.mark.parametrize("K", [64, 48, 17])
+def test_zipf_rows_large_k(K):
+    """The paper's configuration (K = 64) and other large K on permuted-zipf rows."""
+    w = synth.WORKLOADS[6]
+    x = synth.logits(w, 0, rows=np.arange(24)).reshape(2, 12, w.V)
+    _check(x, K)
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_rising_rows_fill_every_buffer(dt):
+    """Values that rise along the row: the first tiles hold the smallest values, so every
+    later group passes the first threshold and each wave's buffer fills and merges again
+    and again; with descending rows nothing after the first tiles passes."""
+    V = 151936
+    up = np.linspace(-4.0, 4.0, V)
+    x = synth.store(np.stack([up, up[::-1], np.round(up * 8) / 8]).reshape(1, 3, V), dt)
+    _check(x, 64)
+    _check(x, 33)
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_heavy_duplicates_k64(dt):
+    """Long runs of equal values around the K-th: the selection descends into the ids."""
+    rng = np.random.default_rng(8)
+    x = synth.store(np.round(rng.normal(0, 1, (2, 4, 50000)) * 2) / 2, dt)
+    _check(x, 64)
+
+
 def test_high_entropy_rows():
     w = synth.WORKLOADS[4]
     x = synth.logits(w, 0, rows=np.arange(30)).reshape(2, 15, w.V)
@@ -129,7 +157,7 @@ def test_repeat_is_bitwise_identical():
             assert np.array_equal(o[k], outs[0][k]), f"{k} not bitwise reproducible"
 
 
-@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5, 6])
 def test_workload_full_size(cfg):
     """Every row of the workload at its full size (all buffers of one pool entry)."""
     from gpu_util import say
