@@ -388,12 +388,13 @@ __device__ __forceinline__ void frontier_store(const TreeArgs& a, const FastSmem
   const int gamma = a.gamma, W = a.W;
   const int fb = (d - 1) * W;
   const bool clear = lane >= w_d && lane < W;
+  // A lane may both hold an entry and clear a slot (each lane's slot differs from every
+  // rank < w_d it may store to).
   if (have) {
     sm.s_key[fb + rank] = my;
     sm.s_info[fb + rank] = static_cast<uint32_t>(p) | (static_cast<uint32_t>(c) << 16);
-  } else if (clear) {
-    sm.s_key[fb + lane] = 0u;
   }
+  if (clear) sm.s_key[fb + lane] = 0u;
   if (a.f_count) {
     if (lane == 0) a.f_count[b * gamma + d - 1] = w_d;
     const int64_t o = (b * gamma + d - 1) * W;
@@ -401,7 +402,8 @@ __device__ __forceinline__ void frontier_store(const TreeArgs& a, const FastSmem
       a.f_parent[o + rank] = p;
       a.f_cand[o + rank] = c;
       a.f_score[o + rank] = f32_key_value(my);
-    } else if (clear) {
+    }
+    if (clear) {
       a.f_parent[o + lane] = -1;
       a.f_cand[o + lane] = -1;
       a.f_score[o + lane] = neg_inf();
