@@ -33,7 +33,7 @@ HBM_PEAK_GBPS = 8000.0
 POOL_BYTES = 512 << 20  # pool size that defeats the 256 MB Infinity Cache
 SWEEP_KERNEL = "topk_row_kernel"
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "topk_sweep_zipf-v151936-b32_counters.md")
-SWEEP_SOURCES = ("topk.hip", "sweep.h", "ubt_device.h")
+SWEEP_SOURCES = ("topk.hip", "sweep.h", "sweep_big.h", "ubt_device.h")
 STEP_KERNEL = "draft_pipe_kernel"
 STEP_PROFILE = os.path.join(ROOT, "profiles", "draft_step_pipe_zipf-v151936-b32_counters.md")
 STEP_SOURCES = ("step.hip", "sweep.h", "search.h", "pipe_search.h", "bigram_tile.h", "ubt_device.h")
