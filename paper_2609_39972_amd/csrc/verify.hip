@@ -8,22 +8,31 @@
 // into the cache and the other branches are dropped.  Background, "Tree Drafting".
 //
 // Tree attention: one workgroup of 8 waves per (sequence, key/value head, group of up to
-// 384 query rows).  The query rows of a key/value head are (node, head-in-group) pairs,
+// 320 query rows).  The query rows of a key/value head are (node, head-in-group) pairs,
 // node-major, so grouped heads share every key/value block, and the whole tree of a head
-// fits one group at the usual shapes (65 nodes x 4 heads = 260 rows): keys and values
-// are then read from HBM once.  Each wave holds up to 3 tiles of 16 query rows, so every
-// operand fragment read from LDS feeds up to 3 MFMAs.  Keys stream in blocks of 32
-// through LDS, double-buffered, the next block's global loads in flight while the
-// current one is used.  K is stored as it is; V is stored transposed (d-major), so both
-// products read MFMA operands with plain LDS loads:
+// fits one group at the usual shapes (65 nodes x 4 heads = 260 rows): keys and values are
+// then read from HBM once.  Keys stream in blocks of 32 through LDS.  K is stored as it
+// is; V is stored transposed (d-major), so both products read MFMA operands with plain
+// LDS loads:
 //   S^T = K Q^T     (v_mfma_f32_16x16x32_bf16, A = a K tile, B = 16 queries)
-//   O^T += V^T P^T  (A = a V^T tile, B = P^T straight from the S^T accumulators)
+//   O^T += V^T P^T  (A = a V^T tile, B = P^T in the layout of the S^T accumulators)
 // S^T puts the scores of one query in one lane column, 8 keys per lane, so P^T needs no
 // shuffle: the k order of the second product is permuted to match (slot t of lane group
 // g is key 4g + t for t < 4 and 16 + 4g + t - 4 after), and V^T is read in that order.
-// The running maximum is raised only when a score exceeds it by more than 2^8 (weights
-// then stay below 256, exact enough in fp32 and bf16), so the rescaling of the output
-// accumulators is off the steady-state path.
+//
+// The two products go to different waves.  Each SIMD holds a score wave (waves 0-3: the
+// query fragments, S^T and the softmax) and an output wave (waves 4-7: the output
+// accumulators and O^T), which share up to 5 query tiles of 16 rows.  The score wave
+// hands the weights P^T of a block to its output wave through LDS, so while one wave runs
+// the softmax on the vector ALU the other keeps the matrix core busy; each needs at most
+// 256 registers.  The output wave runs one block behind.  A score wave computes the next
+// block's scores tile by tile right after the tile's weights, so its own MFMAs overlap its
+// vector work too.  K and V are staged through registers two steps ahead of their LDS
+// stores, the output waves on even steps and the score waves on odd ones.  The running
+// maximum is raised only when a score exceeds it by more than 2^8 (weights then stay
+// below 256, exact enough in fp32 and bf16); it is checked on each block's scores as soon
+// as they exist, and the factor by which the output must be rescaled goes to the output
+// wave through LDS before that block's weights are used.
 #include "ubt_device.h"
 #include "ubt_launch.h"
 
@@ -35,25 +44,38 @@ typedef uint32_t v2u __attribute__((ext_vector_type(2)));
 typedef float v4f __attribute__((ext_vector_type(4)));
 typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
 
-constexpr int kAttnWaves = 8;
+constexpr int kPairs = 4;                        // (score wave, output wave) pairs, one per SIMD
+constexpr int kAttnWaves = 2 * kPairs;
 constexpr int kAttnThreads = kAttnWaves * kWave;
-constexpr int kTilesPerWave = 3;
-constexpr int kAttnRows = 16 * kAttnWaves * kTilesPerWave;  // query rows per workgroup (384)
-constexpr int kKB = 32;                                      // keys per block
+constexpr int kStageThreads = kPairs * kWave;    // threads of one role, which stage K and V
+constexpr int kMaxTiles = 5;                     // query tiles per pair
+constexpr int kSlots = kPairs * kMaxTiles;       // query tiles per workgroup
+constexpr int kAttnRows = 16 * kSlots;           // query rows per workgroup (320)
+constexpr int kKB = 32;                          // keys per block
 constexpr int kVtStride = 36;  // bf16 per V^T row: 32 keys + 4, so the transposing writes
                                // of one wave hit each bank at most twice
+constexpr int kMaskWords = 8;  // mask words per node (N <= 256)
 constexpr float kRescaleGap = 8.f;  // log2 units a score may exceed the running maximum
 
 template <int D>
 struct AttnLds {
-  uint16_t k[2][kKB][D + 8];
-  uint16_t vt[2][D][kVtStride];
+  uint16_t k[2][kKB][D + 8];          // K blocks i + 1 (read) and i + 2 (staged)
+  uint16_t vt[3][D][kVtStride];       // V^T blocks i - 1 (read), i, i + 1 (staged)
+  v4u p[2][kSlots][kWave];            // P^T of blocks i (written) and i - 1 (read), per lane
+  float alpha[3][kSlots][16];         // output rescale factor per query, blocks i - 1 .. i + 1
+  uint32_t rescale[3][kPairs];        // nonzero: the pair's output must be rescaled first
+  float fin_m[kSlots][16], fin_l[kSlots][16];  // final running maximum and sum per query
+  uint32_t mask[kAttnRows][kMaskWords];         // the ancestor-mask rows of the group's nodes
 };
 
 typedef __bf16 v2bf __attribute__((ext_vector_type(2)));
 typedef float v2f __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ v8bf as_v8bf(v4u v) { return __builtin_bit_cast(v8bf, v); }
+
+__device__ __forceinline__ v4f mfma_bf16(v4u a, v4u b, v4f c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_v8bf(a), as_v8bf(b), c, 0, 0, 0);
+}
 
 // Two floats to bf16, round to nearest even (one v_cvt_pk_bf16_f32).
 __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
@@ -69,7 +91,7 @@ struct AttnArgs {
   const uint16_t* vt;
   const uint32_t* mask;
   const int32_t* n_nodes;
-  int B, N, H, Hkv, g, R, groups;  // R = N * g query rows per key/value head, in groups of 384
+  int B, N, H, Hkv, g, R, groups;  // R = N * g query rows per key/value head, in groups of 320
   int64_t Pmax;
   float scale_log2;  // scale * log2(e)
   void* out;
@@ -77,75 +99,256 @@ struct AttnArgs {
   float* lse;
 };
 
-// The 16-byte chunks of one key/value block that thread t stages: K rows as they are
-// (chunk = 8 consecutive d of one key) and V as pairs of keys at the same 8 d, so that
-// the transposed write packs two keys per 32-bit LDS word.
-template <int D>
-struct Stage {
-  static constexpr int kChunks = D / 8;                                  // chunks per key row
-  static constexpr int kKPerThread = (kKB * kChunks + kAttnThreads - 1) / kAttnThreads;  // 1
-  v4u k[kKPerThread];
-  v4u v0, v1;
+// Where the keys and values of block `blk` of sequence b, head h live: the context for
+// blk < npb, else the tree.  Rows at or past `lim` do not exist; reads are clamped to row
+// lim - 1 and the value dropped, so every load is issued on every path.
+struct BlockSrc {
+  const uint16_t* k;
+  const uint16_t* v;
+  int64_t stride;  // rows of the source per sequence
+  int base, lim;
 };
 
-// Every load is issued unconditionally (clamped to a valid row, the value then dropped),
-// so the number of loads in flight is the same on every path and the compiler waits for
-// exactly the ones a value needs.
-template <int D>
-__device__ __forceinline__ void stage_load(const AttnArgs& p, Stage<D>& s, int b, int h, int blk, int npb, int P,
-                                           int nn, int t) {
-  constexpr int C = Stage<D>::kChunks;
+__device__ __forceinline__ BlockSrc block_src(const AttnArgs& p, int blk, int npb, int P, int nn) {
   const bool tree = blk >= npb;
-  const int base = tree ? (blk - npb) * kKB : blk * kKB;
-  const int lim = tree ? nn : P;  // >= base + 1 for every block that exists
-  const int64_t S = tree ? p.N : p.Pmax;
-  const uint16_t* ks = tree ? p.kt : p.kc;
-  const uint16_t* vs = tree ? p.vt : p.vc;
-  const v4u zero = v4u{0u, 0u, 0u, 0u};
-  auto row_ptr = [&](const uint16_t* src, int key, int c) {
-    const int kk = min(key, lim - 1);
-    return reinterpret_cast<const v4u*>(src + ((static_cast<int64_t>(b) * S + kk) * p.Hkv + h) * D + 8 * c);
-  };
-#pragma unroll
-  for (int i = 0; i < Stage<D>::kKPerThread; ++i) {
-    const int id = t + kAttnThreads * i;
-    const int row = min(id / C, kKB - 1), c = id % C;
-    const v4u v = *row_ptr(ks, base + row, c);
-    s.k[i] = (id / C < kKB && base + row < lim) ? v : zero;
-  }
-  const int kp = t % 16, c = min(t / 16, C - 1);
-  const int k0 = base + 2 * kp;
-  const bool in = t / 16 < C;  // 16 key pairs x C chunks: the first 16 C threads
-  const v4u a = *row_ptr(vs, k0, c), bb = *row_ptr(vs, k0 + 1, c);
-  s.v0 = (in && k0 < lim) ? a : zero;
-  s.v1 = (in && k0 + 1 < lim) ? bb : zero;
+  return BlockSrc{tree ? p.kt : p.kc, tree ? p.vt : p.vc, tree ? static_cast<int64_t>(p.N) : p.Pmax,
+                  tree ? (blk - npb) * kKB : blk * kKB, tree ? nn : P};
 }
 
 template <int D>
-__device__ __forceinline__ void stage_store(AttnLds<D>& lds, int st, const Stage<D>& s, int t) {
-  constexpr int C = Stage<D>::kChunks;
+__device__ __forceinline__ const v4u* row_chunk(const uint16_t* src, const BlockSrc& bs, const AttnArgs& p, int b,
+                                                int h, int key, int c) {
+  const int kk = min(key, bs.lim - 1);
+  return reinterpret_cast<const v4u*>(src + ((static_cast<int64_t>(b) * bs.stride + kk) * p.Hkv + h) * D + 8 * c);
+}
+
+// The 16-byte chunks of one block that staging thread t (0 .. 255 within its role)
+// moves: K rows as they are (chunk = 8 consecutive d of one key), and V as pairs of keys
+// at the same 8 d, so that the transposed write packs two keys per 32-bit LDS word.
+template <int D>
+struct StageK {
+  static constexpr int kChunks = D / 8;
+  static constexpr int kPer = (kKB * kChunks + kStageThreads - 1) / kStageThreads;
+  v4u k[kPer];
+};
+struct StageV {
+  v4u v0, v1;
+};
+
+// The loads keep the raw values; the stores zero the rows past the block's end, so no
+// instruction waits for a load before its data go to LDS.
+template <int D>
+__device__ __forceinline__ void load_k(const AttnArgs& p, StageK<D>& s, const BlockSrc& bs, int b, int h, int t) {
+  constexpr int C = StageK<D>::kChunks;
 #pragma unroll
-  for (int i = 0; i < Stage<D>::kKPerThread; ++i) {
-    const int id = t + kAttnThreads * i;
-    const int row = id / C, c = id % C;
-    if (row < kKB) *reinterpret_cast<v4u*>(&lds.k[st][row][8 * c]) = s.k[i];
+  for (int i = 0; i < StageK<D>::kPer; ++i) {
+    const int id = t + kStageThreads * i;
+    s.k[i] = *row_chunk<D>(bs.k, bs, p, b, h, bs.base + min(id / C, kKB - 1), id % C);
   }
+}
+
+template <int D>
+__device__ __forceinline__ void load_v(const AttnArgs& p, StageV& s, const BlockSrc& bs, int b, int h, int t) {
+  constexpr int C = D / 8;
+  const int kp = t % 16, c = min(t / 16, C - 1);
+  const int k0 = bs.base + 2 * kp;
+  s.v0 = *row_chunk<D>(bs.v, bs, p, b, h, k0, c);
+  s.v1 = *row_chunk<D>(bs.v, bs, p, b, h, k0 + 1, c);
+}
+
+template <int D>
+__device__ __forceinline__ void store_k(AttnLds<D>& lds, int st, const StageK<D>& s, const BlockSrc& bs, int t) {
+  constexpr int C = StageK<D>::kChunks;
+  const v4u zero = v4u{0u, 0u, 0u, 0u};
+#pragma unroll
+  for (int i = 0; i < StageK<D>::kPer; ++i) {
+    const int id = t + kStageThreads * i;
+    const int row = id / C, c = id % C;
+    if (row < kKB) *reinterpret_cast<v4u*>(&lds.k[st][row][8 * c]) = bs.base + row < bs.lim ? s.k[i] : zero;
+  }
+}
+
+template <int D>
+__device__ __forceinline__ void store_v(AttnLds<D>& lds, int st, const StageV& s, const BlockSrc& bs, int t) {
+  constexpr int C = D / 8;
   const int kp = t % 16, c = t / 16;
+  const int k0 = bs.base + 2 * kp;
   if (c < C) {
+    const v4u zero = v4u{0u, 0u, 0u, 0u};
+    const v4u v0 = k0 < bs.lim ? s.v0 : zero, v1 = k0 + 1 < bs.lim ? s.v1 : zero;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      const uint32_t a = (s.v0[e / 2] >> (16 * (e % 2))) & 0xFFFFu;
-      const uint32_t bb = (s.v1[e / 2] >> (16 * (e % 2))) & 0xFFFFu;
+      const uint32_t a = (v0[e / 2] >> (16 * (e % 2))) & 0xFFFFu;
+      const uint32_t bb = (v1[e / 2] >> (16 * (e % 2))) & 0xFFFFu;
       *reinterpret_cast<uint32_t*>(&lds.vt[st][8 * c + e][2 * kp]) = a | (bb << 16);
     }
   }
 }
 
+// The lane's 8 keys of a block as visibility bits: bit t is key 4 kg + t (t < 4) or
+// 16 + 4 kg + t - 4 (t >= 4), the order of the score accumulators.
+__device__ __forceinline__ uint32_t lane_bits(uint32_t keys32, int kg) {
+  return ((keys32 >> (4 * kg)) & 0xFu) | (((keys32 >> (16 + 4 * kg)) & 0xFu) << 4);
+}
+
+// Which keys of a block a score wave's lane sees, per tile.  The context blocks come
+// first, then the tree's; `ml` is the tile row's node in the mask rows staged in LDS, or
+// -1 for a row with no query.
+struct VisCtx {
+  int P, npb, nn, kg;
+};
+
 template <int D>
+__device__ __forceinline__ uint32_t tile_vis(const AttnLds<D>& lds, const VisCtx& v, int blk, int ml) {
+  if (ml < 0) return 0u;
+  if (blk < v.npb) {
+    const int left = v.P - blk * kKB;  // >= 1 keys of the block inside the prefix
+    return lane_bits(left >= kKB ? ~0u : ((1u << left) - 1u), v.kg);
+  }
+  const int tb = blk - v.npb;
+  const int left = v.nn - tb * kKB;
+  const uint32_t in = left >= kKB ? ~0u : ((1u << left) - 1u);
+  return lane_bits(lds.mask[ml][tb] & in, v.kg);
+}
+
+// Largest visible score of a tile in log2 units (kAll: every key is visible).
+template <bool kAll>
+__device__ __forceinline__ float tile_max(v4f s0, v4f s1, uint32_t vis, float c) {
+  float m;
+  if (kAll) {
+    m = fmaxf(fmaxf(fmaxf(s0[0], s0[1]), fmaxf(s0[2], s0[3])), fmaxf(fmaxf(s1[0], s1[1]), fmaxf(s1[2], s1[3])));
+  } else {
+    m = neg_inf();
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      m = ((vis >> e) & 1u) ? fmaxf(m, s0[e]) : m;
+      m = ((vis >> (4 + e)) & 1u) ? fmaxf(m, s1[e]) : m;
+    }
+  }
+  return m * c;
+}
+
+template <bool B>
+struct BoolTag {
+  static constexpr bool value = B;
+};
+
+// Score wave state: query fragments, the score tiles of one block (keys 0..15 and
+// 16..31), the running maximum (log2 units) and this lane's partial sum of weights.
+template <int D, int TW>
+struct ScoreState {
+  v4u qf[TW][D / 32];
+  v4f s0[TW], s1[TW];
+  float m_run[TW], l_part[TW];
+};
+
+// The score tiles of K slot `ks` for every tile.
+template <int D, int TW>
+__device__ __forceinline__ void block_scores(const AttnLds<D>& lds, int ks, ScoreState<D, TW>& S, int lr, int kg) {
+#pragma unroll
+  for (int j = 0; j < TW; ++j) S.s0[j] = S.s1[j] = v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int s = 0; s < D / 32; ++s) {
+    const v4u a0 = *reinterpret_cast<const v4u*>(&lds.k[ks][lr][32 * s + 8 * kg]);
+    const v4u a1 = *reinterpret_cast<const v4u*>(&lds.k[ks][16 + lr][32 * s + 8 * kg]);
+#pragma unroll
+    for (int j = 0; j < TW; ++j) {
+      S.s0[j] = mfma_bf16(a0, S.qf[j][s], S.s0[j]);
+      S.s1[j] = mfma_bf16(a1, S.qf[j][s], S.s1[j]);
+    }
+  }
+}
+
+// Raise the running maxima that fell more than the gap behind (uniform over each query's
+// 4 lanes) and rescale the sums at once; the factors go to the output wave through LDS
+// slot `as` with a flag, written for every block.
+template <int D, int TW>
+__device__ __forceinline__ void raise_max(AttnLds<D>& lds, int as, int pair, int lane, ScoreState<D, TW>& S,
+                                          const float (&mx)[TW]) {
+  bool grow = false;
+#pragma unroll
+  for (int j = 0; j < TW; ++j) grow = grow || (mx[j] > S.m_run[j] + kRescaleGap);
+  const bool resc = ballot(grow) != 0ull;
+  if (lane == 0) lds.rescale[as][pair] = resc ? 1u : 0u;
+  if (resc) {
+#pragma unroll
+    for (int j = 0; j < TW; ++j) {
+      float m = mx[j];
+      m = fmaxf(m, __shfl_xor(m, 16));
+      m = fmaxf(m, __shfl_xor(m, 32));
+      float alpha = 1.f;
+      if (m > S.m_run[j] + kRescaleGap) {
+        alpha = __builtin_amdgcn_exp2f(S.m_run[j] - m);
+        S.m_run[j] = m;
+        S.l_part[j] *= alpha;
+      }
+      if (lane < 16) lds.alpha[as][pair + kPairs * j][lane] = alpha;
+    }
+  }
+}
+
+// A score wave's step on block blk.  Tile by tile: the weights from the tile's scores,
+// written to LDS for the output wave, then the next block's scores of keys 0..15 (K slot
+// `ks`) into the same registers; then keys 16..31 of every tile, so only half of the
+// next block's K fragments are live at a time.  Ends with the next block's maxima.
+// kFull: every key of the block is visible to every query; kFullNext: the same for the
+// next block.
+template <int D, int TW, bool kFull, bool kFullNext>
+__device__ __forceinline__ void score_block(AttnLds<D>& lds, int blk, int ks, int ps, int slot0,
+                                            ScoreState<D, TW>& S, const VisCtx& vc, const int (&ml)[TW], float c,
+                                            int lane, float (&mx_next)[TW]) {
+  constexpr int DS = D / 32;
+  const int lr = lane & 15, kg = lane >> 4;
+  v4u kf[DS];
+#pragma unroll
+  for (int s = 0; s < DS; ++s) kf[s] = *reinterpret_cast<const v4u*>(&lds.k[ks][lr][32 * s + 8 * kg]);
+#pragma unroll
+  for (int j = 0; j < TW; ++j) {
+    // A stored row sees a visible key in its first block, so m_run is finite there.
+    const float nm = -S.m_run[j];
+    float pr[8];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      pr[e] = __builtin_amdgcn_exp2f(fmaf(S.s0[j][e], c, nm));
+      pr[4 + e] = __builtin_amdgcn_exp2f(fmaf(S.s1[j][e], c, nm));
+    }
+    if (!kFull) {
+      const uint32_t vis = tile_vis<D>(lds, vc, blk, ml[j]);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) pr[e] = ((vis >> e) & 1u) ? pr[e] : 0.f;
+    }
+    S.l_part[j] += ((pr[0] + pr[1]) + (pr[2] + pr[3])) + ((pr[4] + pr[5]) + (pr[6] + pr[7]));
+    lds.p[ps][slot0 + kPairs * j][lane] = v4u{pack_bf16(pr[0], pr[1]), pack_bf16(pr[2], pr[3]),
+                                              pack_bf16(pr[4], pr[5]), pack_bf16(pr[6], pr[7])};
+    v4f n0 = v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < DS; ++s) n0 = mfma_bf16(kf[s], S.qf[j][s], n0);
+    S.s0[j] = n0;
+  }
+  // Keep the second half's fragment loads below the first half (register pressure).
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int s = 0; s < DS; ++s) kf[s] = *reinterpret_cast<const v4u*>(&lds.k[ks][16 + lr][32 * s + 8 * kg]);
+#pragma unroll
+  for (int j = 0; j < TW; ++j) {
+    v4f n1 = v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < DS; ++s) n1 = mfma_bf16(kf[s], S.qf[j][s], n1);
+    S.s1[j] = n1;
+  }
+  // The next block's maxima (none when this is the last block: its scores are stale).
+#pragma unroll
+  for (int j = 0; j < TW; ++j) {
+    const uint32_t vis = kFullNext ? 0xFFu : (blk + 1 < vc.npb + (vc.nn + kKB - 1) / kKB
+                                                  ? tile_vis<D>(lds, vc, blk + 1, ml[j]) : 0u);
+    mx_next[j] = tile_max<kFullNext>(S.s0[j], S.s1[j], vis, c);
+  }
+}
+
+template <int D, int TW>
 __global__ __launch_bounds__(kAttnThreads) void tree_attention_kernel(AttnArgs p) {
-  constexpr int DS = D / 32;  // k steps of S^T
-  constexpr int DT = D / 16;  // output tiles of O^T
-  constexpr int TW = kTilesPerWave;
+  constexpr int DS = D / 32;
+  constexpr int DT = D / 16;
   __shared__ AttnLds<D> lds;
 
   // Workgroup -> (sequence, key/value head, row group).  Consecutive workgroups go to
@@ -162,8 +365,11 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attention_kernel(AttnArgs p
 
   const int t = static_cast<int>(threadIdx.x);
   const int w = __builtin_amdgcn_readfirstlane(t / kWave);
+  const int pair = w % kPairs;
+  const bool scorer = w < kPairs;
   const int lane = t % kWave;
   const int lr = lane & 15, kg = lane >> 4;
+  const int ts = t - kStageThreads;  // staging thread index of the output waves
 
   const int P = min(max(p.prefix_len[b], 0), static_cast<int>(p.Pmax));
   const int nn = min(max(p.n_nodes[b], 0), p.N);
@@ -171,198 +377,196 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attention_kernel(AttnArgs p
   const int nblk = npb + (nn + kKB - 1) / kKB;
   const int words = (p.N + 31) / 32;
 
-  // Tile j of this wave holds query rows r0 + 16 (w + 8 j) + [0, 16); this lane is the
-  // column lr of each.
+  // Tile j of this pair holds query rows r0 + 16 (pair + 4 j) + [0, 16) (slot pair + 4 j
+  // of the LDS hand-over); this lane is the column lr of each.  Rows past R (and nodes
+  // past n_nodes) have zero queries and are never stored.
   const int r0 = grp * kAttnRows;
-  int ntile = 0;  // tiles of this wave with at least one row (wave-uniform)
-#pragma unroll
-  for (int j = 0; j < TW; ++j) ntile += (r0 + 16 * (w + kAttnWaves * j) < p.R) ? 1 : 0;
-  int n_of[TW], head_of[TW];
-  bool rin[TW], live[TW];
-  v4u qf[TW][DS];
-  const uint32_t* mrow[TW];
-#pragma unroll
-  for (int j = 0; j < TW; ++j) {
-    const int r = r0 + 16 * (w + kAttnWaves * j) + lr;
-    rin[j] = r < p.R;
-    n_of[j] = rin[j] ? r / p.g : 0;
-    head_of[j] = h * p.g + (rin[j] ? r % p.g : 0);
-    live[j] = rin[j] && n_of[j] < nn;
-    const uint16_t* qr = p.q + ((static_cast<int64_t>(b) * p.N + n_of[j]) * p.H + head_of[j]) * D;
-#pragma unroll
-    for (int s = 0; s < DS; ++s) {
-      const v4u v = *reinterpret_cast<const v4u*>(qr + 32 * s + 8 * kg);
-      qf[j][s] = live[j] ? v : v4u{0u, 0u, 0u, 0u};
-    }
-    mrow[j] = p.mask + (static_cast<int64_t>(b) * p.N + n_of[j]) * words;
-  }
-
-  v4f o[TW][DT];
-  float m_run[TW], l_part[TW];
-#pragma unroll
-  for (int j = 0; j < TW; ++j) {
-#pragma unroll
-    for (int i = 0; i < DT; ++i) o[j][i] = v4f{0.f, 0.f, 0.f, 0.f};
-    m_run[j] = neg_inf();
-    l_part[j] = 0.f;
-  }
+  const int n_base = r0 / p.g;  // the group's first node
+  // Row r of tile j: node r / g, head h g + r % g; a row has a query when r < R and its
+  // node is below n_nodes.
+  auto tile_row = [&](int j) { return r0 + 16 * (pair + kPairs * j) + lr; };
+  auto has_query = [&](int r) { return r < p.R && r / p.g < nn; };
   const float c = p.scale_log2;
 
-  Stage<D> sg;
-  if (nblk > 0) {
-    stage_load<D>(p, sg, b, h, 0, npb, P, nn, t);
-    stage_store<D>(lds, 0, sg, t);
+  // The mask rows of the group's nodes (at most 320) into LDS.
+  const int n_hi = min(p.N, (r0 + kAttnRows + p.g - 1) / p.g);
+  for (int e = t; e < (n_hi - n_base) * words; e += kAttnThreads) {
+    const int ln = e / words, wd = e % words;
+    lds.mask[ln][wd] = p.mask[(static_cast<int64_t>(b) * p.N + n_base + ln) * words + wd];
   }
-  // Nothing is in flight when the loop starts: the first MFMA of each block then waits
-  // for no global load, and the next block's loads stay in flight behind the compute.
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  for (int blk = 0; blk < nblk; ++blk) {
-    const int st = blk & 1;
-    // This block's mask words, then the next block's K/V (the last block loads itself
-    // again, unused), all unconditional.
-    const int tb = blk >= npb ? blk - npb : 0;
-    uint32_t mw[TW];
-#pragma unroll
-    for (int j = 0; j < TW; ++j) mw[j] = mrow[j][tb];
-    stage_load<D>(p, sg, b, h, blk + 1 < nblk ? blk + 1 : blk, npb, P, nn, t);
 
-    // ---- S^T = K Q^T for 32 keys and each tile ----
-    v4f s0[TW], s1[TW];
-#pragma unroll
-    for (int j = 0; j < TW; ++j) s0[j] = s1[j] = v4f{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int s = 0; s < DS; ++s) {
-      const v4u a0 = *reinterpret_cast<const v4u*>(&lds.k[st][lr][32 * s + 8 * kg]);
-      const v4u a1 = *reinterpret_cast<const v4u*>(&lds.k[st][16 + lr][32 * s + 8 * kg]);
-#pragma unroll
-      for (int j = 0; j < TW; ++j) {
-        if (j < ntile) {
-          s0[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_v8bf(a0), as_v8bf(qf[j][s]), s0[j], 0, 0, 0);
-          s1[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_v8bf(a1), as_v8bf(qf[j][s]), s1[j], 0, 0, 0);
-        }
-      }
-    }
-
-    // ---- softmax weights: which of the lane's 8 keys each query sees ----
-    // Bit t of vis: key 4 kg + t (t < 4) or 16 + 4 kg + t - 4 (t >= 4) of this block.
-    const bool full = blk < npb && (blk + 1) * kKB <= P;  // a context block wholly inside the prefix
-    uint32_t vis[TW];
-    if (full) {
-#pragma unroll
-      for (int j = 0; j < TW; ++j) vis[j] = live[j] ? 0xFFu : 0u;
-    } else if (blk < npb) {
-      const int left = P - blk * kKB;  // 1..31 keys of the block inside the prefix
-      const uint32_t all = (1u << left) - 1u;
-      const uint32_t v = ((all >> (4 * kg)) & 0xFu) | (((all >> (16 + 4 * kg)) & 0xFu) << 4);
-#pragma unroll
-      for (int j = 0; j < TW; ++j) vis[j] = live[j] ? v : 0u;
-    } else {
-      const int left = nn - tb * kKB;
-      const uint32_t in = left >= 32 ? ~0u : ((1u << left) - 1u);
-#pragma unroll
-      for (int j = 0; j < TW; ++j) {
-        const uint32_t bits = live[j] ? (mw[j] & in) : 0u;
-        vis[j] = ((bits >> (4 * kg)) & 0xFu) | (((bits >> (16 + 4 * kg)) & 0xFu) << 4);
-      }
-    }
-    // Fully visible blocks use the scores as they are; only partial blocks mask: the
-    // maximum over visible scores, and a zero weight for each invisible key.
-    bool grow = false;
-    float mxs[TW];
+  if (scorer) {
+    // ---------------- score wave ----------------
+    ScoreState<D, TW> S;
+    int ml[TW];
 #pragma unroll
     for (int j = 0; j < TW; ++j) {
-      float mx;
-      if (full) {
-        mx = fmaxf(fmaxf(fmaxf(s0[j][0], s0[j][1]), fmaxf(s0[j][2], s0[j][3])),
-                   fmaxf(fmaxf(s1[j][0], s1[j][1]), fmaxf(s1[j][2], s1[j][3])));
-      } else {
-        mx = neg_inf();
+      const int r = tile_row(j);
+      const bool live = has_query(r);
+      ml[j] = live ? r / p.g - n_base : -1;
+      const uint16_t* qr = p.q + ((static_cast<int64_t>(b) * p.N + (live ? r / p.g : 0)) * p.H + h * p.g +
+                                  (live ? r % p.g : 0)) * D;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          mx = ((vis[j] >> e) & 1u) ? fmaxf(mx, s0[j][e]) : mx;
-          mx = ((vis[j] >> (4 + e)) & 1u) ? fmaxf(mx, s1[j][e]) : mx;
-        }
+      for (int s = 0; s < DS; ++s) {
+        const v4u v = *reinterpret_cast<const v4u*>(qr + 32 * s + 8 * kg);
+        S.qf[j][s] = live ? v : v4u{0u, 0u, 0u, 0u};
       }
-      mxs[j] = mx * c;
-      grow = grow || (mxs[j] > m_run[j] + kRescaleGap);
+      S.l_part[j] = 0.f;
+      S.m_run[j] = 0.f;
     }
-    if (ballot(grow)) {
-      // Raise the running maxima that fell behind (uniform over each query's 4 lanes).
+    const VisCtx vc{P, npb, nn, kg};
+    if (lane == 0) lds.rescale[0][pair] = 0u;
+    // Staging of the odd steps: step s stores K block s + 2 and V block s + 1, loaded two
+    // steps earlier, and loads K block s + 4 and V block s + 3 (the output waves do the
+    // same on the even steps).
+    StageK<D> sk;
+    StageV sv;
+    const int last = max(nblk - 1, 0);
+    if (nblk > 0) {
+      load_k<D>(p, sk, block_src(p, min(3, last), npb, P, nn), b, h, t);
+      load_v<D>(p, sv, block_src(p, min(2, last), npb, P, nn), b, h, t);
+    }
+    __syncthreads();  // K blocks 0 and 1, V block 0 and the mask rows are in
+    if (nblk > 0) {
+      block_scores<D, TW>(lds, 0, S, lr, kg);
+      // A row with a query sees a key of its first block (key 0 of the context, or the
+      // root), so its maximum is finite; rows with no query keep 0 and never rescale.
 #pragma unroll
       for (int j = 0; j < TW; ++j) {
-        float mx = mxs[j];
-        mx = fmaxf(mx, __shfl_xor(mx, 16));
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
-        if (mx > m_run[j] + kRescaleGap) {
-          const float alpha = __builtin_amdgcn_exp2f(m_run[j] - mx);
-          m_run[j] = mx;
-          l_part[j] *= alpha;
-#pragma unroll
-          for (int i = 0; i < DT; ++i) o[j][i] *= alpha;
-        }
+        float m = tile_max<false>(S.s0[j], S.s1[j], tile_vis<D>(lds, vc, 0, ml[j]), c);
+        m = fmaxf(m, __shfl_xor(m, 16));
+        m = fmaxf(m, __shfl_xor(m, 32));
+        S.m_run[j] = ml[j] >= 0 ? m : 0.f;
       }
     }
-    v4u pt[TW];
+    __syncthreads();  // K slot 0 is refilled during the first step
+    // One step per block; the last step's "next" scores come from a stale K slot and are
+    // never used.  The rescale found on the next block's scores goes to the output wave
+    // with it.
+    auto step = [&](auto full, auto full_next, int blk) {
+      if (blk & 1) {
+        if (blk + 2 < nblk) store_k<D>(lds, blk & 1, sk, block_src(p, blk + 2, npb, P, nn), t);
+        if (blk + 1 < nblk) store_v<D>(lds, (blk + 1) % 3, sv, block_src(p, blk + 1, npb, P, nn), t);
+        load_k<D>(p, sk, block_src(p, min(blk + 4, last), npb, P, nn), b, h, t);
+        load_v<D>(p, sv, block_src(p, min(blk + 3, last), npb, P, nn), b, h, t);
+      }
+      float mx[TW];
+      score_block<D, TW, decltype(full)::value, decltype(full_next)::value>(lds, blk, (blk + 1) & 1, blk & 1, pair,
+                                                                           S, vc, ml, c, lane, mx);
+      raise_max<D, TW>(lds, (blk + 1) % 3, pair, lane, S, mx);
+      __syncthreads();
+    };
+    // Blocks 0 .. nf - 1 lie wholly inside the context; each loop below runs one variant.
+    const int nf = P / kKB;
+    int blk = 0;
+    for (; blk + 1 < nf; ++blk) step(BoolTag<true>{}, BoolTag<true>{}, blk);
+    if (blk < nf) step(BoolTag<true>{}, BoolTag<false>{}, blk++);
+    for (; blk < nblk; ++blk) step(BoolTag<false>{}, BoolTag<false>{}, blk);
+    __syncthreads();  // the output wave's last block
+    // Final maximum and sum per query for the output wave.
 #pragma unroll
     for (int j = 0; j < TW; ++j) {
-      // A stored row sees a visible key in its first block, so m_run is finite there; rows
-      // never stored may turn NaN, which stays in their own column.
-      const float nm = -m_run[j];
-      float pr[8];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        pr[e] = __builtin_amdgcn_exp2f(fmaf(s0[j][e], c, nm));
-        pr[4 + e] = __builtin_amdgcn_exp2f(fmaf(s1[j][e], c, nm));
+      float l = S.l_part[j] + __shfl_xor(S.l_part[j], 16);
+      l = l + __shfl_xor(l, 32);
+      if (kg == 0) {
+        lds.fin_m[pair + kPairs * j][lr] = S.m_run[j];
+        lds.fin_l[pair + kPairs * j][lr] = l;
       }
-      if (!full) {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) pr[e] = ((vis[j] >> e) & 1u) ? pr[e] : 0.f;
-      }
-      l_part[j] += ((pr[0] + pr[1]) + (pr[2] + pr[3])) + ((pr[4] + pr[5]) + (pr[6] + pr[7]));
-      pt[j] = v4u{pack_bf16(pr[0], pr[1]), pack_bf16(pr[2], pr[3]), pack_bf16(pr[4], pr[5]),
-                  pack_bf16(pr[6], pr[7])};
     }
-
-    // ---- O^T += V^T P^T ----
-#pragma unroll
-    for (int i = 0; i < DT; ++i) {
-      const uint16_t* vrow = &lds.vt[st][16 * i + lr][0];
-      const v2u lo = *reinterpret_cast<const v2u*>(vrow + 4 * kg);
-      const v2u hi = *reinterpret_cast<const v2u*>(vrow + 16 + 4 * kg);
-      const v4u a = v4u{lo.x, lo.y, hi.x, hi.y};
-#pragma unroll
-      for (int j = 0; j < TW; ++j)
-        if (j < ntile) o[j][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_v8bf(a), as_v8bf(pt[j]), o[j][i], 0, 0, 0);
-    }
-
-    if (blk + 1 < nblk) stage_store<D>(lds, st ^ 1, sg, t);
     __syncthreads();
-  }
-
-  // ---- normalise and store: lane (lr, kg) holds d = 16 i + 4 kg + e of its query ----
+  } else {
+    // ---------------- output wave ----------------
+    v4f o[TW][DT];
 #pragma unroll
-  for (int j = 0; j < TW; ++j) {
-    float l = l_part[j] + __shfl_xor(l_part[j], 16);
-    l = l + __shfl_xor(l, 32);
-    if (!rin[j]) continue;
-    const bool has = live[j] && l > 0.f;
-    const float inv = has ? 1.f / l : 0.f;
-    const int64_t orow = (static_cast<int64_t>(b) * p.N + n_of[j]) * p.H + head_of[j];
-    if (p.out_f32) {
-      float* op = static_cast<float*>(p.out) + orow * D;
+    for (int j = 0; j < TW; ++j)
 #pragma unroll
-      for (int i = 0; i < DT; ++i)
-        *reinterpret_cast<v4f*>(op + 16 * i + 4 * kg) = has ? o[j][i] * inv : v4f{0.f, 0.f, 0.f, 0.f};
-    } else {
-      uint16_t* op = static_cast<uint16_t*>(p.out) + orow * D;
-#pragma unroll
-      for (int i = 0; i < DT; ++i) {
-        const v4f v = has ? o[j][i] * inv : v4f{0.f, 0.f, 0.f, 0.f};
-        *reinterpret_cast<v2u*>(op + 16 * i + 4 * kg) = v2u{pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3])};
+      for (int i = 0; i < DT; ++i) o[j][i] = v4f{0.f, 0.f, 0.f, 0.f};
+    // Staging of the even steps: step s stores K block s + 2 and V block s + 1, loaded two
+    // steps earlier, then loads K block s + 4 and V block s + 3, so two steps cover their
+    // latency (the score waves stage the odd steps).
+    StageK<D> sk;
+    StageV sv;
+    const int last = max(nblk - 1, 0);
+    if (nblk > 0) {
+      const BlockSrc b0 = block_src(p, 0, npb, P, nn);
+      load_k<D>(p, sk, b0, b, h, ts);
+      load_v<D>(p, sv, b0, b, h, ts);
+      store_k<D>(lds, 0, sk, b0, ts);
+      store_v<D>(lds, 0, sv, b0, ts);
+      if (nblk > 1) {
+        const BlockSrc b1 = block_src(p, 1, npb, P, nn);
+        load_k<D>(p, sk, b1, b, h, ts);
+        store_k<D>(lds, 1, sk, b1, ts);
       }
+      // The first step stores K block 2 and V block 1.
+      load_k<D>(p, sk, block_src(p, min(2, last), npb, P, nn), b, h, ts);
+      load_v<D>(p, sv, block_src(p, min(1, last), npb, P, nn), b, h, ts);
     }
-    if (p.lse && kg == 0) p.lse[orow] = has ? (m_run[j] + __builtin_amdgcn_logf(l)) * kLn2 : neg_inf();
+    __syncthreads();  // K blocks 0 and 1, V block 0 and the mask rows are in
+    __syncthreads();  // the score waves have read K slot 0
+    for (int blk = 0; blk <= nblk; ++blk) {
+      // K block blk + 2 replaces block blk (read by the score waves in the previous step),
+      // V block blk + 1 replaces block blk - 2 (read here in the previous step).
+      if (!(blk & 1)) {
+        if (blk + 2 < nblk) store_k<D>(lds, blk & 1, sk, block_src(p, blk + 2, npb, P, nn), ts);
+        if (blk + 1 < nblk) store_v<D>(lds, (blk + 1) % 3, sv, block_src(p, blk + 1, npb, P, nn), ts);
+        if (blk < nblk) {  // clamped; unused past the end
+          load_k<D>(p, sk, block_src(p, min(blk + 4, last), npb, P, nn), b, h, ts);
+          load_v<D>(p, sv, block_src(p, min(blk + 3, last), npb, P, nn), b, h, ts);
+        }
+      }
+      if (blk > 0) {
+        // O^T += V^T P^T for block blk - 1, after the rescale its scores asked for.
+        const int qb = blk - 1, ps = qb & 1, vs = qb % 3;
+        if (lds.rescale[vs][pair] != 0u) {
+#pragma unroll
+          for (int j = 0; j < TW; ++j) {
+            const float a = lds.alpha[vs][pair + kPairs * j][lr];
+#pragma unroll
+            for (int i = 0; i < DT; ++i) o[j][i] *= a;
+          }
+        }
+        v4u pt[TW];
+#pragma unroll
+        for (int j = 0; j < TW; ++j) pt[j] = lds.p[ps][pair + kPairs * j][lane];
+#pragma unroll
+        for (int i = 0; i < DT; ++i) {
+          const uint16_t* vrow = &lds.vt[vs][16 * i + lr][0];
+          const v2u lo = *reinterpret_cast<const v2u*>(vrow + 4 * kg);
+          const v2u hi = *reinterpret_cast<const v2u*>(vrow + 16 + 4 * kg);
+          const v4u a = v4u{lo.x, lo.y, hi.x, hi.y};
+#pragma unroll
+          for (int j = 0; j < TW; ++j) o[j][i] = mfma_bf16(a, pt[j], o[j][i]);
+        }
+      }
+      __syncthreads();
+    }
+    __syncthreads();  // the final statistics are in
+    // ---- normalise and store: lane (lr, kg) holds d = 16 i + 4 kg + e of its query ----
+#pragma unroll
+    for (int j = 0; j < TW; ++j) {
+      const int r = tile_row(j);
+      if (r >= p.R) continue;
+      const float l = lds.fin_l[pair + kPairs * j][lr];
+      const bool has = has_query(r) && l > 0.f;
+      const float inv = has ? 1.f / l : 0.f;
+      const int64_t orow = (static_cast<int64_t>(b) * p.N + r / p.g) * p.H + h * p.g + r % p.g;
+      if (p.out_f32) {
+        float* op = static_cast<float*>(p.out) + orow * D;
+#pragma unroll
+        for (int i = 0; i < DT; ++i)
+          *reinterpret_cast<v4f*>(op + 16 * i + 4 * kg) = has ? o[j][i] * inv : v4f{0.f, 0.f, 0.f, 0.f};
+      } else {
+        uint16_t* op = static_cast<uint16_t*>(p.out) + orow * D;
+#pragma unroll
+        for (int i = 0; i < DT; ++i) {
+          const v4f v = has ? o[j][i] * inv : v4f{0.f, 0.f, 0.f, 0.f};
+          *reinterpret_cast<v2u*>(op + 16 * i + 4 * kg) = v2u{pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3])};
+        }
+      }
+      if (p.lse && kg == 0)
+        p.lse[orow] = has ? (lds.fin_m[pair + kPairs * j][lr] + __builtin_amdgcn_logf(l)) * kLn2 : neg_inf();
+    }
   }
 }
 
@@ -463,10 +667,19 @@ hipError_t launch_tree_attention(const TreeAttnArgs& a, hipStream_t stream) {
   p.out_f32 = a.out_f32;
   p.lse = a.lse;
   const dim3 grid(static_cast<unsigned>(p.B * p.Hkv * p.groups));
-  if (a.D == 128)
-    hipLaunchKernelGGL(tree_attention_kernel<128>, grid, dim3(kAttnThreads), 0, stream, p);
-  else
-    hipLaunchKernelGGL(tree_attention_kernel<64>, grid, dim3(kAttnThreads), 0, stream, p);
+  // Tiles per pair: enough for the group's rows (1, 3 or 5; rows past R are empty tiles).
+  const int tiles = (min(p.R, kAttnRows) + 15) / 16;
+  const int tw = (tiles + kPairs - 1) / kPairs;
+  if (a.D == 128) {
+    if (tw <= 1)
+      hipLaunchKernelGGL((tree_attention_kernel<128, 1>), grid, dim3(kAttnThreads), 0, stream, p);
+    else if (tw <= 3)
+      hipLaunchKernelGGL((tree_attention_kernel<128, 3>), grid, dim3(kAttnThreads), 0, stream, p);
+    else
+      hipLaunchKernelGGL((tree_attention_kernel<128, kMaxTiles>), grid, dim3(kAttnThreads), 0, stream, p);
+  } else {
+    hipLaunchKernelGGL((tree_attention_kernel<64, kMaxTiles>), grid, dim3(kAttnThreads), 0, stream, p);
+  }
   return hipGetLastError();
 }
 
