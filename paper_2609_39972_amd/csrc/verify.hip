@@ -57,10 +57,11 @@ constexpr int kVtStride = 36;  // bf16 per V^T row: 32 keys + 4, so the transpos
 constexpr int kMaskWords = 8;  // mask words per node (N <= 256)
 constexpr float kRescaleGap = 8.f;  // log2 units a score may exceed the running maximum
 
+constexpr int kRing = 4;  // K and V blocks in LDS, loaded straight from global memory
+
 template <int D>
 struct AttnLds {
-  uint16_t k[2][kKB][D + 8];          // K blocks i + 1 (read) and i + 2 (staged)
-  uint16_t vt[3][D][kVtStride];       // V^T blocks i - 1 (read), i, i + 1 (staged)
+  uint16_t vt[3][D][kVtStride];       // V^T blocks i - 1 (read), i (transposed)
   v4u p[2][kSlots][kWave];            // P^T of blocks i (written) and i - 1 (read), per lane
   float alpha[3][kSlots][16];         // output rescale factor per query, blocks i - 1 .. i + 1
   uint32_t rescale[3][kPairs];        // nonzero: the pair's output must be rescaled first
@@ -101,7 +102,7 @@ struct AttnArgs {
 
 // Where the keys and values of block `blk` of sequence b, head h live: the context for
 // blk < npb, else the tree.  Rows at or past `lim` do not exist; reads are clamped to row
-// lim - 1 and the value dropped, so every load is issued on every path.
+// lim - 1.
 struct BlockSrc {
   const uint16_t* k;
   const uint16_t* v;
@@ -115,67 +116,72 @@ __device__ __forceinline__ BlockSrc block_src(const AttnArgs& p, int blk, int np
                   tree ? (blk - npb) * kKB : blk * kKB, tree ? nn : P};
 }
 
-template <int D>
-__device__ __forceinline__ const v4u* row_chunk(const uint16_t* src, const BlockSrc& bs, const AttnArgs& p, int b,
-                                                int h, int key, int c) {
-  const int kk = min(key, bs.lim - 1);
-  return reinterpret_cast<const v4u*>(src + ((static_cast<int64_t>(b) * bs.stride + kk) * p.Hkv + h) * D + 8 * c);
-}
+// K and V blocks go from global memory straight into LDS rings (global_load_lds, 16 bytes
+// per lane, each wave instruction filling 1 KB of consecutive LDS), so the loads of
+// several blocks are in flight without holding registers.  A block is 32 rows of D
+// bf16, C = D / 8 chunks of 16 bytes per row; chunk c of row r sits at chunk position
+// c ^ swz(r) of the row, which keeps the MFMA fragment reads (K) and the transposing
+// reads (V) free of bank conflicts.  Rows past the block's end are copies of its last
+// row: their weights are exactly 0 and their values finite.
+__device__ __forceinline__ int swz_k(int row, int C) { return row & (C - 1); }
+__device__ __forceinline__ int swz_v(int row, int C) { return (row >> 1) & (C - 1); }
 
-// The 16-byte chunks of one block that staging thread t (0 .. 255 within its role)
-// moves: K rows as they are (chunk = 8 consecutive d of one key), and V as pairs of keys
-// at the same 8 d, so that the transposed write packs two keys per 32-bit LDS word.
-template <int D>
-struct StageK {
-  static constexpr int kChunks = D / 8;
-  static constexpr int kPer = (kKB * kChunks + kStageThreads - 1) / kStageThreads;
-  v4u k[kPer];
-};
-struct StageV {
-  v4u v0, v1;
-};
+// The loads of one block by one wave of a role (wave index wr, 0..3): C / 8 instructions.
+// Lane offsets within a block (row r, chunk c) are fixed; `off` holds them in bytes for
+// the wave's instructions.  The block's first row is a wave-uniform address; only a
+// block shorter than 32 rows clamps each lane's row to its last.
+template <int D, bool kV>
+struct DmaLanes {
+  static constexpr int C = D / 8;
+  static constexpr int kRowsPer = kWave / C;  // rows per instruction
+  static constexpr int kPerWave = C / 8;      // instructions per wave and block
+  uint32_t off[kPerWave];
+  int row[kPerWave];
+  int wr;
 
-// The loads keep the raw values; the stores zero the rows past the block's end, so no
-// instruction waits for a load before its data go to LDS.
-template <int D>
-__device__ __forceinline__ void load_k(const AttnArgs& p, StageK<D>& s, const BlockSrc& bs, int b, int h, int t) {
-  constexpr int C = StageK<D>::kChunks;
+  __device__ __forceinline__ DmaLanes(uint32_t row_bytes, int wave, int lane) : wr(wave) {
 #pragma unroll
-  for (int i = 0; i < StageK<D>::kPer; ++i) {
-    const int id = t + kStageThreads * i;
-    s.k[i] = *row_chunk<D>(bs.k, bs, p, b, h, bs.base + min(id / C, kKB - 1), id % C);
+    for (int k = 0; k < kPerWave; ++k) {
+      const int u = wr * kPerWave + k;
+      const int r = u * kRowsPer + lane / C, pos = lane % C;
+      const int c = pos ^ (kV ? swz_v(r, C) : swz_k(r, C));
+      row[k] = r;
+      off[k] = static_cast<uint32_t>(r) * row_bytes + 16u * static_cast<uint32_t>(c);
+    }
   }
-}
 
-template <int D>
-__device__ __forceinline__ void load_v(const AttnArgs& p, StageV& s, const BlockSrc& bs, int b, int h, int t) {
-  constexpr int C = D / 8;
-  const int kp = t % 16, c = min(t / 16, C - 1);
-  const int k0 = bs.base + 2 * kp;
-  s.v0 = *row_chunk<D>(bs.v, bs, p, b, h, k0, c);
-  s.v1 = *row_chunk<D>(bs.v, bs, p, b, h, k0 + 1, c);
-}
-
-template <int D>
-__device__ __forceinline__ void store_k(AttnLds<D>& lds, int st, const StageK<D>& s, const BlockSrc& bs, int t) {
-  constexpr int C = StageK<D>::kChunks;
-  const v4u zero = v4u{0u, 0u, 0u, 0u};
+  __device__ __forceinline__ void load(const AttnArgs& p, const BlockSrc& bs, uint32_t row_bytes, uint16_t* slot,
+                                       int b, int h) const {
+    const char* first = reinterpret_cast<const char*>(kV ? bs.v : bs.k) +
+                        (static_cast<int64_t>(b) * bs.stride + bs.base) * row_bytes + static_cast<int64_t>(h) * D * 2;
+    const int rmax = bs.lim - 1 - bs.base;
+    if (rmax >= kKB - 1) {
 #pragma unroll
-  for (int i = 0; i < StageK<D>::kPer; ++i) {
-    const int id = t + kStageThreads * i;
-    const int row = id / C, c = id % C;
-    if (row < kKB) *reinterpret_cast<v4u*>(&lds.k[st][row][8 * c]) = bs.base + row < bs.lim ? s.k[i] : zero;
+      for (int k = 0; k < kPerWave; ++k) {
+        const void* src = first + off[k];
+        __builtin_amdgcn_global_load_lds(src, slot + (wr * kPerWave + k) * kWave * 8, 16, 0, 0);
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < kPerWave; ++k) {
+        const void* src = first + (off[k] - static_cast<uint32_t>(row[k] - min(row[k], rmax)) * row_bytes);
+        __builtin_amdgcn_global_load_lds(src, slot + (wr * kPerWave + k) * kWave * 8, 16, 0, 0);
+      }
+    }
   }
-}
+};
 
+// V^T slot from a V ring slot: staging thread t (0 .. 255) takes keys 2 kp, 2 kp + 1 at
+// the 8 d of chunk c and packs two keys per 32-bit LDS word.
 template <int D>
-__device__ __forceinline__ void store_v(AttnLds<D>& lds, int st, const StageV& s, const BlockSrc& bs, int t) {
+__device__ __forceinline__ void transpose_v(AttnLds<D>& lds, int st, const uint16_t* vslot, int t) {
   constexpr int C = D / 8;
   const int kp = t % 16, c = t / 16;
-  const int k0 = bs.base + 2 * kp;
   if (c < C) {
-    const v4u zero = v4u{0u, 0u, 0u, 0u};
-    const v4u v0 = k0 < bs.lim ? s.v0 : zero, v1 = k0 + 1 < bs.lim ? s.v1 : zero;
+    const int r0 = 2 * kp;
+    const int pos = c ^ swz_v(r0, C);  // the same for rows 2 kp and 2 kp + 1
+    const v4u v0 = *reinterpret_cast<const v4u*>(vslot + r0 * D + 8 * pos);
+    const v4u v1 = *reinterpret_cast<const v4u*>(vslot + (r0 + 1) * D + 8 * pos);
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const uint32_t a = (v0[e / 2] >> (16 * (e % 2))) & 0xFFFFu;
@@ -183,6 +189,16 @@ __device__ __forceinline__ void store_v(AttnLds<D>& lds, int st, const StageV& s
       *reinterpret_cast<uint32_t*>(&lds.vt[st][8 * c + e][2 * kp]) = a | (bb << 16);
     }
   }
+}
+
+// A workgroup barrier after this wave's LDS writes and all but its N youngest loads have
+// completed.  No release fence: such a fence would also wait for every load into LDS
+// still in flight, which the rings keep several blocks deep.
+template <int N>
+__device__ __forceinline__ void ring_barrier() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4));  // vmcnt(N), lgkmcnt(0)
+  asm volatile("s_barrier" ::: "memory");
 }
 
 // The lane's 8 keys of a block as visibility bits: bit t is key 4 kg + t (t < 4) or
@@ -242,15 +258,22 @@ struct ScoreState {
   float m_run[TW], l_part[TW];
 };
 
-// The score tiles of K slot `ks` for every tile.
+// The MFMA A fragment of K rows `row` (lane's row) at k step s from a ring slot.
+template <int D>
+__device__ __forceinline__ v4u k_frag(const uint16_t* kslot, int row, int s, int kg) {
+  constexpr int C = D / 8;
+  return *reinterpret_cast<const v4u*>(kslot + row * D + 8 * ((4 * s + kg) ^ swz_k(row, C)));
+}
+
+// The score tiles of the K ring slot `kslot` for every tile.
 template <int D, int TW>
-__device__ __forceinline__ void block_scores(const AttnLds<D>& lds, int ks, ScoreState<D, TW>& S, int lr, int kg) {
+__device__ __forceinline__ void block_scores(const uint16_t* kslot, ScoreState<D, TW>& S, int lr, int kg) {
 #pragma unroll
   for (int j = 0; j < TW; ++j) S.s0[j] = S.s1[j] = v4f{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int s = 0; s < D / 32; ++s) {
-    const v4u a0 = *reinterpret_cast<const v4u*>(&lds.k[ks][lr][32 * s + 8 * kg]);
-    const v4u a1 = *reinterpret_cast<const v4u*>(&lds.k[ks][16 + lr][32 * s + 8 * kg]);
+    const v4u a0 = k_frag<D>(kslot, lr, s, kg);
+    const v4u a1 = k_frag<D>(kslot, 16 + lr, s, kg);
 #pragma unroll
     for (int j = 0; j < TW; ++j) {
       S.s0[j] = mfma_bf16(a0, S.qf[j][s], S.s0[j]);
@@ -288,20 +311,22 @@ __device__ __forceinline__ void raise_max(AttnLds<D>& lds, int as, int pair, int
 }
 
 // A score wave's step on block blk.  Tile by tile: the weights from the tile's scores,
-// written to LDS for the output wave, then the next block's scores of keys 0..15 (K slot
-// `ks`) into the same registers; then keys 16..31 of every tile, so only half of the
-// next block's K fragments are live at a time.  Ends with the next block's maxima.
+// written to LDS for the output wave, then the next block's scores (K ring slot `kslot`)
+// into the same registers.  Ends with the next block's maxima.
 // kFull: every key of the block is visible to every query; kFullNext: the same for the
 // next block.
 template <int D, int TW, bool kFull, bool kFullNext>
-__device__ __forceinline__ void score_block(AttnLds<D>& lds, int blk, int ks, int ps, int slot0,
+__device__ __forceinline__ void score_block(AttnLds<D>& lds, int blk, const uint16_t* kslot, int ps, int slot0,
                                             ScoreState<D, TW>& S, const VisCtx& vc, const int (&ml)[TW], float c,
                                             int lane, float (&mx_next)[TW]) {
   constexpr int DS = D / 32;
   const int lr = lane & 15, kg = lane >> 4;
-  v4u kf[DS];
+  v4u kf0[DS], kf1[DS];
 #pragma unroll
-  for (int s = 0; s < DS; ++s) kf[s] = *reinterpret_cast<const v4u*>(&lds.k[ks][lr][32 * s + 8 * kg]);
+  for (int s = 0; s < DS; ++s) {
+    kf0[s] = k_frag<D>(kslot, lr, s, kg);
+    kf1[s] = k_frag<D>(kslot, 16 + lr, s, kg);
+  }
 #pragma unroll
   for (int j = 0; j < TW; ++j) {
     // A stored row sees a visible key in its first block, so m_run is finite there.
@@ -320,20 +345,13 @@ __device__ __forceinline__ void score_block(AttnLds<D>& lds, int blk, int ks, in
     S.l_part[j] += ((pr[0] + pr[1]) + (pr[2] + pr[3])) + ((pr[4] + pr[5]) + (pr[6] + pr[7]));
     lds.p[ps][slot0 + kPairs * j][lane] = v4u{pack_bf16(pr[0], pr[1]), pack_bf16(pr[2], pr[3]),
                                               pack_bf16(pr[4], pr[5]), pack_bf16(pr[6], pr[7])};
-    v4f n0 = v4f{0.f, 0.f, 0.f, 0.f};
+    v4f n0 = v4f{0.f, 0.f, 0.f, 0.f}, n1 = v4f{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int s = 0; s < DS; ++s) n0 = mfma_bf16(kf[s], S.qf[j][s], n0);
+    for (int s = 0; s < DS; ++s) {
+      n0 = mfma_bf16(kf0[s], S.qf[j][s], n0);
+      n1 = mfma_bf16(kf1[s], S.qf[j][s], n1);
+    }
     S.s0[j] = n0;
-  }
-  // Keep the second half's fragment loads below the first half (register pressure).
-  __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-  for (int s = 0; s < DS; ++s) kf[s] = *reinterpret_cast<const v4u*>(&lds.k[ks][16 + lr][32 * s + 8 * kg]);
-#pragma unroll
-  for (int j = 0; j < TW; ++j) {
-    v4f n1 = v4f{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int s = 0; s < DS; ++s) n1 = mfma_bf16(kf[s], S.qf[j][s], n1);
     S.s1[j] = n1;
   }
   // The next block's maxima (none when this is the last block: its scores are stale).
@@ -349,7 +367,10 @@ template <int D, int TW>
 __global__ __launch_bounds__(kAttnThreads) void tree_attention_kernel(AttnArgs p) {
   constexpr int DS = D / 32;
   constexpr int DT = D / 16;
+  constexpr int kBlkLoads = D / 64;  // loads per wave and block (C / 8)
   __shared__ AttnLds<D> lds;
+  __shared__ __attribute__((aligned(16))) uint16_t k_ring[kRing][kKB * D];
+  __shared__ __attribute__((aligned(16))) uint16_t v_ring[kRing][kKB * D];
 
   // Workgroup -> (sequence, key/value head, row group).  Consecutive workgroups go to
   // different XCDs; the remap puts the row groups of one (sequence, head) on one XCD, so
@@ -369,6 +390,7 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attention_kernel(AttnArgs p
   const bool scorer = w < kPairs;
   const int lane = t % kWave;
   const int lr = lane & 15, kg = lane >> 4;
+  const int wr = w % kPairs;          // wave index within its role
   const int ts = t - kStageThreads;  // staging thread index of the output waves
 
   const int P = min(max(p.prefix_len[b], 0), static_cast<int>(p.Pmax));
@@ -416,19 +438,23 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attention_kernel(AttnArgs p
     }
     const VisCtx vc{P, npb, nn, kg};
     if (lane == 0) lds.rescale[0][pair] = 0u;
-    // Staging of the odd steps: step s stores K block s + 2 and V block s + 1, loaded two
-    // steps earlier, and loads K block s + 4 and V block s + 3 (the output waves do the
-    // same on the even steps).
-    StageK<D> sk;
-    StageV sv;
+    // The score waves load V: block X goes to ring slot X % 4 at step X - 3 (blocks 0..2
+    // before the first step); the output waves transpose it at step X.  Past the last
+    // block the loads repeat it into free slots, so every step issues the same count.
     const int last = max(nblk - 1, 0);
+    const uint32_t row_bytes = static_cast<uint32_t>(p.Hkv) * D * 2;
+    const DmaLanes<D, true> dl(row_bytes, wr, lane);
+    auto load_v_block = [&](int x) {
+      dl.load(p, block_src(p, min(x, last), npb, P, nn), row_bytes, v_ring[x % kRing], b, h);
+    };
     if (nblk > 0) {
-      load_k<D>(p, sk, block_src(p, min(3, last), npb, P, nn), b, h, t);
-      load_v<D>(p, sv, block_src(p, min(2, last), npb, P, nn), b, h, t);
+      load_v_block(0);
+      load_v_block(1);
+      load_v_block(2);
     }
-    __syncthreads();  // K blocks 0 and 1, V block 0 and the mask rows are in
+    ring_barrier<2 * kBlkLoads>();  // V block 0 and the mask rows are in; K blocks 0 and 1 too
     if (nblk > 0) {
-      block_scores<D, TW>(lds, 0, S, lr, kg);
+      block_scores<D, TW>(k_ring[0], S, lr, kg);
       // A row with a query sees a key of its first block (key 0 of the context, or the
       // root), so its maximum is finite; rows with no query keep 0 and never rescale.
 #pragma unroll
@@ -439,22 +465,17 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attention_kernel(AttnArgs p
         S.m_run[j] = ml[j] >= 0 ? m : 0.f;
       }
     }
-    __syncthreads();  // K slot 0 is refilled during the first step
+    ring_barrier<2 * kBlkLoads>();  // K slot 0 is refilled during the first step
     // One step per block; the last step's "next" scores come from a stale K slot and are
     // never used.  The rescale found on the next block's scores goes to the output wave
-    // with it.
+    // with it.  Before its barrier a step waits for V block blk + 1.
     auto step = [&](auto full, auto full_next, int blk) {
-      if (blk & 1) {
-        if (blk + 2 < nblk) store_k<D>(lds, blk & 1, sk, block_src(p, blk + 2, npb, P, nn), t);
-        if (blk + 1 < nblk) store_v<D>(lds, (blk + 1) % 3, sv, block_src(p, blk + 1, npb, P, nn), t);
-        load_k<D>(p, sk, block_src(p, min(blk + 4, last), npb, P, nn), b, h, t);
-        load_v<D>(p, sv, block_src(p, min(blk + 3, last), npb, P, nn), b, h, t);
-      }
+      if (nblk > 0) load_v_block(blk + 3);
       float mx[TW];
-      score_block<D, TW, decltype(full)::value, decltype(full_next)::value>(lds, blk, (blk + 1) & 1, blk & 1, pair,
-                                                                           S, vc, ml, c, lane, mx);
+      score_block<D, TW, decltype(full)::value, decltype(full_next)::value>(lds, blk, k_ring[(blk + 1) % kRing],
+                                                                           blk & 1, pair, S, vc, ml, c, lane, mx);
       raise_max<D, TW>(lds, (blk + 1) % 3, pair, lane, S, mx);
-      __syncthreads();
+      ring_barrier<2 * kBlkLoads>();
     };
     // Blocks 0 .. nf - 1 lie wholly inside the context; each loop below runs one variant.
     const int nf = P / kKB;
@@ -462,7 +483,7 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attention_kernel(AttnArgs p
     for (; blk + 1 < nf; ++blk) step(BoolTag<true>{}, BoolTag<true>{}, blk);
     if (blk < nf) step(BoolTag<true>{}, BoolTag<false>{}, blk++);
     for (; blk < nblk; ++blk) step(BoolTag<false>{}, BoolTag<false>{}, blk);
-    __syncthreads();  // the output wave's last block
+    ring_barrier<0>();  // the output wave's last block; no load of this wave is left
     // Final maximum and sum per query for the output wave.
 #pragma unroll
     for (int j = 0; j < TW; ++j) {
@@ -473,7 +494,7 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attention_kernel(AttnArgs p
         lds.fin_l[pair + kPairs * j][lr] = l;
       }
     }
-    __syncthreads();
+    ring_barrier<0>();
   } else {
     // ---------------- output wave ----------------
     v4f o[TW][DT];
@@ -481,40 +502,28 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attention_kernel(AttnArgs p
     for (int j = 0; j < TW; ++j)
 #pragma unroll
       for (int i = 0; i < DT; ++i) o[j][i] = v4f{0.f, 0.f, 0.f, 0.f};
-    // Staging of the even steps: step s stores K block s + 2 and V block s + 1, loaded two
-    // steps earlier, then loads K block s + 4 and V block s + 3, so two steps cover their
-    // latency (the score waves stage the odd steps).
-    StageK<D> sk;
-    StageV sv;
+    // The output waves load K: block X goes to ring slot X % 4 at step X - 4 (blocks 0..3
+    // before the first step), and the score waves read it at step X - 1.  Past the last
+    // block the loads repeat it into free slots, so every step issues the same count.
     const int last = max(nblk - 1, 0);
+    const uint32_t row_bytes = static_cast<uint32_t>(p.Hkv) * D * 2;
+    const DmaLanes<D, false> dl(row_bytes, wr, lane);
+    auto load_k_block = [&](int x) {
+      dl.load(p, block_src(p, min(x, last), npb, P, nn), row_bytes, k_ring[x % kRing], b, h);
+    };
     if (nblk > 0) {
-      const BlockSrc b0 = block_src(p, 0, npb, P, nn);
-      load_k<D>(p, sk, b0, b, h, ts);
-      load_v<D>(p, sv, b0, b, h, ts);
-      store_k<D>(lds, 0, sk, b0, ts);
-      store_v<D>(lds, 0, sv, b0, ts);
-      if (nblk > 1) {
-        const BlockSrc b1 = block_src(p, 1, npb, P, nn);
-        load_k<D>(p, sk, b1, b, h, ts);
-        store_k<D>(lds, 1, sk, b1, ts);
-      }
-      // The first step stores K block 2 and V block 1.
-      load_k<D>(p, sk, block_src(p, min(2, last), npb, P, nn), b, h, ts);
-      load_v<D>(p, sv, block_src(p, min(1, last), npb, P, nn), b, h, ts);
+      load_k_block(0);
+      load_k_block(1);
+      load_k_block(2);
+      load_k_block(3);
     }
-    __syncthreads();  // K blocks 0 and 1, V block 0 and the mask rows are in
-    __syncthreads();  // the score waves have read K slot 0
+    ring_barrier<2 * kBlkLoads>();  // K blocks 0 and 1 are in
+    ring_barrier<2 * kBlkLoads>();  // the score waves have read K slot 0
     for (int blk = 0; blk <= nblk; ++blk) {
-      // K block blk + 2 replaces block blk (read by the score waves in the previous step),
-      // V block blk + 1 replaces block blk - 2 (read here in the previous step).
-      if (!(blk & 1)) {
-        if (blk + 2 < nblk) store_k<D>(lds, blk & 1, sk, block_src(p, blk + 2, npb, P, nn), ts);
-        if (blk + 1 < nblk) store_v<D>(lds, (blk + 1) % 3, sv, block_src(p, blk + 1, npb, P, nn), ts);
-        if (blk < nblk) {  // clamped; unused past the end
-          load_k<D>(p, sk, block_src(p, min(blk + 4, last), npb, P, nn), b, h, ts);
-          load_v<D>(p, sv, block_src(p, min(blk + 3, last), npb, P, nn), b, h, ts);
-        }
-      }
+      if (nblk > 0) load_k_block(blk + 4);  // into the slot of block blk, read in the previous step
+      // V^T of block blk (from its ring slot, in since the previous step's barrier) into
+      // the slot of block blk - 3, read here three steps ago.
+      if (blk < nblk) transpose_v<D>(lds, blk % 3, v_ring[blk % kRing], ts);
       if (blk > 0) {
         // O^T += V^T P^T for block blk - 1, after the rescale its scores asked for.
         const int qb = blk - 1, ps = qb & 1, vs = qb % 3;
@@ -539,9 +548,9 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attention_kernel(AttnArgs p
           for (int j = 0; j < TW; ++j) o[j][i] = mfma_bf16(a, pt[j], o[j][i]);
         }
       }
-      __syncthreads();
+      ring_barrier<2 * kBlkLoads>();  // K block blk + 2 is in
     }
-    __syncthreads();  // the final statistics are in
+    ring_barrier<0>();  // the final statistics are in; no load of this wave is left
     // ---- normalise and store: lane (lr, kg) holds d = 16 i + 4 kg + e of its query ----
 #pragma unroll
     for (int j = 0; j < TW; ++j) {
