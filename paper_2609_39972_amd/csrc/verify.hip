@@ -312,7 +312,7 @@ __device__ __forceinline__ void raise_max(AttnLds<D>& lds, int as, int pair, int
 
 // A score wave's step on block blk.  Tile by tile: the weights from the tile's scores,
 // written to LDS for the output wave, then the next block's scores (K ring slot `kslot`)
-// into the same registers.  Ends with the next block's maxima.
+// into the same registers, and the next block's maxima one tile behind.
 // kFull: every key of the block is visible to every query; kFullNext: the same for the
 // next block.
 template <int D, int TW, bool kFull, bool kFullNext>
@@ -321,6 +321,13 @@ __device__ __forceinline__ void score_block(AttnLds<D>& lds, int blk, const uint
                                             int lane, float (&mx_next)[TW]) {
   constexpr int DS = D / 32;
   const int lr = lane & 15, kg = lane >> 4;
+  // The next block's maximum of tile j (none when this is the last block: its scores are
+  // stale).
+  const bool has_next = blk + 1 < vc.npb + (vc.nn + kKB - 1) / kKB;
+  auto next_max = [&](int j) {
+    const uint32_t vis = kFullNext ? 0xFFu : (has_next ? tile_vis<D>(lds, vc, blk + 1, ml[j]) : 0u);
+    return tile_max<kFullNext>(S.s0[j], S.s1[j], vis, c);
+  };
   v4u kf0[DS], kf1[DS];
 #pragma unroll
   for (int s = 0; s < DS; ++s) {
@@ -353,14 +360,11 @@ __device__ __forceinline__ void score_block(AttnLds<D>& lds, int blk, const uint
     }
     S.s0[j] = n0;
     S.s1[j] = n1;
+    // The previous tile's next-block maximum, once its MFMAs have had this tile's vector
+    // work to finish behind.
+    if (j > 0) mx_next[j - 1] = next_max(j - 1);
   }
-  // The next block's maxima (none when this is the last block: its scores are stale).
-#pragma unroll
-  for (int j = 0; j < TW; ++j) {
-    const uint32_t vis = kFullNext ? 0xFFu : (blk + 1 < vc.npb + (vc.nn + kKB - 1) / kKB
-                                                  ? tile_vis<D>(lds, vc, blk + 1, ml[j]) : 0u);
-    mx_next[j] = tile_max<kFullNext>(S.s0[j], S.s1[j], vis, c);
-  }
+  mx_next[TW - 1] = next_max(TW - 1);
 }
 
 template <int D, int TW>
