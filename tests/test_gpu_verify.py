@@ -79,6 +79,8 @@ def _check_attention(out, lse, ref, ref_lse, d, bf16_out: bool, seqs=None):
     (3, 33, 16, 2, 64, 70, (70, 1, 32), (33, 1, 20)),  # group of 8, a root-only tree
     (1, 1, 4, 4, 128, 0, (0,), (1,)),                 # root only, no context at all
     (2, 256, 4, 1, 128, 31, (31, 5), (256, 200)),      # largest tree: 8 mask words
+    (1, 129, 8, 2, 128, 64, (64,), (129,)),           # 516 query rows per head: two row groups
+    (2, 256, 16, 4, 64, 40, (40, 7), (256, 100)),      # 1024 rows per head: four groups, partial tree
 ])
 @pytest.mark.parametrize("out_dtype", ["f32", "bf16"])
 def test_tree_attention_small(B, N, H, Hkv, D, Pmax, plen, nn, out_dtype):
