@@ -28,6 +28,7 @@ namespace ubt {
 namespace {
 
 constexpr int kPipeRing = 4;
+constexpr int kFinishSurv = 256;  // survivors the finish ranks by counting (else the general path)
 constexpr int kPipeStageLive = kFastMaxW + 16;             // up to W live entries + 16 zero entries
 constexpr int kPipeStageCap = kPipeStageLive + kWave;      // + one dummy slot per lane
 
@@ -48,7 +49,7 @@ __host__ __device__ inline PipeSearchLayout pipe_search_layout(uint32_t base, in
   L.stage_ready = take(static_cast<size_t>(gamma) * sizeof(uint32_t));
   L.rank_ready = take(static_cast<size_t>(gamma) * sizeof(uint32_t));
   L.fbuf = take((kWave + 16) * sizeof(uint2));    // stage entries (+16 zero entries) for ranking
-  L.misc = take(4 * sizeof(uint32_t));            // the supertree's node count
+  L.misc = take(4 * sizeof(uint32_t));            // the supertree's node count, the finish's survivor count
   L.total = p;
   return L;
 }
@@ -59,7 +60,7 @@ struct PipeSearchSmem {
   uint32_t* stage_ready;  // [gamma]
   uint32_t* rank_ready;   // [gamma]
   uint2* fbuf;            // [80]: F_d's (~true index, key) in stage order, then 16 zero entries
-  uint32_t* misc;         // [4]: the supertree's node count (pruner -> every wave)
+  uint32_t* misc;         // [4]: the supertree's node count (pruner -> every wave), the finish's survivors
 };
 
 __device__ __forceinline__ PipeSearchSmem pipe_search_smem(unsigned char* raw, const PipeSearchLayout& L) {
@@ -276,64 +277,132 @@ __device__ __forceinline__ void pipe_prune_wave(const TreeArgs& a, const FastSme
 }
 
 // Global pruning (Eq. ubtree-pruning), emission and the mask, by every wave of the
-// workgroup once the pruner has stored the whole supertree: wave 0 selects Top_budget
-// (prune_supertree); the emission ranks are counted chunk by chunk, each 16-entry chunk
-// of the selection scanned by one wave for every selected entry (LDS adds combine the
-// counts); node writes and the mask's rows (each a walk up the parent slots) are spread
-// over all threads.  Every wave of the workgroup must call it.
+// workgroup once the pruner has stored the whole supertree.  The entries at or above a
+// lower bound of the budget-th key (the survivors) are ranked by counting, one thread
+// per survivor: rank < budget selects Top_budget and is the emission order at once.
+// Node writes and the mask's rows (each a walk up the parent slots) are spread over all
+// threads.  Every wave of the workgroup must call it.
 template <int KT>
 __device__ __forceinline__ void finish_tree_coop(const TreeArgs& a, const FastSmem& sm, const PipeSearchSmem& ps,
                                                  int64_t b, int w, int nw, int lane, uint64_t magic_w) {
   const int gamma = a.gamma, W = a.W, budget = a.budget;
   const int GW = gamma * W;
   const int tid = static_cast<int>(threadIdx.x), nthreads = static_cast<int>(blockDim.x);
-  // kPipeRing * 64 >= 256 counters over the rank ring, which is free once every wave has
-  // arrived (the pruner writes it up to its last depth).
-  int32_t* erank = ps.rank;
+  // The rank ring and the children's transpose buffer are free once every wave has
+  // arrived (the pruner writes the ring up to its last depth).
+  uint32_t* n_surv = ps.misc + 1;                            // the survivor count
+  int32_t* srank = reinterpret_cast<int32_t*>(sm.xpose);     // rank of each staged entry
+  if (tid == 0) *n_surv = 0u;                                // only the finish uses misc[1]
   __syncthreads();
-  for (int i = tid; i < kPipeRing * kWave; i += nthreads) erank[i] = 0;
   const int total = static_cast<int>(ps.misc[0]);
   const int n_sel = total < budget ? total : budget;
-  if (w == 0) {
-    if (GW <= 4 * kWave)
-      prune_supertree<4>(sm, GW, total, n_sel, lane);
-    else if (GW <= 8 * kWave)
-      prune_supertree<8>(sm, GW, total, n_sel, lane);
-    else
-      prune_supertree<16>(sm, GW, total, n_sel, lane);
-  }
-  __syncthreads();
-  // Emission rank = the number of selected entries before it under (score desc, depth
-  // asc, rank asc); entries n_sel .. n_sel + 15 of the stage are zero.
-  const int nrows = (n_sel + kWave - 1) / kWave;  // <= 4
-  uint64_t mine[4];
-#pragma unroll
-  for (int rb = 0; rb < 4; ++rb) {
-    const int i = rb * kWave + lane;
-    const uint2 st = sm.stage[i < n_sel ? i : 0];
-    mine[rb] = i < n_sel ? order_value(st.x, st.y) : ~0ull;
-  }
-  const uint4* s4 = reinterpret_cast<const uint4*>(sm.stage);
-  for (int ch = w; ch < (n_sel + 15) / 16; ch += nw) {
-    uint4 v[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) v[i] = s4[ch * 8 + i];
-#pragma unroll
-    for (int rb = 0; rb < 4; ++rb) {
-      if (rb < nrows) {
-        int c0 = 0, c1 = 0;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          c0 += order_value(v[i].x, v[i].y) > mine[rb] ? 1 : 0;
-          c1 += order_value(v[i].z, v[i].w) > mine[rb] ? 1 : 0;
-        }
-        const int cnt = c0 + c1;
-        if (rb * kWave + lane < n_sel && cnt) atomicAdd(&erank[rb * kWave + lane], cnt);
-      }
+  // A lower bound of the n_sel-th largest key: the smallest key of the shallowest depths
+  // that hold n_sel entries together (depth d holds w_d = min(w_{d-1} K, W) of them).
+  int fcut = 0;
+  {
+    int np = 1, cum = 0;
+    for (int d = 1; d <= gamma && cum < n_sel; ++d) {
+      const int n = np * KT;
+      np = n < W ? n : W;
+      cum += np;
+      fcut = d * W;
     }
   }
+  // Every wave takes the bound itself (a few dozen keys), so no barrier is needed before
+  // the survivors are staged.
+  uint32_t lo = ~0u;
+  for (int f = lane; f < fcut; f += kWave) {
+    const uint32_t k = sm.s_key[f];
+    lo = k != 0u ? min(lo, k) : lo;
+  }
+  const uint32_t bound = wave_umin(lo);
+  // The survivors (keys at or above the bound) hold Top_budget; they are staged as
+  // (~flat index, key) in any order.
+  for (int f0 = 0; f0 < GW; f0 += nthreads) {
+    const int f = f0 + tid;
+    const uint32_t k = f < GW ? sm.s_key[f] : 0u;
+    const bool in = k != 0u && k >= bound;
+    const uint64_t m = ballot(in);
+    uint32_t at = 0u;
+    if (lane == 0 && m != 0ull)
+      at = atomicAdd(n_surv, static_cast<uint32_t>(popc(m)));
+    const int pos = static_cast<int>(__builtin_amdgcn_readlane(at, 0)) + static_cast<int>(lanes_below(m));
+    if (in && pos < kFinishSurv) sm.stage[pos] = make_uint2(~static_cast<uint32_t>(f), k);
+  }
   __syncthreads();
-  for (int i = tid; i < n_sel; i += nthreads) sm.f_slot[~sm.stage[i].x] = 1 + erank[i];
+  int n_stage = static_cast<int>(*n_surv);
+  if (n_stage <= kFinishSurv) {
+    // Rank of each survivor under (score desc, depth asc, rank asc): the selection is
+    // rank < n_sel, and the rank is its emission order.
+    // Four lanes per survivor, lane q of the quad counting the pairs j = 2 q, 2 q + 8, ...
+    // (two entries per 16-byte load).
+    const uint4* s4 = reinterpret_cast<const uint4*>(sm.stage);
+    const int q = tid & 3;
+    for (int i0 = tid >> 2; i0 < n_stage; i0 += nthreads >> 2) {  // the same for a quad's lanes
+      const uint2 me = sm.stage[i0];
+      const uint64_t mv = order_value(me.x, me.y);
+      int a0 = 0, a1 = 0;
+#pragma unroll 4
+      for (int j = 2 * q; j < n_stage; j += 8) {
+        const uint4 o = s4[j >> 1];
+        a0 += order_value(o.x, o.y) > mv ? 1 : 0;
+        a1 += (j + 1 < n_stage && order_value(o.z, o.w) > mv) ? 1 : 0;
+      }
+      const int ahead = quad_sum(a0 + a1);
+      if (q == 0) {
+        srank[i0] = ahead;
+        if (ahead < n_sel) sm.f_slot[~me.x] = 1 + ahead;
+      }
+    }
+  } else {
+    // Many equal keys at the bound: wave 0 selects Top_budget (prune_supertree), then the
+    // emission ranks are counted chunk by chunk, each 16-entry chunk of the selection
+    // scanned by one wave for every selected entry (LDS adds combine the counts).
+    int32_t* erank = ps.rank;
+    for (int i = tid; i < kPipeRing * kWave; i += nthreads) erank[i] = 0;
+    if (w == 0) {
+      if (GW <= 4 * kWave)
+        prune_supertree<4>(sm, GW, total, n_sel, lane);
+      else if (GW <= 8 * kWave)
+        prune_supertree<8>(sm, GW, total, n_sel, lane);
+      else
+        prune_supertree<16>(sm, GW, total, n_sel, lane);
+    }
+    __syncthreads();
+    const int nrows = (n_sel + kWave - 1) / kWave;  // <= 4
+    uint64_t mine[4];
+#pragma unroll
+    for (int rb = 0; rb < 4; ++rb) {
+      const int i = rb * kWave + lane;
+      const uint2 st = sm.stage[i < n_sel ? i : 0];
+      mine[rb] = i < n_sel ? order_value(st.x, st.y) : ~0ull;
+    }
+    const uint4* s4 = reinterpret_cast<const uint4*>(sm.stage);
+    for (int ch = w; ch < (n_sel + 15) / 16; ch += nw) {
+      uint4 v[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] = s4[ch * 8 + i];
+#pragma unroll
+      for (int rb = 0; rb < 4; ++rb) {
+        if (rb < nrows) {
+          int c0 = 0, c1 = 0;
+#pragma unroll
+          for (int i = 0; i < 8; ++i) {
+            c0 += order_value(v[i].x, v[i].y) > mine[rb] ? 1 : 0;
+            c1 += order_value(v[i].z, v[i].w) > mine[rb] ? 1 : 0;
+          }
+          const int cnt = c0 + c1;
+          if (rb * kWave + lane < n_sel && cnt) atomicAdd(&erank[rb * kWave + lane], cnt);
+        }
+      }
+    }
+    __syncthreads();
+    for (int i = tid; i < n_sel; i += nthreads) {
+      srank[i] = erank[i];
+      sm.f_slot[~sm.stage[i].x] = 1 + erank[i];
+    }
+    n_stage = n_sel;
+  }
   __syncthreads();
   const int N = budget + 1;
   const int words = (N + 31) / 32;
@@ -358,7 +427,8 @@ __device__ __forceinline__ void finish_tree_coop(const TreeArgs& a, const FastSm
     scr[0] = 0.f;
     sm.anc[0] = -1;
   }
-  for (int i = tid; i < n_sel; i += nthreads) {
+  for (int i = tid; i < n_stage; i += nthreads) {
+    if (srank[i] >= n_sel) continue;
     const uint2 st = sm.stage[i];
     const int f = static_cast<int>(~st.x);
     const int d = div_k(f, magic_w) + 1;
@@ -366,7 +436,7 @@ __device__ __forceinline__ void finish_tree_coop(const TreeArgs& a, const FastSm
     const int p = static_cast<int>(info & 0xFFFFu);
     const int c = static_cast<int>(info >> 16);
     const int ps_ = d == 1 ? 0 : sm.f_slot[(d - 2) * W + p];
-    const int slot = 1 + erank[i];
+    const int slot = 1 + srank[i];
     tok[slot] = sm.cids[(d - 1) * KT + c];
     par[slot] = ps_;
     dep[slot] = d;
@@ -383,8 +453,8 @@ __device__ __forceinline__ void finish_tree_coop(const TreeArgs& a, const FastSm
   }
   __syncthreads();
   if (a.mask) {
-    // Row n: the node and its ancestors, by walking the parent slots (a chain of at
-    // most gamma + 1 nodes; parents precede children, so every step decreases).
+    // Row n: the node and its ancestors, by walking the parent slots (a chain of at most
+    // gamma + 1 nodes; parents precede children, so every step decreases).
     uint32_t* mrow = a.mask + b * static_cast<int64_t>(N) * words;
     for (int nn = tid; nn < N; nn += nthreads) {
       uint32_t wv[kMaskWords] = {0, 0, 0, 0, 0, 0, 0, 0};
