@@ -51,6 +51,112 @@ __device__ __forceinline__ void split_gated(u32x4 g, u32x4 p, u32x4& hi, u32x4& 
   }
 }
 
+// Table rows of the tile's operands: pred[t] is the predecessor of A-operand row
+// a = 16 t + (lane & 15) (x_0 alone at i = 0), succ[t] the successor of B-operand column
+// c = 16 t + (lane & 15); -1 past K (those operands are zero).
+template <int KT>
+__device__ __forceinline__ void tile_ids(int64_t V, int i, int K, const int32_t* anchor, const int32_t* pred_ids,
+                                         const int32_t* succ_ids, int lane, int64_t (&pred)[KT],
+                                         int64_t (&succ)[KT]) {
+  const int lr = lane & 15;
+#pragma unroll
+  for (int t = 0; t < KT; ++t) {
+    const int a = 16 * t + lr;
+    pred[t] = (i == 0) ? (a == 0 ? clamp_id(*anchor, V) : -1) : (a < K ? clamp_id(pred_ids[a], V) : -1);
+    succ[t] = a < K ? clamp_id(succ_ids[a], V) : -1;
+  }
+}
+
+// Operands of the 32-wide k-step starting at k = kb: lane group kg = lane >> 4 holds
+// slots kb + 8 kg .. kb + 8 kg + 7 of the gate, of each predecessor row and of each
+// successor row (zero past r and past K).
+template <int KT>
+__device__ __forceinline__ void load_step(const uint16_t* __restrict__ phi, const uint16_t* __restrict__ psi,
+                                          const uint16_t* g_row, int r, int kb, const int64_t (&pred)[KT],
+                                          const int64_t (&succ)[KT], int lane, u32x4& gq, u32x4 (&pq)[KT],
+                                          u32x4 (&sq)[KT]) {
+  const u32x4 zero = u32x4{0u, 0u, 0u, 0u};
+  const int k0 = kb + 8 * (lane >> 4);
+  const bool in = k0 < r;
+  gq = in ? *reinterpret_cast<const u32x4*>(g_row + k0) : zero;
+#pragma unroll
+  for (int t = 0; t < KT; ++t) {
+    pq[t] = (in && pred[t] >= 0) ? *reinterpret_cast<const u32x4*>(phi + pred[t] * r + k0) : zero;
+    sq[t] = (in && succ[t] >= 0) ? *reinterpret_cast<const u32x4*>(psi + succ[t] * r + k0) : zero;
+  }
+}
+
+// One k-step of every output tile: acc[mt][nt] += (hi + lo)(g phi)[rows of mt] psi[cols of nt]^T.
+template <int KT>
+__device__ __forceinline__ void mfma_step(u32x4 gq, const u32x4 (&pq)[KT], const u32x4 (&sq)[KT],
+                                          f32x4 (&acc)[KT][KT]) {
+  u32x4 ahi[KT], alo[KT];
+#pragma unroll
+  for (int t = 0; t < KT; ++t) split_gated(gq, pq[t], ahi[t], alo[t]);
+#pragma unroll
+  for (int mt = 0; mt < KT; ++mt)
+#pragma unroll
+    for (int nt = 0; nt < KT; ++nt) {
+      acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(ahi[mt]), as_bf16x8(sq[nt]), acc[mt][nt], 0, 0, 0);
+      acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(alo[mt]), as_bf16x8(sq[nt]), acc[mt][nt], 0, 0, 0);
+    }
+}
+
+// Unigram terms al * succ_logit[c] for the successor column c = 16 nt + (lane & 15) of
+// each output tile column (0 past K).
+template <int KT>
+__device__ __forceinline__ void succ_terms(const float* succ_logit, float al, int K, int lane, float (&au)[KT]) {
+#pragma unroll
+  for (int nt = 0; nt < KT; ++nt) {
+    const int c = 16 * nt + (lane & 15);
+    au[nt] = c < K ? al * succ_logit[c] : 0.f;
+  }
+}
+
+// Epilogue of one row of output tiles: accr[nt][j] = delta(a, c) with a = 16 mt + 4 kg + j,
+// c = 16 nt + (lane & 15), kg = lane >> 4.  Forms s = al u + la delta and, with
+// kNormalise, the log-softmax over the K successors of each row (a row lives in one
+// aligned group of 16 lanes), then writes rows a < K.
+template <int KT, bool kNormalise>
+__device__ __forceinline__ void tile_rows_out(const f32x4 (&accr)[KT], int mt, int i, int K, const float (&au)[KT],
+                                              float la, float* dslab, float* qslab, float* qslab2, int lane) {
+  const int lr = lane & 15, kg = lane >> 4;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int a = 16 * mt + 4 * kg + j;
+    float s[KT];
+    float m = neg_inf();
+#pragma unroll
+    for (int nt = 0; nt < KT; ++nt) {
+      const int c = 16 * nt + lr;
+      s[nt] = c < K ? fmaf(la, accr[nt][j], au[nt]) : neg_inf();
+      m = fmaxf(m, s[nt]);
+    }
+    float norm = 0.f;
+    if (kNormalise) {
+      m = group16_max(m);
+      float e = 0.f;
+#pragma unroll
+      for (int nt = 0; nt < KT; ++nt) e += __builtin_amdgcn_exp2f((s[nt] - m) * kLog2e);
+      e = group16_sum(e);
+      norm = m + __builtin_amdgcn_logf(e) * kLn2;
+    }
+    const bool real = (i == 0) ? a == 0 : a < K;
+    if (a < K) {
+#pragma unroll
+      for (int nt = 0; nt < KT; ++nt) {
+        const int c = 16 * nt + lr;
+        if (c < K) {
+          const float q = real ? (kNormalise ? fminf(s[nt] - norm, 0.f) : s[nt]) : 0.f;
+          if (dslab) dslab[a * K + c] = real ? accr[nt][j] : 0.f;
+          qslab[a * K + c] = q;
+          if (qslab2) qslab2[a * K + c] = q;
+        }
+      }
+    }
+  }
+}
+
 // Scores of position i (depth i + 1) of one sequence.  anchor points at x_0 (read at
 // i = 0 only); pred_ids = C_{i-1} (read at i > 0 only); succ_ids / succ_logit = C_i and
 // its logits; g_row = P(h_i).  Writes delta (if dslab) and log q^bi to qslab and, if
@@ -64,17 +170,8 @@ __device__ __forceinline__ void bigram_tile_bf16(const uint16_t* __restrict__ ph
                                                  const int32_t* anchor, const int32_t* pred_ids,
                                                  const int32_t* succ_ids, const float* succ_logit, float al,
                                                  float la, float* dslab, float* qslab, float* qslab2, int lane) {
-  const int lr = lane & 15;  // operand row (A) / column (B) inside a tile
-  const int kg = lane >> 4;  // k-slice group: slots 8*kg .. 8*kg+7 of each 32-wide step
-
   int64_t pred[KT], succ[KT];
-#pragma unroll
-  for (int t = 0; t < KT; ++t) {
-    const int a = 16 * t + lr;
-    pred[t] = (i == 0) ? (a == 0 ? clamp_id(*anchor, V) : -1) : (a < K ? clamp_id(pred_ids[a], V) : -1);
-    const int c = 16 * t + lr;
-    succ[t] = c < K ? clamp_id(succ_ids[c], V) : -1;
-  }
+  tile_ids<KT>(V, i, K, anchor, pred_ids, succ_ids, lane, pred, succ);
 
   f32x4 acc[KT][KT];
 #pragma unroll
@@ -85,81 +182,21 @@ __device__ __forceinline__ void bigram_tile_bf16(const uint16_t* __restrict__ ph
   // The k range is walked in 32-wide steps, ceil(r / 32) of them, in order; the operands
   // of kSteps consecutive steps are gathered together so their loads overlap.
   constexpr int kSteps = 4;
-  const u32x4 zero = u32x4{0u, 0u, 0u, 0u};
   for (int kb = 0; kb < r; kb += 32 * kSteps) {
     u32x4 gq[kSteps], pq[kSteps][KT], sq[kSteps][KT];
 #pragma unroll
-    for (int st = 0; st < kSteps; ++st) {
-      const int k0 = kb + 32 * st + 8 * kg;
-      const bool in = k0 < r;
-      gq[st] = in ? *reinterpret_cast<const u32x4*>(g_row + k0) : zero;
-#pragma unroll
-      for (int t = 0; t < KT; ++t) {
-        pq[st][t] = (in && pred[t] >= 0) ? *reinterpret_cast<const u32x4*>(phi + pred[t] * r + k0) : zero;
-        sq[st][t] = (in && succ[t] >= 0) ? *reinterpret_cast<const u32x4*>(psi + succ[t] * r + k0) : zero;
-      }
-    }
+    for (int st = 0; st < kSteps; ++st) load_step<KT>(phi, psi, g_row, r, kb + 32 * st, pred, succ, lane, gq[st], pq[st], sq[st]);
 #pragma unroll
     for (int st = 0; st < kSteps; ++st) {
       if (kb + 32 * st >= r) break;  // wave-uniform: no step past ceil(r / 32)
-      u32x4 ahi[KT], alo[KT];
-#pragma unroll
-      for (int t = 0; t < KT; ++t) split_gated(gq[st], pq[st][t], ahi[t], alo[t]);
-#pragma unroll
-      for (int mt = 0; mt < KT; ++mt)
-#pragma unroll
-        for (int nt = 0; nt < KT; ++nt) {
-          acc[mt][nt] =
-              __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(ahi[mt]), as_bf16x8(sq[st][nt]), acc[mt][nt], 0, 0, 0);
-          acc[mt][nt] =
-              __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(alo[mt]), as_bf16x8(sq[st][nt]), acc[mt][nt], 0, 0, 0);
-        }
+      mfma_step<KT>(gq[st], pq[st], sq[st], acc);
     }
   }
 
-  // Epilogue.  acc[mt][nt][j] = delta(a, c) with a = 16 mt + 4 kg + j, c = 16 nt + lr.
   float au[KT];
+  succ_terms<KT>(succ_logit, al, K, lane, au);
 #pragma unroll
-  for (int nt = 0; nt < KT; ++nt) {
-    const int c = 16 * nt + lr;
-    au[nt] = c < K ? al * succ_logit[c] : 0.f;
-  }
-#pragma unroll
-  for (int mt = 0; mt < KT; ++mt)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int a = 16 * mt + 4 * kg + j;
-      float s[KT];
-      float m = neg_inf();
-#pragma unroll
-      for (int nt = 0; nt < KT; ++nt) {
-        const int c = 16 * nt + lr;
-        s[nt] = c < K ? fmaf(la, acc[mt][nt][j], au[nt]) : neg_inf();
-        m = fmaxf(m, s[nt]);
-      }
-      float norm = 0.f;
-      if (kNormalise) {
-        m = group16_max(m);
-        float e = 0.f;
-#pragma unroll
-        for (int nt = 0; nt < KT; ++nt) e += __builtin_amdgcn_exp2f((s[nt] - m) * kLog2e);
-        e = group16_sum(e);
-        norm = m + __builtin_amdgcn_logf(e) * kLn2;
-      }
-      const bool real = (i == 0) ? a == 0 : a < K;
-      if (a < K) {
-#pragma unroll
-        for (int nt = 0; nt < KT; ++nt) {
-          const int c = 16 * nt + lr;
-          if (c < K) {
-            const float q = real ? (kNormalise ? fminf(s[nt] - norm, 0.f) : s[nt]) : 0.f;
-            if (dslab) dslab[a * K + c] = real ? acc[mt][nt][j] : 0.f;
-            qslab[a * K + c] = q;
-            if (qslab2) qslab2[a * K + c] = q;
-          }
-        }
-      }
-    }
+  for (int mt = 0; mt < KT; ++mt) tile_rows_out<KT, kNormalise>(acc[mt], mt, i, K, au, la, dslab, qslab, qslab2, lane);
 }
 
 }  // namespace ubt

@@ -48,6 +48,9 @@ def _run(phi, psi, gate, ids, logit, anchor, alpha, lam):
 CASES = [  # B, gamma, K, V, r
     (2, 3, 1, 50, 16), (3, 5, 4, 300, 32), (2, 4, 8, 1000, 64), (2, 15, 8, 5000, 128), (2, 6, 16, 3000, 128),
     (1, 4, 17, 500, 48), (1, 3, 32, 800, 256), (1, 3, 33, 800, 80), (1, 2, 64, 2000, 512), (4, 31, 16, 2000, 256),
+    # K > 16 splits each position's contraction over K/16 waves: the paper's shape (K = 64, r = 256),
+    # fewer k-steps than waves (r = 48), a half last step (r = 208), and rows past K in the last tile row
+    (2, 15, 64, 5000, 256), (2, 5, 40, 3000, 48), (1, 3, 24, 700, 208), (2, 4, 49, 1500, 144),
 ]
 
 
