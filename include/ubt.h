@@ -264,7 +264,17 @@ ubt_status_t ubt_draft_tree(const void* phi_tab, const void* psi_tab, const void
  * affected sequences are written with n_nodes = 0, the call's outputs are unspecified,
  * and the workspace must be zero-filled again before the next call (a late chunk may
  * still raise a counter).  A missing, short or misaligned workspace returns
- * UBT_ERR_WORKSPACE.  Other shapes run the two calls' kernels in order on `stream` and
+ * UBT_ERR_WORKSPACE.
+ *
+ * With K = 64 (bf16 features, the four-wave search of ubt_draft_tree: W <= 16, B <= 64
+ * and below the compute-unit count) the step is TWO launches: the sweep of ubt_topk, then
+ * the selector and the search together, one workgroup per sequence searching while the
+ * score slabs are computed by other workgroups in depth order; a search waits for each
+ * slab (two depths ahead) on a ready word that the slab's workgroup sets once its
+ * agent-scope stores have completed.  The ready words are the workspace's row counters
+ * (from byte 256, one per row; the same zero-fill, reset, error-word and bounded-wait
+ * rules as above).  A missing, short or misaligned workspace here runs the separate
+ * kernels instead.  Other shapes run the two calls' kernels in order on `stream` and
  * ignore the workspace.
  * ------------------------------------------------------------------------------------ */
 size_t ubt_draft_step_workspace_bytes(int B, int gamma, int64_t V, int K, ubt_dtype_t dt);
@@ -293,8 +303,9 @@ ubt_status_t ubt_draft_step(const void* logits, ubt_dtype_t dt, int B, int gamma
  * one left behind.  Calls that overlap on one device share that array and race: issue
  * them on one stream (or otherwise order them).  A sequence whose bounded wait ran out
  * of time (a stalled device) is written with n_nodes = 0.  A shape whose workspace would
- * exceed the array returns UBT_ERR_WORKSPACE (the one-launch shapes never do); shapes the
- * one launch does not take run the separate kernels, which need no workspace.
+ * exceed the array returns UBT_ERR_WORKSPACE (the one-launch shapes never do); the K = 64
+ * selector + search launch keeps its ready words in the same array (cleared the same
+ * way); other shapes run the separate kernels, which need no workspace.
  * ------------------------------------------------------------------------------------ */
 ubt_status_t ubt_draft_step_noalloc(const void* logits, ubt_dtype_t dt, int B, int gamma,
                                     int64_t V, int64_t stride_b, int64_t stride_i, int K,

@@ -231,10 +231,32 @@ ubt_status_t draft_step_impl(const void* logits, ubt_dtype_t dt, int B, int gamm
   a.logq = logq;
   const int64_t es = dt == UBT_BF16 ? 2 : 4;
   const bool aligned = aligned16(logits) && (stride_b * es) % 16 == 0 && (stride_i * es) % 16 == 0;
+  ubt::SelectorArgs s;
+  s.phi = static_cast<const uint16_t*>(phi_tab);
+  s.psi = static_cast<const uint16_t*>(psi_tab);
+  s.gate = static_cast<const uint16_t*>(gate);
+  s.V = V;
+  s.r = r;
+  s.cand_logit = cand_logit;
+  s.logq = logq;
+  s.sc = sc;
   if (!ubt::draft_step_fused(static_cast<int>(dt), aligned, B, gamma, V, K, static_cast<int>(feat_dt), W)) {
     st = hip_status(ubt::launch_topk(logits, static_cast<int>(dt), aligned, B, gamma, V, stride_b, stride_i, K,
                                      cand_ids, cand_logit, cand_logprob, lse, stream));
     if (st != UBT_OK) return st;
+    // K = 64: the selector and the search in one launch when a workspace is at hand.
+    if (ubt::draft_step_k64(static_cast<int>(feat_dt), B, gamma, K, W)) {
+      const size_t need = ubt::step_k64_workspace_bytes(B, gamma);
+      if (use_static && need <= ubt::step_static_scratch_bytes()) {
+        st = hip_status(ubt::step_static_scratch(&workspace));
+        if (st != UBT_OK) return st;
+        st = hip_status(ubt::clear_step_flags(workspace, B, gamma, stream));
+        if (st != UBT_OK) return st;
+        return hip_status(ubt::launch_draft_step_k64(s, a, workspace, stream));
+      }
+      if (!use_static && workspace && (reinterpret_cast<uintptr_t>(workspace) & 255u) == 0 && workspace_bytes >= need)
+        return hip_status(ubt::launch_draft_step_k64(s, a, workspace, stream));
+    }
     return ubt_draft_tree(phi_tab, psi_tab, gate, feat_dt, V, r, anchor, cand_ids, cand_logit, alpha, lambda, B,
                           gamma, K, W, budget, zeta, logq, n_nodes, token, parent, depth, cand_rank, score, mask,
                           stream);
@@ -251,15 +273,6 @@ ubt_status_t draft_step_impl(const void* logits, ubt_dtype_t dt, int B, int gamm
   } else if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0 || workspace_bytes < need) {
     return UBT_ERR_WORKSPACE;
   }
-  ubt::SelectorArgs s;
-  s.phi = static_cast<const uint16_t*>(phi_tab);
-  s.psi = static_cast<const uint16_t*>(psi_tab);
-  s.gate = static_cast<const uint16_t*>(gate);
-  s.V = V;
-  s.r = r;
-  s.cand_logit = cand_logit;
-  s.logq = logq;
-  s.sc = sc;
   return hip_status(ubt::launch_draft_step(logits, static_cast<int>(dt), B, gamma, V, stride_b, stride_i, K, cand_ids,
                                            cand_logit, cand_logprob, lse, s, a, workspace, stream));
 }

@@ -16,11 +16,12 @@
 // the waves split the r-contraction between them (wave w takes the 32-wide k-steps
 // w, w + KT, ...), so each gathers a fraction of the rows' slots and all of its loads are
 // in flight at once; the partial tiles then meet in LDS, each wave sums its own tile row
-// over the waves in wave order and runs that row's epilogue.  The gate is folded into the predecessor operand: g_k * phi_k(a) is exact in
-// fp32 (two 8-bit significands) and is split into hi + lo bf16 parts, so the two MFMAs
-// form every product g_k phi_k(a) psi_k(b) exactly and only the fp32 accumulation
-// rounds.  The row log-softmax runs on the accumulator tile: a row of the tile lives in
-// one aligned group of 16 lanes.  fp32 features use fp32 FMAs on the vector ALUs.
+// over the waves in wave order and runs that row's epilogue (bigram_split_tile).  The
+// gate is folded into the predecessor operand: g_k * phi_k(a) is exact in fp32 (two 8-bit
+// significands) and is split into hi + lo bf16 parts, so the two MFMAs form every product
+// g_k phi_k(a) psi_k(b) exactly and only the fp32 accumulation rounds.  The row
+// log-softmax runs on the accumulator tile: a row of the tile lives in one aligned group
+// of 16 lanes.  fp32 features use fp32 FMAs on the vector ALUs.
 #include "bigram_tile.h"
 #include "ubt_launch.h"
 
@@ -50,70 +51,16 @@ __global__ __launch_bounds__(KT * kWave) __attribute__((amdgpu_waves_per_eu(2)))
     int r, const int32_t* __restrict__ anchor, const int32_t* __restrict__ cand_ids,
     const float* __restrict__ cand_logit, Scales sc, int gamma, int K, float* __restrict__ delta,
     float* __restrict__ logq) {
-  // part[v][s][nt]: wave v's partial of tile (mt, nt) for the s-th tile row mt != v.
-  __shared__ f32x4 part[KT][KT - 1][KT][kWave];
+  __shared__ f32x4 part[kSplitPartBytes<KT> / sizeof(f32x4)];
   const int lane = static_cast<int>(threadIdx.x) & (kWave - 1);
   const int w = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) / kWave);
   const int64_t bi = blockIdx.x;  // b * gamma + i
   const int i = static_cast<int>(bi % gamma);
   const int64_t b = bi / gamma;
-
-  int64_t pred[KT], succ[KT];
-  tile_ids<KT>(V, i, K, anchor + b, i > 0 ? cand_ids + (bi - 1) * K : cand_ids, cand_ids + bi * K, lane, pred, succ);
-  f32x4 acc[KT][KT];
-#pragma unroll
-  for (int mt = 0; mt < KT; ++mt)
-#pragma unroll
-    for (int nt = 0; nt < KT; ++nt) acc[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  // This wave's k-steps w, w + KT, ..., kSteps of them gathered together.
-  const uint16_t* g_row = gate + bi * r;
-  const int n_steps = (r + 31) / 32;
-  constexpr int kSteps = 2;
-  for (int s0 = w; s0 < n_steps; s0 += KT * kSteps) {
-    u32x4 gq[kSteps], pq[kSteps][KT], sq[kSteps][KT];
-#pragma unroll
-    for (int st = 0; st < kSteps; ++st)
-      load_step<KT>(phi, psi, g_row, r, 32 * (s0 + KT * st), pred, succ, lane, gq[st], pq[st], sq[st]);
-#pragma unroll
-    for (int st = 0; st < kSteps; ++st) {
-      if (s0 + KT * st >= n_steps) break;  // wave-uniform
-      mfma_step<KT>(gq[st], pq[st], sq[st], acc);
-    }
-  }
-
-  // Hand over the tile rows the other waves finish; keep this wave's own row.
-  f32x4 own[KT];
-#pragma unroll
-  for (int mt = 0; mt < KT; ++mt) {
-    if (mt == w) {
-#pragma unroll
-      for (int nt = 0; nt < KT; ++nt) own[nt] = acc[mt][nt];
-    } else {
-#pragma unroll
-      for (int nt = 0; nt < KT; ++nt) part[w][mt < w ? mt : mt - 1][nt][lane] = acc[mt][nt];
-    }
-  }
-  __syncthreads();
-  f32x4 row[KT];
-#pragma unroll
-  for (int nt = 0; nt < KT; ++nt) row[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int v = 0; v < KT; ++v) {
-    if (v == w) {
-#pragma unroll
-      for (int nt = 0; nt < KT; ++nt) row[nt] += own[nt];
-    } else {
-      const int slot = w < v ? w : w - 1;
-#pragma unroll
-      for (int nt = 0; nt < KT; ++nt) row[nt] += part[v][slot][nt][lane];
-    }
-  }
-
-  float au[KT];
-  succ_terms<KT>(cand_logit + bi * K, sc.alpha[i], K, lane, au);
-  tile_rows_out<KT, kNormalise>(row, w, i, K, au, sc.lambda[i], delta ? delta + bi * K * K : nullptr,
-                                logq + bi * K * K, nullptr, lane);
+  bigram_split_tile<KT, kNormalise>(phi, psi, gate + bi * r, V, r, i, K, anchor + b,
+                                    i > 0 ? cand_ids + (bi - 1) * K : cand_ids, cand_ids + bi * K, cand_logit + bi * K,
+                                    sc.alpha[i], sc.lambda[i], delta ? delta + bi * K * K : nullptr, logq + bi * K * K,
+                                    part, w, lane);
 }
 
 __global__ __launch_bounds__(kWave) void bigram_f32_kernel(const float* __restrict__ phi, const float* __restrict__ psi,

@@ -117,7 +117,9 @@ __device__ __forceinline__ void succ_terms(const float* succ_logit, float al, in
 // c = 16 nt + (lane & 15), kg = lane >> 4.  Forms s = al u + la delta and, with
 // kNormalise, the log-softmax over the K successors of each row (a row lives in one
 // aligned group of 16 lanes), then writes rows a < K.
-template <int KT, bool kNormalise>
+// kCoherent: qslab is written with agent-scope stores, which reach the device-coherent
+// level, for a reader in another workgroup of the same launch.
+template <int KT, bool kNormalise, bool kCoherent = false>
 __device__ __forceinline__ void tile_rows_out(const f32x4 (&accr)[KT], int mt, int i, int K, const float (&au)[KT],
                                               float la, float* dslab, float* qslab, float* qslab2, int lane) {
   const int lr = lane & 15, kg = lane >> 4;
@@ -149,7 +151,11 @@ __device__ __forceinline__ void tile_rows_out(const f32x4 (&accr)[KT], int mt, i
         if (c < K) {
           const float q = real ? (kNormalise ? fminf(s[nt] - norm, 0.f) : s[nt]) : 0.f;
           if (dslab) dslab[a * K + c] = real ? accr[nt][j] : 0.f;
-          qslab[a * K + c] = q;
+          if constexpr (kCoherent)
+            __hip_atomic_store(reinterpret_cast<uint32_t*>(qslab + a * K + c), __float_as_uint(q), __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+          else
+            qslab[a * K + c] = q;
           if (qslab2) qslab2[a * K + c] = q;
         }
       }
@@ -197,6 +203,82 @@ __device__ __forceinline__ void bigram_tile_bf16(const uint16_t* __restrict__ ph
   succ_terms<KT>(succ_logit, al, K, lane, au);
 #pragma unroll
   for (int mt = 0; mt < KT; ++mt) tile_rows_out<KT, kNormalise>(acc[mt], mt, i, K, au, la, dslab, qslab, qslab2, lane);
+}
+
+// K > 16: the same scores on KT waves of one workgroup, one wave per row of output tiles.
+// The waves split the r-contraction between them (wave w takes the 32-wide k-steps
+// w, w + KT, ...), so each gathers a fraction of every row and all of its loads are in
+// flight at once; the partial tiles then meet in `part` (workgroup LDS of
+// kSplitPartBytes<KT> bytes), and wave w sums tile row w over the waves in wave order and
+// runs that row's epilogue.  All KT waves of the workgroup must call it (it holds one
+// workgroup barrier); w is the caller's wave index.
+template <int KT>
+constexpr size_t kSplitPartBytes = static_cast<size_t>(KT) * (KT - 1) * KT * kWave * sizeof(f32x4);
+
+template <int KT, bool kNormalise, bool kCoherent = false>
+__device__ __forceinline__ void bigram_split_tile(const uint16_t* __restrict__ phi, const uint16_t* __restrict__ psi,
+                                                  const uint16_t* g_row, int64_t V, int r, int i, int K,
+                                                  const int32_t* anchor, const int32_t* pred_ids,
+                                                  const int32_t* succ_ids, const float* succ_logit, float al,
+                                                  float la, float* dslab, float* qslab, f32x4* part, int w,
+                                                  int lane) {
+  // part[((v (KT - 1) + s) KT + nt) 64 + lane]: wave v's partial of tile (mt, nt) for the
+  // s-th tile row mt != v.
+  int64_t pred[KT], succ[KT];
+  tile_ids<KT>(V, i, K, anchor, pred_ids, succ_ids, lane, pred, succ);
+  f32x4 acc[KT][KT];
+#pragma unroll
+  for (int mt = 0; mt < KT; ++mt)
+#pragma unroll
+    for (int nt = 0; nt < KT; ++nt) acc[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // This wave's k-steps w, w + KT, ..., kSteps of them gathered together.
+  const int n_steps = (r + 31) / 32;
+  constexpr int kSteps = 2;
+  for (int s0 = w; s0 < n_steps; s0 += KT * kSteps) {
+    u32x4 gq[kSteps], pq[kSteps][KT], sq[kSteps][KT];
+#pragma unroll
+    for (int st = 0; st < kSteps; ++st)
+      load_step<KT>(phi, psi, g_row, r, 32 * (s0 + KT * st), pred, succ, lane, gq[st], pq[st], sq[st]);
+#pragma unroll
+    for (int st = 0; st < kSteps; ++st) {
+      if (s0 + KT * st >= n_steps) break;  // wave-uniform
+      mfma_step<KT>(gq[st], pq[st], sq[st], acc);
+    }
+  }
+
+  // Hand over the tile rows the other waves finish; keep this wave's own row.
+  f32x4 own[KT];
+#pragma unroll
+  for (int mt = 0; mt < KT; ++mt) {
+    if (mt == w) {
+#pragma unroll
+      for (int nt = 0; nt < KT; ++nt) own[nt] = acc[mt][nt];
+    } else {
+      const int slot = mt < w ? mt : mt - 1;
+#pragma unroll
+      for (int nt = 0; nt < KT; ++nt) part[((w * (KT - 1) + slot) * KT + nt) * kWave + lane] = acc[mt][nt];
+    }
+  }
+  __syncthreads();
+  f32x4 row[KT];
+#pragma unroll
+  for (int nt = 0; nt < KT; ++nt) row[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int v = 0; v < KT; ++v) {
+    if (v == w) {
+#pragma unroll
+      for (int nt = 0; nt < KT; ++nt) row[nt] += own[nt];
+    } else {
+      const int slot = w < v ? w : w - 1;
+#pragma unroll
+      for (int nt = 0; nt < KT; ++nt) row[nt] += part[((v * (KT - 1) + slot) * KT + nt) * kWave + lane];
+    }
+  }
+
+  float au[KT];
+  succ_terms<KT>(succ_logit, al, K, lane, au);
+  tile_rows_out<KT, kNormalise, kCoherent>(row, w, i, K, au, la, dslab, qslab, nullptr, lane);
 }
 
 }  // namespace ubt

@@ -299,6 +299,32 @@ __device__ __forceinline__ bool wait_slab(const FastSmem& sm, int i, uint64_t t0
   return wait_flag(&sm.ready[i], sm.fail, t0);
 }
 
+// Relaxed agent-scope accesses: they go to and come from the device-coherent level, so a
+// workgroup on another XCD (with its own L2) sees them.
+__device__ __forceinline__ uint32_t agent_load_u32(const uint32_t* p) {
+  return __hip_atomic_load(const_cast<uint32_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void agent_store_u32(uint32_t* p, uint32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Waits until the agent-scope word *f, set by another workgroup of the same launch, is
+// nonzero.  The wave's later loads are issued only after this load has returned (the loop
+// exits on its value).  Returns false if the wait ran out of time; the workgroup's fail
+// word is then set.
+__device__ __forceinline__ bool wait_agent_word(const uint32_t* f, uint32_t* fail, uint64_t t0) {
+  for (;;) {
+    if (__builtin_amdgcn_readfirstlane(agent_load_u32(f)) != 0u) break;
+    if (__builtin_amdgcn_s_memrealtime() - t0 > kWaitTicks) {
+      __hip_atomic_store(fail, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+      return false;
+    }
+    __builtin_amdgcn_s_sleep(2);
+  }
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);  // no load is moved above the wait
+  return true;
+}
+
 // Ancestor mask of a tree whose slots 0..n_nodes-1 are in `anc` (anc[n] = parent slot,
 // anc[0] = -1), by pointer jumping: after round k, a node's mask covers it and its
 // 2^k - 1 nearest ancestors and `up` points 2^k steps up; a chain of at most
@@ -507,9 +533,16 @@ __device__ __forceinline__ void expand_depths(const TreeArgs& a, const FastSmem&
 // ranked.  All waves return with the same `total`.
 constexpr int kK64Waves = 4;
 
-template <int RW, bool vec>
+//
+// kWait: the slabs are written by other workgroups of the same launch.  Before loading the
+// slab of depth d a wave waits for ready[d - 1] (an agent-scope word its producer sets
+// once the slab's agent-scope stores have completed), then loads it with agent-scope
+// loads; a wait that runs out of time sets the workgroup's fail word.  t0: the wave's
+// start time.
+template <int RW, bool vec, bool kWait = false>
 __device__ __forceinline__ void expand_depths64(const TreeArgs& a, const FastSmem& sm, int64_t b, int w, int lane,
-                                                int& total) {
+                                                int& total, const uint32_t* ready = nullptr, uint64_t t0 = 0) {
+  static_assert(!(kWait && vec), "waited slabs are loaded word by word");
   constexpr int KT = 64;
   constexpr int kQuarter = KT * KT / kK64Waves;  // floats of a slab staged by one wave
   const int gamma = a.gamma, W = a.W;
@@ -517,7 +550,12 @@ __device__ __forceinline__ void expand_depths64(const TreeArgs& a, const FastSme
   float P[kQuarter / kWave];  // this wave's quarter of a slab, in flight
   auto load_slab = [&](int d) {  // slab of depth d (1-based)
     const float* src = gq + static_cast<int64_t>(d - 1) * KT * KT;
-    if constexpr (vec) {
+    if constexpr (kWait) {
+      wait_agent_word(ready + (d - 1), sm.fail, t0);
+      const uint32_t* u = reinterpret_cast<const uint32_t*>(src);
+#pragma unroll
+      for (int i = 0; i < kQuarter / kWave; ++i) P[i] = __uint_as_float(agent_load_u32(u + i * kWave + lane));
+    } else if constexpr (vec) {
 #pragma unroll
       for (int i = 0; i < kQuarter / (4 * kWave); ++i) {
         const float4 t = reinterpret_cast<const float4*>(src)[i * kWave + lane];

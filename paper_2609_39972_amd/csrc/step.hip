@@ -377,6 +377,23 @@ bool draft_step_fused(int dtype, bool aligned, int B, int gamma, int64_t V, int 
   return cus > 0 && B < cus;
 }
 
+bool draft_step_k64(int feat_dtype, int B, int gamma, int K, int W) {
+  if (B > kMaxStepSequences || !draft_tree_k64_fused(feat_dtype, gamma, K, W)) return false;
+  const int cus = compute_units();
+  return cus > 0 && B < cus;
+}
+
+size_t step_k64_workspace_bytes(int B, int gamma) {
+  return kCountBase + align256(static_cast<size_t>(B) * gamma * sizeof(uint32_t));
+}
+
+hipError_t launch_draft_step_k64(const SelectorArgs& s, const TreeArgs& a, void* workspace, hipStream_t stream) {
+  char* ws = static_cast<char*>(workspace);
+  TreeArgs ta = a;
+  ta.err = reinterpret_cast<uint32_t*>(ws);  // a search that ran out of time sets the error word
+  return launch_draft_tree_k64(s, ta, reinterpret_cast<uint32_t*>(ws + kCountBase), stream);
+}
+
 hipError_t launch_draft_step(const void* logits, int dtype, int B, int gamma, int64_t V, int64_t stride_b,
                              int64_t stride_i, int K, int32_t* cand_ids, float* cand_logit, float* cand_logprob,
                              float* lse, const SelectorArgs& s, const TreeArgs& a, void* workspace,

@@ -378,6 +378,67 @@ __global__ __launch_bounds__(kK64Waves* kWave) void build_tree_k64_kernel(TreeAr
   finish_tree<64, false>(a, sm, b, lane, magic_w, total);
 }
 
+// K = 64: selector scores and tree search in one launch (the one-call draft step).
+// Workgroups 0..B-1 search, one per sequence, as build_tree_k64_kernel does.  The other
+// workgroups compute score slab t (position t / B of sequence t % B, depth-major, so the
+// first positions' slabs come first) on four waves (bigram_split_tile), write it with
+// agent-scope stores, wait until they have completed and set the slab's ready word.  A
+// search wave waits for a slab's ready word before loading it, two depths ahead, so the
+// search starts once its first two slabs exist and overlaps the rest of the selector.  Slab workgroups never wait; a search wait that runs out of time marks
+// its sequence with n_nodes = 0 and sets the error word.  The searcher clears the ready
+// words of its sequence at the end, so the next call starts from zero.
+//
+// The slab workgroups are persistent: slab_wgs of them take the slabs t, t + slab_wgs, ...
+// in depth-major order.  One four-wave slab takes about 7 us from dispatch to its ready
+// word even on an idle device (ids 0.4, row gathers 2.2, the hi/lo split and MFMAs 1.3,
+// the LDS reduction 0.6, the epilogue and its stores 1.4 us), so the search starts about
+// 7 us in however many run at once.  Measured at B = 32, gamma = 15, W = 12, r = 256 (us
+// per step with the sweep): 32 slab workgroups 141.7, 64 97.9, 128 79.0, 256 78.7, one
+// per slab (480) 79.4.
+constexpr int kK64SlabRound = 8;  // slab workgroups per sequence
+
+template <int RW>
+__global__ __launch_bounds__(kK64Waves* kWave) __attribute__((amdgpu_waves_per_eu(2))) void draft_tree_k64_kernel(
+    TreeArgs a, SelectorArgs s, uint32_t* ready, int slab_wgs, uint64_t magic_w) {
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  const int w = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) / kWave);
+  const int lane = static_cast<int>(threadIdx.x) % kWave;
+  const int gamma = a.gamma;
+  if (static_cast<int>(blockIdx.x) < a.B) {
+    const int64_t b = blockIdx.x;
+    const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+    const FastSmem sm = fast_smem(smem_raw, fast_layout(gamma, 64, a.W));
+    const int32_t* gids = a.cand_ids + b * gamma * 64;
+    for (int e = static_cast<int>(threadIdx.x); e < gamma * 64; e += static_cast<int>(blockDim.x))
+      sm.cids[e] = gids[e];
+    if (threadIdx.x == 0) *sm.fail = 0u;
+    __syncthreads();
+    int total = 0;
+    expand_depths64<RW, false, true>(a, sm, b, w, lane, total, ready + b * gamma, t0);
+    // Every wave has passed every wait (each depth ends with a workgroup barrier).
+    if (w == 0 && lane < gamma) agent_store_u32(ready + b * gamma + lane, 0u);
+    if (w != 0) return;
+    finish_tree<64, true>(a, sm, b, lane, magic_w, total);
+    return;
+  }
+  for (int t = static_cast<int>(blockIdx.x) - a.B; t < a.B * gamma; t += slab_wgs) {
+    const int i = t / a.B;
+    const int64_t b = t - i * a.B;
+    const int64_t bi = b * gamma + i;
+    bigram_split_tile<4, true, true>(s.phi, s.psi, s.gate + bi * s.r, s.V, s.r, i, 64, a.anchor + b,
+                                     i > 0 ? a.cand_ids + (bi - 1) * 64 : a.cand_ids, a.cand_ids + bi * 64,
+                                     s.cand_logit + bi * 64, s.sc.alpha[i], s.sc.lambda[i], nullptr,
+                                     s.logq + bi * 64 * 64, reinterpret_cast<f32x4*>(smem_raw), w, lane);
+    // Each wave's slab stores have completed before the workgroup barrier (which also
+    // ends this slab's reads of the partial tiles); then the word.
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_waitcnt(0);
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __syncthreads();
+    if (threadIdx.x == 0) agent_store_u32(ready + bi, 1u);
+  }
+}
+
 // Selector scores and tree search in one launch, one workgroup per sequence.  Wave 0
 // computes the score slab of position 0 and starts searching; the other waves compute
 // positions 1, 2, ... (round-robin) and publish each slab as it lands in LDS, and the
@@ -569,6 +630,36 @@ hipError_t launch_draft_tree(const SelectorArgs& s, const TreeArgs& a, hipStream
     UBT_DRAFT_ROWS(16);
 #undef UBT_DRAFT_ROWS
 #undef UBT_DRAFT_LAUNCH
+  return hipGetLastError();
+}
+
+bool draft_tree_k64_fused(int feat_dtype, int gamma, int K, int W) {
+  return feat_dtype == 1 && K == 64 && fast_tree_fits(gamma, K, W);
+}
+
+hipError_t launch_draft_tree_k64(const SelectorArgs& s, const TreeArgs& a, uint32_t* ready, hipStream_t stream) {
+  const uint64_t magic_w = (0x100000000ull + a.W - 1) / a.W;
+  const size_t search_smem = fast_layout(a.gamma, 64, a.W).total;
+  const size_t slab_smem = kSplitPartBytes<4>;
+  const size_t smem = search_smem > slab_smem ? search_smem : slab_smem;
+  const int slabs = a.B * a.gamma;
+  const int slab_wgs = slabs < kK64SlabRound * a.B ? slabs : kK64SlabRound * a.B;
+  const dim3 grid(static_cast<unsigned>(a.B + slab_wgs)), block(kK64Waves * kWave);
+#define UBT_K64_DRAFT(RW)                                                                                    \
+  do {                                                                                                       \
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&draft_tree_k64_kernel<RW>),                     \
+                              hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(smem));           \
+    hipLaunchKernelGGL((draft_tree_k64_kernel<RW>), grid, block, smem, stream, a, s, ready, slab_wgs, magic_w); \
+  } while (0)
+  if (a.W <= 4)
+    UBT_K64_DRAFT(1);
+  else if (a.W <= 8)
+    UBT_K64_DRAFT(2);
+  else if (a.W <= 12)
+    UBT_K64_DRAFT(3);
+  else
+    UBT_K64_DRAFT(4);
+#undef UBT_K64_DRAFT
   return hipGetLastError();
 }
 

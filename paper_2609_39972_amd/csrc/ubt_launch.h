@@ -70,6 +70,11 @@ struct SelectorArgs {
 // True if the one-launch kernel handles the shape (bf16 features and the register-
 // resident search: K in {4, 8, 16}, W <= 64, W*K <= 512, gamma*W <= 1024).
 bool draft_tree_fused(int feat_dtype, int gamma, int K, int W);
+// True if draft_tree_k64_kernel handles the shape (bf16 features, K = 64 and the
+// four-wave search: W*64 <= 1024, W <= 64, gamma*W <= 1024).
+bool draft_tree_k64_fused(int feat_dtype, int gamma, int K, int W);
+// Selector scores and the K = 64 search in one launch; ready: B*gamma zero words, left zero.
+hipError_t launch_draft_tree_k64(const SelectorArgs& s, const TreeArgs& a, uint32_t* ready, hipStream_t stream);
 hipError_t launch_draft_tree(const SelectorArgs& s, const TreeArgs& a, hipStream_t stream);
 
 // ---- the whole step: depth-major chunked sweep beside per-sequence searchers ----------
@@ -92,6 +97,14 @@ size_t step_static_scratch_bytes();
 hipError_t step_static_scratch(void** ptr);
 // Zero-fills the error word and the B * gamma row counters of a step workspace.
 hipError_t clear_step_flags(void* workspace, int B, int gamma, hipStream_t stream);
+// K = 64: the step is the sweep, then draft_tree_k64_kernel, whose slab ready words are
+// the workspace's row counters (the error word first, the words from byte 256).  True if
+// that launch takes the shape: bf16 features, K = 64, the four-wave search, B <=
+// kMaxStepSequences and fewer sequences than compute units (the searchers and the slab
+// workgroups are resident together).
+bool draft_step_k64(int feat_dtype, int B, int gamma, int K, int W);
+size_t step_k64_workspace_bytes(int B, int gamma);
+hipError_t launch_draft_step_k64(const SelectorArgs& s, const TreeArgs& a, void* workspace, hipStream_t stream);
 
 // ---- verification: tree attention, acceptance walk, KV commit -------------------------
 struct TreeAttnArgs {

@@ -212,6 +212,11 @@ def _custom(cfg: int, **kw) -> synth.Workload:
     dict(B=2, L=6, V=10000, K=16, W=32, budget=60),   # W * K = 512
     dict(B=2, L=6, V=10000, K=5, W=4, budget=20),     # K outside {4, 8, 16}: the separate calls
     dict(B=2, L=6, V=10001, K=8, W=4, budget=20),     # V * 2 bytes not a multiple of 16
+    # K = 64: the sweep, then the selector and the four-wave search in one launch
+    dict(B=2, L=7, V=6000, K=64, W=12, r=256, budget=64),   # the paper's search shape, fewer positions
+    dict(B=3, L=2, V=3000, K=64, W=4, r=64, budget=20),     # one position (no slab two depths ahead)
+    dict(B=2, L=17, V=5000, K=64, W=16, r=48, budget=120),  # W = 16, 16 positions, fewer k-steps than waves
+    dict(B=2, L=9, V=6000, K=64, W=16, r=32, budget=16),    # W = budget
 ])
 def test_step_shapes(kw):
     w = _custom(300, **kw)

@@ -57,3 +57,14 @@ def test_noalloc_separate_kernel_shape():
     w = synth.custom(501, B=2, L=6, V=10000, K=5, r=32, budget=20, W=4, dtype="bf16", feat_dtype="bf16",
                      logits="normal", logit_std=2.0)
     _both(w)
+
+
+def test_noalloc_k64_twice():
+    """K = 64 (the selector and the search in one launch, ready words in the static array):
+    the paper's shape at B = 32, then a smaller one."""
+    big = synth.WORKLOADS[6]
+    small = synth.custom(502, B=3, L=5, V=8000, K=64, r=64, budget=30, W=8, dtype="bf16", feat_dtype="bf16",
+                         logits="zipf")
+    a = _both(big)
+    b = _both(small)
+    assert a["n_nodes"].shape[0] == 32 and b["n_nodes"].shape[0] == 3
