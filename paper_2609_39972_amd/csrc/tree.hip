@@ -384,9 +384,10 @@ __global__ __launch_bounds__(kK64Waves* kWave) void build_tree_k64_kernel(TreeAr
 // first positions' slabs come first) on four waves (bigram_split_tile), write it with
 // agent-scope stores, wait until they have completed and set the slab's ready word.  A
 // search wave waits for a slab's ready word before loading it, two depths ahead, so the
-// search starts once its first two slabs exist and overlaps the rest of the selector.  Slab workgroups never wait; a search wait that runs out of time marks
-// its sequence with n_nodes = 0 and sets the error word.  The searcher clears the ready
-// words of its sequence at the end, so the next call starts from zero.
+// search starts once its first two slabs exist and overlaps the rest of the selector.
+// Slab workgroups never wait; a search wait that runs out of time marks its sequence
+// with n_nodes = 0 and sets the error word.  The searcher clears the ready words of its
+// sequence at the end (gamma <= 64, one lane each), so the next call starts from zero.
 //
 // The slab workgroups are persistent: slab_wgs of them take the slabs t, t + slab_wgs, ...
 // in depth-major order.  One four-wave slab takes about 7 us from dispatch to its ready
